@@ -1,0 +1,223 @@
+"""Throughput of the scheduled denoiser step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config llada] [--budget 35]
+
+A "step" is one network evaluation of the whole unit stack plus the sampler update,
+for the full batch of the workload (Alg. 2 + the update of Sec. 3.1).  Steps run in
+trajectory order 1..T and wrap to a fresh trajectory (cache reset) after step T, so K = T
+times one complete scheduled trajectory.  Inputs and weights are seeded synthetic data
+with the workload's shapes (planted power-law spectra), resident in HBM before timing.
+
+Prints one JSON line.  `value` is scheduled denoising steps/s at the headline budget; the
+all-active rate (every unit computing at every step, same launcher) and the other budgets
+are reported beside it.  `roofline` times the dominant kernel (the gated MLP input GEMM)
+with HIP events on the launch stream inside the timed region.  `cpu_baseline` times the
+CPU oracle on a bounded sample (a few units of an all-active step).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16 = 2.5e15      # dense MFMA bf16, FLOP/s
+PEAK_F32 = 157.3e12     # fp32 vector
+PEAK_HBM = 8.0e12       # bytes/s
+
+
+def log(msg: str) -> None:
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def unit_flops(cfg) -> dict:
+    """Algorithmic FLOP of one active unit, per GEMM / attention (2 M N K; 4 B H S_q S_k d_h)."""
+    M, d, F, H, dh, N, B = cfg.M, cfg.d, cfg.F, cfg.H, cfg.dh, cfg.N, cfg.B
+    f = {
+        "gemm_qkv": 2.0 * M * 3 * d * d,
+        "attn": 4.0 * B * H * N * N * dh,
+        "gemm_o": 2.0 * M * d * d,
+        "gemm_w1": 2.0 * M * (2 * F if cfg.gated else F) * d,
+        "gemm_w2": 2.0 * M * d * F,
+    }
+    if cfg.arch == "sdxl":
+        f["gemm_x"] = 2.0 * M * d * d * 2
+        f["attn_x"] = 4.0 * B * H * N * cfg.ctx_len * dh
+    return f
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=0, help="timed steps (default 2 T)")
+    ap.add_argument("--warmup", type=int, default=0, help="warm-up steps (default T)")
+    ap.add_argument("--config", default="llada")
+    ap.add_argument("--budget", type=int, default=0, help="headline budget in percent (default: smallest)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-units", type=int, default=2, help="oracle sample: units of one all-active step")
+    ap.add_argument("--profile-kernel", default="gemm_w1")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md, 'Sharding').",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2609_29505_amd as P
+
+    cfg = synth.get_config(args.config)
+    T, L = cfg.T, cfg.L
+    K = args.steps or 2 * T
+    W = args.warmup or T
+    budgets = sorted(cfg.budgets)
+    head = args.budget or budgets[0]
+    if head not in budgets:
+        budgets.append(head)
+
+    log(f"config {cfg.name}: B={cfg.B} N={cfg.N} d={cfg.d} F={cfg.F} L={L} T={T}; generating weights")
+    t0 = time.time()
+    cache_dir = os.environ.get("SGD_SYNTH_CACHE") or "/tmp/sgd_synth_cache"
+    weights = synth.model_weights(cfg, workers=min(16, os.cpu_count() or 1), cache_dir=cache_dir)
+    inputs = synth.inputs(cfg)
+    log(f"weights ready in {time.time() - t0:.1f}s; uploading")
+    torch.cuda.set_device(0)
+    dm = P.DeviceModel(cfg, weights, inputs)
+    torch.cuda.synchronize()
+    log(f"workspace {dm.workspace_bytes / 2**20:.0f} MiB, cache {dm.cache_bytes / 2**20:.0f} MiB; building schedules")
+
+    t0 = time.time()
+    scheds = {}
+    for pct in budgets:
+        n = P.budget_layer_steps(pct, L, T)
+        scheds[pct] = P.schedule_build(dm.scored_units(), [cfg.dh] * L, T, budget=n)
+        log(f"budget {pct}%: N*={n} lifetimes={list(scheds[pct].lifetimes)} margin={scheds[pct].cut_margin:.3g}")
+    log(f"schedules built in {time.time() - t0:.1f}s (offline, not timed)")
+    all_active = P.schedule_from_lifetimes([T] * L, T)
+
+    z0 = torch.from_numpy(inputs["z"]).cuda()
+    z = z0.clone()
+    cache = P.Cache(dm)
+    stream = torch.cuda.current_stream()
+
+    def run(sched, nsteps, start):
+        """Enqueue nsteps steps continuing a trajectory at step `start` (1-based)."""
+        s = start
+        for _ in range(nsteps):
+            if s == 1:
+                cache.reset()
+                z.copy_(z0)
+            dm.step(z, s, sched, cache)
+            s = s + 1 if s < T else 1
+        return s
+
+    def timed(sched, profile=None):
+        run(sched, W, 1)
+        torch.cuda.synchronize()
+        if profile:
+            dm.profile_begin(profile, 8192)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        run(sched, K, 1)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1)
+        prof = dm.profile_end() if profile else None
+        return ms, prof
+
+    results = {}
+    for pct in budgets:
+        ms, prof = timed(scheds[pct], args.profile_kernel if pct == head else None)
+        results[pct] = (ms, prof)
+        log(f"budget {pct}%: {K} steps in {ms:.2f} ms -> {K * 1000.0 / ms:.2f} steps/s")
+    ms_all, prof_all = timed(all_active, args.profile_kernel)
+    log(f"all-active: {K} steps in {ms_all:.2f} ms -> {K * 1000.0 / ms_all:.2f} steps/s")
+
+    ms_head, prof_head = results[head]
+    value = K * 1000.0 / ms_head
+    all_rate = K * 1000.0 / ms_all
+
+    # roofline of the dominant kernel, from the all-active run (largest launch count)
+    fl = unit_flops(cfg)
+    kern = args.profile_kernel
+    kms, kn = prof_all
+    kavg = kms / max(kn, 1) / 1000.0
+    peak = PEAK_BF16 if cfg.dtype == "bf16" else PEAK_F32
+    achieved = fl.get(kern, 0.0) / kavg if kavg > 0 else 0.0
+    roofline = {"bound": "mfma", "kernel": kern, "achieved": achieved / 1e12, "peak": peak / 1e12,
+                "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                "avg_launch_us": kavg * 1e6, "launches": kn,
+                "flop_per_launch": fl.get(kern, 0.0)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, weights, inputs, scheds[head], args.cpu_units)
+
+    lay = {pct: scheds[pct].layer_steps for pct in budgets}
+    line = {
+        "metric": "denoise steps/s scheduled vs all-active; MFMA % peak; LLaDA-8B shape",
+        "value": round(value, 3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(ms_head / K, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded planted-spectrum weights and inputs)",
+        "config": {"workload": f"{cfg.name}: B={cfg.B} N={cfg.N} d={cfg.d} H={cfg.H} F={cfg.F} L={L} T={T}",
+                   "budget_pct": head, "layer_steps": lay[head], "of": L * T,
+                   "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "single GPU"},
+        "all_active_steps_per_s": round(all_rate, 3),
+        "speedup_vs_all_active": round(value / all_rate, 4),
+        "skipped_layer_step_fraction": round(1 - lay[head] / (L * T), 4),
+        "budgets": {str(p): {"steps_per_s": round(K * 1000.0 / results[p][0], 3), "layer_steps": lay[p],
+                             "speedup": round((K * 1000.0 / results[p][0]) / all_rate, 4)} for p in budgets},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    dm.close()
+    return 0
+
+
+def cpu_baseline(cfg, weights, inputs, sched, n_units):
+    """Oracle (numpy float64) on a bounded sample: n_units units of an all-active step.
+
+    Scaled to steps/s of the scheduled trajectory: the oracle's time per step is its time per
+    active unit times the mean active units per step (frozen units cost an addition each).
+    """
+    import numpy as np
+    from oracle import model as om
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+    sub = [weights[l] for l in range(n_units)]
+    import dataclasses
+    small = dataclasses.replace(cfg, L=n_units)
+    log(f"cpu baseline: oracle on {n_units} units of an all-active step ({threads} threads)")
+    m = om.Model(small, sub, inputs)
+    h = om.initial_stream(m, inputs["z"], 1)
+    t0 = time.time()
+    for l in range(n_units):
+        h, _ = m.unit_active(l, h, om.timestep_value(1, cfg.T))
+    dt = time.time() - t0
+    per_unit = dt / n_units
+    mean_active = float(np.asarray(sched.active, np.float64).sum(axis=1).mean())
+    per_step = per_unit * mean_active
+    log(f"cpu baseline: {per_unit:.2f}s per active unit -> {per_step:.1f}s per scheduled step")
+    return {"value": round(1.0 / per_step, 6), "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_units} of {cfg.L} units of one all-active step at full size ({dt:.1f}s), "
+                      f"scaled by {mean_active:.2f} mean active units per scheduled step"}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,244 @@
+/*
+ * sgd.h -- C ABI of the scheduled denoiser step of Spectral-Guided Diffusion
+ * (static spectral layer scheduling) on AMD MI355X (gfx950).
+ *
+ * Two operations define the method:
+ *   - sgd_schedule_build: Alg. 1 (Sec. 4.1).  Every scheduled weight matrix
+ *     gets its regularised Spectral Concentration Ratio (Sec. 3.2, Eq.
+ *     scr-reg) and matrix score g(W) (appendix, Eq. app-matrix-score);
+ *     component scores (Eqs. app-attn-score, app-xattn-score, app-mlp-score)
+ *     sum to a unit score (Eq. app-block-score) that is normalised (Eq.
+ *     app-score-normalization) and mapped to an integer lifetime S_l by
+ *     Eq. schedule, either at a fixed tau or at an exact layer-step budget.
+ *   - sgd_denoise_step: Alg. 2 (Sec. 4.2) with the residual-update semantics
+ *     of Sec. 3.1.  Units with s <= S_l compute their residual branches and
+ *     refresh their cached update Delta_l; units with s > S_l only add the
+ *     cached Delta_l to the current residual stream.  Conditioning and
+ *     skip inputs keep propagating.  The step ends with the deterministic
+ *     update z <- alpha z - beta eps.
+ *
+ * Conventions
+ *   - Every function returns an int status: SGD_OK (0) or a negative SGD_E_*
+ *     code.  Nothing aborts or throws across the ABI.  sgd_last_error()
+ *     returns a thread-local description of the last failure.
+ *   - "Device pointer" means memory of the current HIP device.  The caller
+ *     owns every buffer (weights, state, cache, workspace); handles only
+ *     borrow pointers and never allocate or free device memory, with one
+ *     exception: sgd_schedule_build and sgd_matrix_stats allocate and free a
+ *     temporary fp64 Gram matrix (offline work).
+ *   - Weight matrices are row-major [out, in] (y = x W^T), dtype SGD_F32 or
+ *     SGD_BF16.  Norm gains/shifts, biases, class embeddings: fp32.
+ *   - Calls that take a hip_stream enqueue on it and return without a host
+ *     synchronisation unless documented otherwise.  All arguments are
+ *     validated before anything is enqueued: a failing call enqueues
+ *     nothing.  Kernel faults surface as SGD_E_HIP on a later call.
+ *   - Handles are not thread-safe; use one cache per concurrent trajectory.
+ */
+#ifndef SGD_H
+#define SGD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------------ status */
+#define SGD_OK 0
+#define SGD_E_ARG (-1)         /* null pointer, bad enum, inconsistent argument   */
+#define SGD_E_SHAPE (-2)       /* a size the kernels do not support              */
+#define SGD_E_DTYPE (-3)       /* unsupported dtype                              */
+#define SGD_E_BUDGET (-4)      /* N* < L*S_min or N* > L*T                       */
+#define SGD_E_STEP (-5)        /* step != previous step + 1, or outside 1..T     */
+#define SGD_E_CACHE (-6)       /* frozen unit whose cache slot was never written */
+#define SGD_E_HIP (-7)         /* HIP runtime error                              */
+#define SGD_E_NUMERIC (-8)     /* non-finite weights or scores                   */
+
+enum sgd_dtype { SGD_F32 = 0, SGD_BF16 = 1 };
+
+enum sgd_arch {
+    SGD_ARCH_TINY = 0,   /* RMSNorm, MHA (no bias, no RoPE), GELU(erf) MLP             */
+    SGD_ARCH_LLADA = 1,  /* RMSNorm, MHA with RoPE, SwiGLU MLP                          */
+    SGD_ARCH_DIT = 2,    /* LayerNorm + AdaLN shift/scale/gate, biased MHA, GELU(tanh)  */
+    SGD_ARCH_UVIT = 3,   /* LayerNorm, MHA, GELU(erf) MLP, long skips via a skip linear */
+    SGD_ARCH_SDXL = 4    /* LayerNorm, self-attn, cross-attn to a context, GEGLU MLP    */
+};
+
+/* Role of a scored matrix inside its unit (appendix "Exact Block-Level Scores"). */
+enum sgd_role {
+    SGD_ROLE_Q = 0, SGD_ROLE_K = 1, SGD_ROLE_V = 2, SGD_ROLE_O = 3,
+    SGD_ROLE_XQ = 4, SGD_ROLE_XK = 5, SGD_ROLE_XV = 6, SGD_ROLE_XO = 7,
+    SGD_ROLE_W1 = 8,   /* MLP input projection; gated MLPs: stacked [W_gate; W_up] */
+    SGD_ROLE_W2 = 9,   /* MLP output projection                                  */
+    SGD_ROLE_CONV = 10 /* convolution kernel unfolded to C_out x (C_in k_h k_w)   */
+};
+
+const char* sgd_last_error(void);
+int sgd_version(void);
+
+/* ---------------------------------------------------------------- schedule */
+
+/* One scored matrix: device pointer to a row-major rows x cols matrix. */
+typedef struct {
+    const void* ptr;
+    int64_t rows, cols;
+    int32_t dtype; /* sgd_dtype */
+    int32_t role;  /* sgd_role  */
+} sgd_matrix;
+
+/* One scheduled unit: its scored matrices and the attention head dimension d_h. */
+typedef struct {
+    const sgd_matrix* mats;
+    int32_t n_mats;
+    int32_t head_dim;
+} sgd_unit;
+
+/* Schedule parameters.
+ *   T                  horizon (denoising steps), >= 1
+ *   budget_layer_steps N* >= 0 selects budget mode (Eq. schedule swept over tau, filled to
+ *                      exactly N*; increments granted in increasing key j / Lambda_hat_l,
+ *                      ties to the lower unit index, then the lower j); -1 selects tau mode
+ *   tau                scale of Eq. schedule (tau mode only), > 0
+ *   s_min              minimum lifetime, 1..T
+ *   eta                regulariser of Eq. scr-reg, >= 0                                     */
+typedef struct {
+    int32_t T;
+    int32_t budget_layer_steps;
+    double tau;
+    int32_t s_min;
+    double eta;
+} sgd_sched_params;
+
+/* Output of the schedule calls.  The caller allocates every array on the host; optional
+ * arrays may be NULL.  L and T are filled in by the library.
+ *   lifetimes  [L]      S_l
+ *   active     [T*L]    active[(s-1)*L + l] = (s <= S_l)
+ *   unit_raw   [L]      raw unit score q~_l                    (optional)
+ *   unit_score [L]      Lambda_hat_l                           (optional)
+ *   mat_stats  [5*n]    per matrix, in input order: E_k, tail energy, ||W||_F^2,
+ *                       SCR_eta, g(W)                          (optional)
+ *   layer_steps         sum_l S_l
+ *   cut_margin          budget mode: (kappa_next - kappa_last) / kappa_last between the
+ *                       first refused and the last granted increment (+inf if none)     */
+typedef struct {
+    int32_t L, T;
+    int32_t* lifetimes;
+    uint8_t* active;
+    double* unit_raw;
+    double* unit_score;
+    double* mat_stats;
+    int64_t layer_steps;
+    double cut_margin;
+} sgd_schedule;
+
+/* Alg. 1: score every matrix of every unit on the GPU (fp64 Gram of the short side,
+ * Householder tridiagonalisation, host implicit-QL eigenvalues), then set lifetimes.
+ * Synchronises hip_stream before returning.  Errors: SGD_E_ARG, SGD_E_DTYPE,
+ * SGD_E_BUDGET, SGD_E_NUMERIC, SGD_E_HIP. */
+int sgd_schedule_build(const sgd_unit* units, int32_t L, const sgd_sched_params* params,
+                       void* hip_stream, sgd_schedule* out);
+
+/* Statistics of one matrix (Eq. scr-reg, Eq. app-matrix-score): out[5] =
+ * {E_k, tail energy, ||W||_F^2, SCR_eta, g}.  Synchronises hip_stream. */
+int sgd_matrix_stats(const sgd_matrix* m, double eta, void* hip_stream, double out[5]);
+
+/* Host only: lifetimes from given normalised scores Lambda_hat_l in [0, 1] (Eq. schedule
+ * and the budget reading above).  unit_raw / mat_stats of out are left untouched. */
+int sgd_schedule_from_scores(const double* unit_score, int32_t L, const sgd_sched_params* params,
+                             sgd_schedule* out);
+
+/* Host only: a schedule with the given lifetimes (1..T each), e.g. the all-active S_l = T. */
+int sgd_schedule_from_lifetimes(int32_t L, int32_t T, const int32_t* lifetimes, sgd_schedule* out);
+
+/* ------------------------------------------------------------------- model */
+
+/* Device pointers of one unit.  Unused entries are NULL.
+ *   norm{1,2,x}_{w,b}  fp32 [d]      (DiT: none; LLaDA/tiny: gains only)
+ *   w_qkv  [3d x d]   rows: W_Q, W_K, W_V        b_qkv fp32 [3d]
+ *   w_o    [d x d]                                b_o   fp32 [d]
+ *   w1     [F x d], gated archs [2F x d] = [W_gate; W_up]   b1 fp32 [F or 2F]
+ *   w2     [d x F]                                b2    fp32 [d]
+ *   w_xq   [d x d], w_xkv [2d x ctx_dim] = [W_K^x; W_V^x], w_xo [d x d], b_xo fp32 [d]  (SDXL)
+ *   w_ada  [6d x d], b_ada fp32 [6d]: shift1, scale1, gate1, shift2, scale2, gate2  (DiT)
+ *   w_skip [d x 2d], b_skip fp32 [d]  (U-ViT out-blocks: h <- [h ; skip] W_skip^T + b)      */
+typedef struct {
+    const void *norm1_w, *norm1_b, *w_qkv, *b_qkv, *w_o, *b_o;
+    const void *norm2_w, *norm2_b, *w1, *b1, *w2, *b2;
+    const void *normx_w, *normx_b, *w_xq, *w_xkv, *w_xo, *b_xo;
+    const void *w_ada, *b_ada;
+    const void *w_skip, *b_skip;
+} sgd_unit_weights;
+
+/* Model description.  B samples of N tokens, width d = H * head_dim, MLP width F,
+ * L units, horizon T.  Rows [update_row_begin, update_row_end) of each sample are the
+ * ones the sampler updates.  class_emb: DiT per-sample class vectors fp32 [B x d].
+ * ctx: SDXL context, dtype [B x ctx_len x ctx_dim].  U-ViT: L odd; units < L/2 are
+ * in-blocks, unit L/2 the mid block, unit l > L/2 takes the skip of in-block L-1-l;
+ * token 0 of each sample is the time token, rewritten every step.
+ * Shape limits: d % 128 == 0, F % 64 == 0, ctx_dim % 64 == 0, head_dim in {64, 72, 128}
+ * (LLaDA: 128), ctx_len <= 128.                                                    */
+typedef struct {
+    int32_t arch, dtype;
+    int32_t B, N, d, H, head_dim, F, L, T;
+    int32_t ctx_len, ctx_dim;
+    int32_t update_row_begin, update_row_end;
+    const void* class_emb;
+    const void* ctx;
+    const sgd_unit_weights* units; /* [L], copied by sgd_model_create */
+} sgd_model_desc;
+
+typedef struct sgd_model sgd_model;
+typedef struct sgd_cache sgd_cache;
+
+int sgd_model_create(const sgd_model_desc* desc, sgd_model** out);
+int sgd_model_destroy(sgd_model* model);
+
+/* Bytes of scratch one sgd_denoise_step needs (device, 256-byte aligned). */
+int sgd_workspace_bytes(const sgd_model* model, size_t* bytes);
+/* Bytes of the per-trajectory delta cache: L fp32 [B x N x d] slots (+ SDXL context K/V). */
+int sgd_cache_bytes(const sgd_model* model, size_t* bytes);
+/* Wrap a caller-owned device buffer of sgd_cache_bytes as the cache of one trajectory. */
+int sgd_cache_bind(sgd_model* model, void* device_buffer, size_t bytes, sgd_cache** out);
+/* Start a new trajectory on this cache: the next step must be 1; no slot is valid. */
+int sgd_cache_reset(sgd_cache* cache);
+int sgd_cache_destroy(sgd_cache* cache);
+
+typedef struct {
+    float alpha, beta;      /* sampler coefficients of this step                      */
+    void* workspace;        /* device buffer of sgd_workspace_bytes                    */
+    size_t workspace_bytes;
+} sgd_step_args;
+
+/* One network evaluation at step s (Alg. 2) followed by the sampler update.
+ *   state  device fp32 [B x N x d] (z_s on entry, z_{s+1} on return; updated in place)
+ *   step   s in 1..T
+ *   sched  NULL runs the unscheduled forward (every unit active, cache untouched, cache
+ *          may be NULL); otherwise a schedule with sched->L == L and sched->T == T
+ *   cache  the trajectory's cache; steps must arrive in order 1, 2, ..., T
+ * A frozen unit's slot must have been written by an earlier step of this trajectory
+ * (SGD_E_CACHE).  Returns after enqueueing on hip_stream.                           */
+int sgd_denoise_step(sgd_model* model, void* state, int32_t step, const sgd_schedule* sched,
+                     sgd_cache* cache, const sgd_step_args* args, void* hip_stream);
+
+/* ------------------------------------------------------------- profiling */
+
+/* Kernel classes the launcher can time with HIP events. */
+enum sgd_kernel_class {
+    SGD_K_NORM = 0, SGD_K_GEMM_QKV = 1, SGD_K_ATTN = 2, SGD_K_GEMM_O = 3,
+    SGD_K_GEMM_W1 = 4, SGD_K_GEMM_W2 = 5, SGD_K_FROZEN = 6, SGD_K_STATE = 7,
+    SGD_K_COND = 8, SGD_K_GEMM_SKIP = 9, SGD_K_GEMM_X = 10, SGD_K_ATTN_X = 11,
+    SGD_K_COUNT = 12
+};
+
+/* Start timing every launch of kernel class `kclass` (or -1 to stop): the launcher records
+ * a HIP event pair around each such launch on the step's stream, up to `max_launches`. */
+int sgd_profile_begin(sgd_model* model, int32_t kclass, int32_t max_launches);
+/* Synchronise on the recorded events and return the summed duration and launch count. */
+int sgd_profile_end(sgd_model* model, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SGD_H */

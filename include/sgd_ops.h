@@ -1,0 +1,67 @@
+/*
+ * sgd_ops.h -- single-kernel entry points of libsgd, for kernel-level parity tests and
+ * microbenchmarks.  They run exactly the kernels that sgd_denoise_step launches.
+ *
+ * Conventions as in sgd.h: int status (SGD_OK or SGD_E_*), device pointers, enqueue on
+ * hip_stream without synchronising, caller-owned buffers, no allocation.
+ */
+#ifndef SGD_OPS_H
+#define SGD_OPS_H
+
+#include <stdint.h>
+
+#include "sgd.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum sgd_act { SGD_ACT_NONE = 0, SGD_ACT_GELU_ERF = 1, SGD_ACT_GELU_TANH = 2, SGD_ACT_SILU = 3 };
+
+/* out[M x N] = act(A[M x K] W[N x K]^T + bias) in dtype (the branch GEMM of an MLP input
+ * projection).  gated != 0: W is [2N x K] = [W_gate; W_up] and out = act(A W_gate^T +
+ * b[:N]) * (A W_up^T + b[N:]).  lda/ldw/ldo are row strides in elements.  tile selects a
+ * block tile for bf16 (0 auto, 1: 256x256, 2: 256x128, 3: 128x128).  Shape limits:
+ * K % 64 == 0 and N % tile width == 0 (bf16), K % 16 == 0 and N % 64 == 0 (fp32). */
+int sgd_op_linear(int32_t dtype, const void* A, int64_t lda, const void* W, int64_t ldw, const float* bias,
+                  void* out, int64_t ldo, int32_t M, int32_t N, int32_t K, int32_t act, int32_t gated,
+                  int32_t tile, void* hip_stream);
+
+/* Attention (Sec. 3 units; the softmax(q k^T / sqrt(dh)) v of every head).  q [B*H, npq, dh],
+ * k [B*H, npk, dh], vt [B*H, dh, npk] (dtype), o [B, nq, H*dh].  Keys >= nk are masked;
+ * npk must be a multiple of 64 and >= nk; npq >= nq. */
+int sgd_op_attention(int32_t dtype, const void* q, const void* k, const void* vt, void* o, int32_t B, int32_t H,
+                     int32_t dh, int32_t nq, int32_t npq, int32_t nk, int32_t npk, void* hip_stream);
+
+/* Pre-norm of M rows of width d from fp32 x into y (dtype).  kind 0: RMSNorm with gain w;
+ * 1: LayerNorm with gain w and shift b; 2: LayerNorm without affine parameters followed by
+ * y * (1 + scale[r / ntok]) + shift[r / ntok] (rows of scale/shift mod_ld apart). */
+int sgd_op_norm(int32_t dtype, int32_t kind, const float* x, void* y, int32_t M, int32_t d, float eps,
+                const float* w, const float* b, const float* shift, const float* scale, int64_t mod_ld,
+                int32_t ntok, void* hip_stream);
+
+/* Projection into attention heads (the QKV GEMM of a unit): P = A[M x K] W[n_proj*d x K]^T
+ * (+ bias), column n of P belongs to projection which0 + n / d (0: q, 1: k, 2: v^T), head
+ * (n % d) / dh, dim n % dh; row r is token r % ntok of sample r / ntok.  q, k are
+ * [B*H, np, dh], vt is [B*H, dh, np].  rope != 0 rotates the q and k pairs (i, i + dh/2) of
+ * token t by t * 10000^(-2i/dh) (dh must be 128).  Padded tokens (>= ntok) are not written. */
+int sgd_op_heads(int32_t dtype, const void* A, const void* W, const float* bias, void* q, void* k, void* vt,
+                 int32_t M, int32_t K, int32_t n_proj, int32_t which0, int32_t ntok, int32_t np, int32_t H,
+                 int32_t dh, int32_t rope, void* hip_stream);
+
+/* Residual projection of a branch (the O and W2 GEMMs): v = (A[M x K] W[N x K]^T + bias),
+ * v *= gate[r / ntok] if gate != NULL (rows gate_ld apart), then h += v (fp32 [M x N]);
+ * delta_mode 1 stores v into delta, 2 adds v to delta (the cached update of Sec. 3.1). */
+int sgd_op_residual(int32_t dtype, const void* A, int64_t lda, const void* W, const float* bias, float* h,
+                    float* delta, int32_t delta_mode, const float* gate, int64_t gate_ld, int32_t ntok,
+                    int32_t M, int32_t N, int32_t K, void* hip_stream);
+
+/* h <- h + delta[0] + ... + delta[r-1] elementwise over n fp32 values (n % 4 == 0), in
+ * that order (the frozen-unit update of Sec. 3.1 for a run of r frozen units). */
+int sgd_op_frozen_run(float* h, const float* const* deltas, int32_t r, int64_t n, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SGD_OPS_H */

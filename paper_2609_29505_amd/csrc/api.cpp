@@ -1,0 +1,574 @@
+// C ABI: model and cache handles, and the step launcher of the jagged denoiser step
+// (Alg. 2, Sec. 4.2; residual-update semantics of Sec. 3.1).
+//
+// The launcher walks the units in stack order and enqueues only the kernels of active
+// units.  A maximal run of consecutive frozen units becomes one bandwidth-bound kernel
+// h <- h + Delta_l1 + ... + Delta_lr.  An active unit writes its cached update Delta_l
+// (the sum of its branch updates, in branch order) only at its last active step s = S_l,
+// because that is the update every later frozen step reads (r_l(s) = S_l).
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+#include "kernels.h"
+
+namespace sgd {
+
+static thread_local std::string g_last_error;
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+int fail(int code, const std::string& msg) {
+    g_last_error = msg;
+    return code;
+}
+int hip_fail(hipError_t e, const char* what) {
+    g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+    return SGD_E_HIP;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+}  // namespace sgd
+
+using namespace sgd;
+
+struct sgd_model {
+    sgd_model_desc d;
+    std::vector<sgd_unit_weights> u;
+    int dt = 1;       // 0 fp32, 1 bf16
+    size_t es = 2;    // element bytes of activations
+    int np = 64;      // tokens padded to 64
+    int npc = 64;     // context tokens padded to 64
+    long M = 0;
+    // workspace layout
+    size_t w_h, w_xb, w_q, w_k, w_vt, w_ob, w_hid, w_siluc, w_mod, w_hb, w_skip, w_ckv, w_total;
+    // cache layout
+    size_t c_delta, c_ctx, c_total;
+    size_t ckv_unit;  // bytes of one unit's context K and V^T
+    // profiling
+    int prof_class = -1;
+    int prof_max = 0;
+    int prof_n = 0;
+    std::vector<hipEvent_t> prof_ev;
+};
+
+struct sgd_cache {
+    sgd_model* m;
+    char* base;
+    size_t bytes;
+    int last_step;
+    std::vector<int> written;
+    bool ctx_valid;
+};
+
+extern "C" const char* sgd_last_error(void) { return sgd::g_last_error.c_str(); }
+extern "C" int sgd_version(void) { return 1; }
+
+namespace {
+
+bool arch_gated(int a) { return a == SGD_ARCH_LLADA || a == SGD_ARCH_SDXL; }
+
+int check_unit(const sgd_model_desc& d, const sgd_unit_weights& w, int l) {
+    auto need = [&](const void* p, const char* name) -> int {
+        if (!p) return fail(SGD_E_ARG, "unit " + std::to_string(l) + ": " + name + " is NULL");
+        return SGD_OK;
+    };
+    int rc = SGD_OK;
+    if ((rc = need(w.w_qkv, "w_qkv")) || (rc = need(w.w_o, "w_o")) || (rc = need(w.w1, "w1")) ||
+        (rc = need(w.w2, "w2")))
+        return rc;
+    switch (d.arch) {
+        case SGD_ARCH_TINY:
+        case SGD_ARCH_LLADA:
+            if ((rc = need(w.norm1_w, "norm1_w")) || (rc = need(w.norm2_w, "norm2_w"))) return rc;
+            break;
+        case SGD_ARCH_DIT:
+            if ((rc = need(w.w_ada, "w_ada"))) return rc;
+            break;
+        case SGD_ARCH_UVIT:
+        case SGD_ARCH_SDXL:
+            if ((rc = need(w.norm1_w, "norm1_w")) || (rc = need(w.norm1_b, "norm1_b")) ||
+                (rc = need(w.norm2_w, "norm2_w")) || (rc = need(w.norm2_b, "norm2_b")))
+                return rc;
+            break;
+    }
+    if (d.arch == SGD_ARCH_UVIT && l > d.L / 2 && (rc = need(w.w_skip, "w_skip"))) return rc;
+    if (d.arch == SGD_ARCH_SDXL) {
+        if ((rc = need(w.normx_w, "normx_w")) || (rc = need(w.normx_b, "normx_b")) || (rc = need(w.w_xq, "w_xq")) ||
+            (rc = need(w.w_xkv, "w_xkv")) || (rc = need(w.w_xo, "w_xo")))
+            return rc;
+    }
+    return SGD_OK;
+}
+
+}  // namespace
+
+extern "C" int sgd_model_create(const sgd_model_desc* desc, sgd_model** out) {
+    if (!desc || !out || !desc->units) return fail(SGD_E_ARG, "NULL argument");
+    const sgd_model_desc& d = *desc;
+    if (d.arch < SGD_ARCH_TINY || d.arch > SGD_ARCH_SDXL) return fail(SGD_E_ARG, "unknown arch");
+    if (d.dtype != SGD_F32 && d.dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
+    if (d.dtype == SGD_F32 && (arch_gated(d.arch) || d.arch == SGD_ARCH_LLADA))
+        return fail(SGD_E_DTYPE, "fp32 is supported for the tiny, DiT and U-ViT architectures");
+    if (d.B < 1 || d.N < 1 || d.L < 1 || d.T < 1 || d.H < 1 || d.head_dim < 1)
+        return fail(SGD_E_SHAPE, "B, N, L, T, H, head_dim must be >= 1");
+    if (d.d != d.H * d.head_dim) return fail(SGD_E_SHAPE, "d must equal H * head_dim");
+    if (d.d % 128) return fail(SGD_E_SHAPE, "d must be a multiple of 128");
+    if (d.F < 64 || d.F % 64 || (!arch_gated(d.arch) && d.F % 128))
+        return fail(SGD_E_SHAPE, "F must be a multiple of 128 (gated MLPs: 64)");
+    if (d.head_dim != 64 && d.head_dim != 72 && d.head_dim != 128) return fail(SGD_E_SHAPE, "head_dim must be 64, 72 or 128");
+    if (d.arch == SGD_ARCH_LLADA && d.head_dim != 128) return fail(SGD_E_SHAPE, "rotary heads need head_dim 128");
+    if (d.update_row_begin < 0 || d.update_row_end > d.N || d.update_row_begin > d.update_row_end)
+        return fail(SGD_E_ARG, "update rows outside [0, N]");
+    if (d.arch == SGD_ARCH_DIT && !d.class_emb) return fail(SGD_E_ARG, "DiT needs class_emb");
+    if (d.arch == SGD_ARCH_UVIT && (d.L % 2 == 0 || d.L < 3)) return fail(SGD_E_SHAPE, "U-ViT needs an odd L >= 3");
+    if (d.arch == SGD_ARCH_UVIT && d.N < 2) return fail(SGD_E_SHAPE, "U-ViT needs the time and class tokens");
+    if (d.arch == SGD_ARCH_SDXL) {
+        if (!d.ctx) return fail(SGD_E_ARG, "SDXL needs ctx");
+        if (d.ctx_len < 1 || d.ctx_dim < 64 || d.ctx_dim % 64) return fail(SGD_E_SHAPE, "ctx_len >= 1, ctx_dim % 64 == 0");
+    }
+    if ((long)d.B * d.N * d.d >= (1L << 31)) return fail(SGD_E_SHAPE, "B * N * d must stay below 2^31");
+    for (int l = 0; l < d.L; ++l) {
+        int rc = check_unit(d, d.units[l], l);
+        if (rc) return rc;
+    }
+    sgd_model* m = new sgd_model();
+    m->d = d;
+    m->u.assign(d.units, d.units + d.L);
+    m->d.units = nullptr;
+    m->dt = d.dtype == SGD_BF16 ? 1 : 0;
+    m->es = m->dt ? 2 : 4;
+    m->np = (d.N + 63) / 64 * 64;
+    m->npc = d.arch == SGD_ARCH_SDXL ? (d.ctx_len + 63) / 64 * 64 : 64;
+    m->M = (long)d.B * d.N;
+    const size_t Md = (size_t)m->M * d.d;
+    const size_t heads = (size_t)d.B * d.H * m->np * d.head_dim;
+    const size_t cheads = (size_t)d.B * d.H * m->npc * d.head_dim;
+    size_t o = 0;
+    auto take = [&](size_t bytes) { size_t r = o; o = align256(o + bytes); return r; };
+    m->w_h = take(Md * 4);
+    m->w_xb = take(Md * m->es);
+    m->w_q = take(heads * m->es);
+    m->w_k = take(heads * m->es);
+    m->w_vt = take(heads * m->es);
+    m->w_ob = take(Md * m->es);
+    m->w_hid = take((size_t)m->M * d.F * m->es);
+    m->w_siluc = take(d.arch == SGD_ARCH_DIT ? (size_t)d.B * d.d * 4 : 0);
+    m->w_mod = take(d.arch == SGD_ARCH_DIT ? (size_t)d.B * 6 * d.d * 4 : 0);
+    m->w_hb = take(d.arch == SGD_ARCH_UVIT ? 2 * Md * m->es : 0);
+    m->w_skip = take(d.arch == SGD_ARCH_UVIT ? (size_t)(d.L / 2) * align256(Md * m->es) : 0);
+    m->ckv_unit = align256(2 * cheads * m->es);
+    m->w_ckv = take(d.arch == SGD_ARCH_SDXL ? m->ckv_unit : 0);
+    m->w_total = o;
+    o = 0;
+    m->c_delta = take((size_t)d.L * align256(Md * 4));
+    m->c_ctx = take(d.arch == SGD_ARCH_SDXL ? (size_t)d.L * m->ckv_unit : 0);
+    m->c_total = o;
+    *out = m;
+    return SGD_OK;
+}
+
+extern "C" int sgd_model_destroy(sgd_model* m) {
+    if (!m) return fail(SGD_E_ARG, "NULL model");
+    for (hipEvent_t e : m->prof_ev) (void)hipEventDestroy(e);
+    delete m;
+    return SGD_OK;
+}
+
+extern "C" int sgd_workspace_bytes(const sgd_model* m, size_t* bytes) {
+    if (!m || !bytes) return fail(SGD_E_ARG, "NULL argument");
+    *bytes = m->w_total;
+    return SGD_OK;
+}
+
+extern "C" int sgd_cache_bytes(const sgd_model* m, size_t* bytes) {
+    if (!m || !bytes) return fail(SGD_E_ARG, "NULL argument");
+    *bytes = m->c_total;
+    return SGD_OK;
+}
+
+extern "C" int sgd_cache_bind(sgd_model* m, void* buf, size_t bytes, sgd_cache** out) {
+    if (!m || !buf || !out) return fail(SGD_E_ARG, "NULL argument");
+    if (bytes < m->c_total) return fail(SGD_E_ARG, "cache buffer smaller than sgd_cache_bytes");
+    if ((uintptr_t)buf % 256) return fail(SGD_E_ARG, "cache buffer must be 256-byte aligned");
+    sgd_cache* c = new sgd_cache();
+    c->m = m;
+    c->base = (char*)buf;
+    c->bytes = bytes;
+    c->last_step = 0;
+    c->written.assign(m->d.L, 0);
+    c->ctx_valid = false;
+    *out = c;
+    return SGD_OK;
+}
+
+extern "C" int sgd_cache_reset(sgd_cache* c) {
+    if (!c) return fail(SGD_E_ARG, "NULL cache");
+    c->last_step = 0;
+    std::fill(c->written.begin(), c->written.end(), 0);
+    c->ctx_valid = false;
+    return SGD_OK;
+}
+
+extern "C" int sgd_cache_destroy(sgd_cache* c) {
+    if (!c) return fail(SGD_E_ARG, "NULL cache");
+    delete c;
+    return SGD_OK;
+}
+
+extern "C" int sgd_profile_begin(sgd_model* m, int32_t kclass, int32_t max_launches) {
+    if (!m) return fail(SGD_E_ARG, "NULL model");
+    if (kclass >= SGD_K_COUNT || kclass < -1) return fail(SGD_E_ARG, "unknown kernel class");
+    for (hipEvent_t e : m->prof_ev) (void)hipEventDestroy(e);
+    m->prof_ev.clear();
+    m->prof_class = -1;
+    m->prof_n = 0;
+    if (kclass < 0) return SGD_OK;
+    if (max_launches < 1 || max_launches > (1 << 16)) return fail(SGD_E_ARG, "max_launches must lie in 1..65536");
+    m->prof_ev.resize(2 * (size_t)max_launches);
+    for (auto& e : m->prof_ev) SGD_HIP_TRY(hipEventCreate(&e));
+    m->prof_class = kclass;
+    m->prof_max = max_launches;
+    return SGD_OK;
+}
+
+extern "C" int sgd_profile_end(sgd_model* m, double* total_ms, int64_t* launches) {
+    if (!m || !total_ms || !launches) return fail(SGD_E_ARG, "NULL argument");
+    double tot = 0.0;
+    for (int i = 0; i < m->prof_n; ++i) {
+        SGD_HIP_TRY(hipEventSynchronize(m->prof_ev[2 * i + 1]));
+        float ms = 0.f;
+        SGD_HIP_TRY(hipEventElapsedTime(&ms, m->prof_ev[2 * i], m->prof_ev[2 * i + 1]));
+        tot += ms;
+    }
+    *total_ms = tot;
+    *launches = m->prof_n;
+    m->prof_class = -1;
+    m->prof_n = 0;
+    return SGD_OK;
+}
+
+// ---------------------------------------------------------------------------- step
+
+namespace {
+
+struct Step {
+    sgd_model* m;
+    hipStream_t st;
+    char* ws;
+    hipError_t err = hipSuccess;
+
+    template <typename F>
+    void run(int kclass, F&& f) {
+        if (err != hipSuccess) return;
+        const bool prof = m->prof_class == kclass && m->prof_n < m->prof_max;
+        if (prof) err = hipEventRecord(m->prof_ev[2 * m->prof_n], st);
+        if (err == hipSuccess) err = f();
+        if (prof && err == hipSuccess) {
+            err = hipEventRecord(m->prof_ev[2 * m->prof_n + 1], st);
+            m->prof_n++;
+        }
+    }
+};
+
+}  // namespace
+
+extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const sgd_schedule* sched,
+                                sgd_cache* cache, const sgd_step_args* args, void* hip_stream) {
+    if (!m || !state || !args) return fail(SGD_E_ARG, "NULL argument");
+    const sgd_model_desc& d = m->d;
+    if (!args->workspace || args->workspace_bytes < m->w_total) return fail(SGD_E_ARG, "workspace missing or too small");
+    if ((uintptr_t)args->workspace % 256) return fail(SGD_E_ARG, "workspace must be 256-byte aligned");
+    if ((uintptr_t)state % 16) return fail(SGD_E_ARG, "state must be 16-byte aligned");
+    if (step < 1 || step > d.T) return fail(SGD_E_STEP, "step outside 1..T");
+    const int L = d.L;
+    std::vector<uint8_t> act(L, 1);
+    std::vector<int> life(L, d.T);
+    if (sched) {
+        if (!cache) return fail(SGD_E_ARG, "a scheduled step needs a cache");
+        if (cache->m != m) return fail(SGD_E_ARG, "cache bound to another model");
+        if (sched->L != L || sched->T != d.T || !sched->lifetimes || !sched->active)
+            return fail(SGD_E_ARG, "schedule does not match the model");
+        if (step != cache->last_step + 1) return fail(SGD_E_STEP, "steps must arrive in order 1, 2, ..., T");
+        for (int l = 0; l < L; ++l) {
+            life[l] = sched->lifetimes[l];
+            act[l] = sched->active[(size_t)(step - 1) * L + l];
+            if (life[l] < 1 || life[l] > d.T) return fail(SGD_E_ARG, "lifetime outside 1..T");
+            if ((act[l] != 0) != (step <= life[l])) return fail(SGD_E_ARG, "active mask disagrees with lifetimes");
+            if (!act[l] && !cache->written[l])
+                return fail(SGD_E_CACHE, "unit " + std::to_string(l) + " is frozen but its cache slot was never written");
+        }
+    }
+
+    Step S{m, (hipStream_t)hip_stream, (char*)args->workspace};
+    const int dt = m->dt;
+    const long M = m->M;
+    const int dd = d.d, F = d.F, H = d.H, dh = d.head_dim, N = d.N;
+    const size_t Md = (size_t)M * dd;
+    float* h = (float*)(S.ws + m->w_h);
+    void* xb = S.ws + m->w_xb;
+    void* qb = S.ws + m->w_q;
+    void* kb = S.ws + m->w_k;
+    void* vtb = S.ws + m->w_vt;
+    void* ob = S.ws + m->w_ob;
+    void* hid = S.ws + m->w_hid;
+    float* siluc = (float*)(S.ws + m->w_siluc);
+    float* mod = (float*)(S.ws + m->w_mod);
+    auto hb = [&](int i) { return (void*)(S.ws + m->w_hb + i * Md * m->es); };
+    auto skipbuf = [&](int i) { return (void*)(S.ws + m->w_skip + (size_t)i * align256(Md * m->es)); };
+    auto delta = [&](int l) { return (float*)(cache->base + m->c_delta + (size_t)l * align256(Md * 4)); };
+    const bool uvit = d.arch == SGD_ARCH_UVIT, dit = d.arch == SGD_ARCH_DIT, sdxl = d.arch == SGD_ARCH_SDXL;
+    const int half = L / 2;
+    const float t = (float)(1000.0 * (double)(d.T - step + 1) / (double)d.T);
+    const int norm_kind = (d.arch == SGD_ARCH_TINY || d.arch == SGD_ARCH_LLADA) ? 0 : dit ? 2 : 1;
+    const float norm_eps = dit ? 1e-6f : 1e-5f;
+    const bool gated = arch_gated(d.arch);
+    const int mlp_act = d.arch == SGD_ARCH_LLADA ? ACT_SILU : dit ? ACT_GELU_TANH : ACT_GELU_ERF;
+
+    // shape check of every GEMM before enqueueing anything
+    {
+        GemmArgs g;
+        EpiParams e;
+        g.M = (int)M; g.K = dd; g.N = 3 * dd; e.kind = EP_HEADS; e.rope = d.arch == SGD_ARCH_LLADA; e.dh = dh; e.d = dd;
+        bool ok = gemm_shape_ok(dt, g, e);
+        e.rope = 0; e.kind = EP_RESID; g.N = dd; ok = ok && gemm_shape_ok(dt, g, e);
+        e.kind = gated ? EP_GATED : EP_ACT; g.N = gated ? 2 * F : F; ok = ok && gemm_shape_ok(dt, g, e);
+        e.kind = EP_RESID; g.N = dd; g.K = F; ok = ok && gemm_shape_ok(dt, g, e);
+        if (!ok) return fail(SGD_E_SHAPE, "GEMM shapes not supported by the kernels");
+    }
+
+    // ---- stream set-up and per-step conditioning
+    S.run(SGD_K_STATE, [&] { return launch_stream_init((const float*)state, h, d.B, N, dd, uvit ? 1 : 0, t, S.st); });
+    if (dit) S.run(SGD_K_COND, [&] { return launch_cond_silu((const float*)d.class_emb, siluc, d.B, dd, t, S.st); });
+
+    // SDXL: context keys/values are step-invariant; the scheduled path computes them once
+    // per trajectory into the cache, the unscheduled path into the workspace per unit.
+    const size_t cheads = (size_t)d.B * H * m->npc * dh;
+    auto ctx_kv = [&](int l, char* dst) {
+        GemmArgs g;
+        g.A0 = d.ctx; g.lda0 = d.ctx_dim; g.B = m->u[l].w_xkv; g.ldb = d.ctx_dim;
+        g.M = d.B * d.ctx_len; g.N = 2 * dd; g.K = d.ctx_dim;
+        EpiParams e;
+        e.kind = EP_HEADS; e.which0 = 1; e.k = dst; e.vt = dst + cheads * m->es;
+        e.ntok = d.ctx_len; e.np = m->npc; e.H = H; e.dh = dh; e.d = dd;
+        S.run(SGD_K_GEMM_X, [&] { return launch_gemm(dt, g, e, S.st); });
+    };
+    if (sdxl && sched && !cache->ctx_valid)
+        for (int l = 0; l < L; ++l) ctx_kv(l, cache->base + m->c_ctx + (size_t)l * m->ckv_unit);
+
+    auto norm = [&](const float* w, const float* b, const float* shift, const float* scale) {
+        NormArgs a{h, xb, (int)M, dd, norm_kind, norm_eps, w, b, shift, scale, 6L * dd, N};
+        S.run(SGD_K_NORM, [&] { return launch_norm(dt, a, S.st); });
+    };
+    auto resid = [&](int kclass, const void* A, long lda, int K, const void* W, const void* bias, const float* gate,
+                     float* dlt, int dmode, void* hcopy) {
+        GemmArgs g;
+        g.A0 = A; g.lda0 = lda; g.B = W; g.ldb = K; g.M = (int)M; g.N = dd; g.K = K;
+        EpiParams e;
+        e.kind = EP_RESID; e.bias = (const float*)bias; e.h = h; e.d = dd; e.delta = dlt; e.delta_mode = dmode;
+        e.gate = gate; e.gate_ld = 6L * dd; e.ntok = N; e.hcopy = hcopy;
+        S.run(kclass, [&] { return launch_gemm(dt, g, e, S.st); });
+    };
+    auto attention = [&](const void* q, const void* k, const void* vt, int nk, int npk, int kclass) {
+        AttnArgs a{q, k, vt, ob, d.B, H, dh, N, m->np, nk, npk};
+        S.run(kclass, [&] { return launch_attention(dt, a, S.st); });
+    };
+
+    int hb_cur = 0;
+    // where unit l's output copy (for a long skip or the next out-block) goes, or NULL
+    auto out_copy = [&](int l) -> void* {
+        if (!uvit) return nullptr;
+        if (l < half) return skipbuf(l);
+        if (l + 1 < L) return hb(hb_cur);
+        return nullptr;
+    };
+
+    int l = 0;
+    while (l < L && S.err == hipSuccess) {
+        const sgd_unit_weights& w = m->u[l];
+        const bool out_block = uvit && l > half;
+        const bool store_delta = sched && step == life[l] && life[l] < d.T;
+        if (!act[l] && !out_block) {
+            // maximal run of frozen units that need no skip linear in between
+            FrozenRun fr{};
+            fr.h = h; fr.n = (long)Md; fr.r = 0; fr.snap_bf16 = dt;
+            while (l < L && !act[l] && !(uvit && l > half) && fr.r < kMaxRun) {
+                fr.delta[fr.r] = delta(l);
+                fr.snap[fr.r] = out_copy(l);
+                fr.r++;
+                ++l;
+            }
+            S.run(SGD_K_FROZEN, [&] { return launch_frozen_run(fr, S.st); });
+            continue;
+        }
+        if (out_block) {
+            // U-ViT skip linear (always executed): h <- [h ; skip] W_skip^T + b (+ Delta if frozen)
+            GemmArgs g;
+            g.A0 = hb(hb_cur); g.lda0 = dd; g.A1 = skipbuf(L - 1 - l); g.lda1 = dd; g.K0 = dd;
+            g.B = w.w_skip; g.ldb = 2L * dd; g.M = (int)M; g.N = dd; g.K = 2 * dd;
+            hb_cur ^= 1;
+            EpiParams e;
+            e.kind = EP_SKIP; e.bias = (const float*)w.b_skip; e.h = h; e.d = dd;
+            if (!act[l]) { e.delta = delta(l); e.delta_mode = 1; e.hcopy = out_copy(l); }
+            S.run(SGD_K_GEMM_SKIP, [&] { return launch_gemm(dt, g, e, S.st); });
+            if (!act[l]) { ++l; continue; }
+        }
+        // ---- active unit: every branch, in order
+        float* dl = store_delta ? delta(l) : nullptr;
+        const float* mod_l = nullptr;
+        if (dit) {
+            S.run(SGD_K_COND, [&] {
+                return launch_adaln_mod(dt, siluc, w.w_ada, (const float*)w.b_ada, mod, d.B, dd, 6 * dd, S.st);
+            });
+            mod_l = mod;
+        }
+        // attention branch
+        norm((const float*)w.norm1_w, (const float*)w.norm1_b, mod_l, mod_l ? mod_l + dd : nullptr);
+        {
+            GemmArgs g;
+            g.A0 = xb; g.lda0 = dd; g.B = w.w_qkv; g.ldb = dd; g.M = (int)M; g.N = 3 * dd; g.K = dd;
+            EpiParams e;
+            e.kind = EP_HEADS; e.bias = (const float*)w.b_qkv; e.q = qb; e.k = kb; e.vt = vtb;
+            e.ntok = N; e.np = m->np; e.H = H; e.dh = dh; e.d = dd;
+            e.rope = d.arch == SGD_ARCH_LLADA; e.rope_log2_theta = (float)std::log2(10000.0);
+            S.run(SGD_K_GEMM_QKV, [&] { return launch_gemm(dt, g, e, S.st); });
+        }
+        attention(qb, kb, vtb, N, m->np, SGD_K_ATTN);
+        resid(SGD_K_GEMM_O, ob, dd, dd, w.w_o, w.b_o, mod_l ? mod_l + 2 * dd : nullptr, dl, dl ? 1 : 0, nullptr);
+        // cross-attention branch (SDXL)
+        if (sdxl) {
+            char* ckv = sched ? cache->base + m->c_ctx + (size_t)l * m->ckv_unit : S.ws + m->w_ckv;
+            if (!sched) ctx_kv(l, ckv);
+            norm((const float*)w.normx_w, (const float*)w.normx_b, nullptr, nullptr);
+            GemmArgs g;
+            g.A0 = xb; g.lda0 = dd; g.B = w.w_xq; g.ldb = dd; g.M = (int)M; g.N = dd; g.K = dd;
+            EpiParams e;
+            e.kind = EP_HEADS; e.q = qb; e.ntok = N; e.np = m->np; e.H = H; e.dh = dh; e.d = dd;
+            S.run(SGD_K_GEMM_X, [&] { return launch_gemm(dt, g, e, S.st); });
+            attention(qb, ckv, ckv + cheads * m->es, d.ctx_len, m->npc, SGD_K_ATTN_X);
+            resid(SGD_K_GEMM_X, ob, dd, dd, w.w_xo, w.b_xo, nullptr, dl, dl ? 2 : 0, nullptr);
+        }
+        // MLP branch
+        norm((const float*)w.norm2_w, (const float*)w.norm2_b, mod_l ? mod_l + 3 * dd : nullptr,
+             mod_l ? mod_l + 4 * dd : nullptr);
+        {
+            GemmArgs g;
+            g.A0 = xb; g.lda0 = dd; g.B = w.w1; g.ldb = dd; g.M = (int)M; g.N = gated ? 2 * F : F; g.K = dd;
+            EpiParams e;
+            e.kind = gated ? EP_GATED : EP_ACT; e.bias = (const float*)w.b1; e.out = hid; e.ldo = F; e.act = mlp_act;
+            e.F = F;
+            S.run(SGD_K_GEMM_W1, [&] { return launch_gemm(dt, g, e, S.st); });
+        }
+        resid(SGD_K_GEMM_W2, hid, F, F, w.w2, w.b2, mod_l ? mod_l + 5 * dd : nullptr, dl, dl ? 2 : 0, out_copy(l));
+        ++l;
+    }
+    S.run(SGD_K_STATE, [&] {
+        return launch_state_update((float*)state, h, d.B, N, dd, d.update_row_begin, d.update_row_end, args->alpha,
+                                   args->beta, S.st);
+    });
+    if (S.err != hipSuccess) return hip_fail(S.err, "enqueue");
+    if (sched) {
+        cache->last_step = step;
+        for (int u = 0; u < L; ++u)
+            if (step == life[u]) cache->written[u] = 1;
+        if (sdxl) cache->ctx_valid = true;
+    }
+    return SGD_OK;
+}
+
+// ---------------------------------------------------------------------------- single ops
+
+#include "../../include/sgd_ops.h"
+
+extern "C" int sgd_op_linear(int32_t dtype, const void* A, int64_t lda, const void* W, int64_t ldw,
+                             const float* bias, void* out, int64_t ldo, int32_t M, int32_t N, int32_t K,
+                             int32_t act, int32_t gated, int32_t tile, void* hip_stream) {
+    if (!A || !W || !out) return fail(SGD_E_ARG, "NULL argument");
+    if (dtype != SGD_F32 && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
+    if (act < 0 || act > 3 || tile < 0 || tile > 3) return fail(SGD_E_ARG, "bad act or tile");
+    if (gated && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "gated GEMMs are bf16 only");
+    GemmArgs g;
+    g.A0 = A; g.lda0 = lda; g.B = W; g.ldb = ldw; g.M = M; g.N = gated ? 2 * N : N; g.K = K;
+    EpiParams e;
+    e.kind = gated ? EP_GATED : EP_ACT; e.bias = bias; e.out = out; e.ldo = ldo; e.act = act; e.F = N;
+    const int dt = dtype == SGD_BF16 ? 1 : 0;
+    if (!gemm_shape_ok(dt, g, e, tile)) return fail(SGD_E_SHAPE, "GEMM shape not supported");
+    SGD_HIP_TRY(launch_gemm(dt, g, e, (hipStream_t)hip_stream, tile));
+    return SGD_OK;
+}
+
+extern "C" int sgd_op_heads(int32_t dtype, const void* A, const void* W, const float* bias, void* q, void* k,
+                            void* vt, int32_t M, int32_t K, int32_t n_proj, int32_t which0, int32_t ntok, int32_t np,
+                            int32_t H, int32_t dh, int32_t rope, void* hip_stream) {
+    if (!A || !W || (which0 == 0 && !q) || (which0 + n_proj > 1 && !k) || (which0 + n_proj > 2 && !vt))
+        return fail(SGD_E_ARG, "NULL argument");
+    if (dtype != SGD_F32 && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
+    if (n_proj < 1 || which0 < 0 || which0 + n_proj > 3 || ntok < 1 || np < ntok || M % ntok || H < 1 || dh < 1)
+        return fail(SGD_E_SHAPE, "bad heads shape");
+    GemmArgs g;
+    g.A0 = A; g.lda0 = K; g.B = W; g.ldb = K; g.M = M; g.N = n_proj * H * dh; g.K = K;
+    EpiParams e;
+    e.kind = EP_HEADS; e.bias = bias; e.q = q; e.k = k; e.vt = vt; e.which0 = which0; e.ntok = ntok; e.np = np;
+    e.H = H; e.dh = dh; e.d = H * dh; e.rope = rope; e.rope_log2_theta = (float)std::log2(10000.0);
+    const int dt = dtype == SGD_BF16 ? 1 : 0;
+    if (!gemm_shape_ok(dt, g, e)) return fail(SGD_E_SHAPE, "GEMM shape not supported");
+    SGD_HIP_TRY(launch_gemm(dt, g, e, (hipStream_t)hip_stream));
+    return SGD_OK;
+}
+
+extern "C" int sgd_op_residual(int32_t dtype, const void* A, int64_t lda, const void* W, const float* bias, float* h,
+                               float* delta, int32_t delta_mode, const float* gate, int64_t gate_ld, int32_t ntok,
+                               int32_t M, int32_t N, int32_t K, void* hip_stream) {
+    if (!A || !W || !h || (delta_mode && !delta)) return fail(SGD_E_ARG, "NULL argument");
+    if (dtype != SGD_F32 && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
+    if (delta_mode < 0 || delta_mode > 2 || ntok < 1) return fail(SGD_E_ARG, "bad delta_mode or ntok");
+    GemmArgs g;
+    g.A0 = A; g.lda0 = lda; g.B = W; g.ldb = K; g.M = M; g.N = N; g.K = K;
+    EpiParams e;
+    e.kind = EP_RESID; e.bias = bias; e.h = h; e.d = N; e.delta = delta; e.delta_mode = delta_mode; e.gate = gate;
+    e.gate_ld = gate_ld; e.ntok = ntok;
+    const int dt = dtype == SGD_BF16 ? 1 : 0;
+    if (!gemm_shape_ok(dt, g, e)) return fail(SGD_E_SHAPE, "GEMM shape not supported");
+    SGD_HIP_TRY(launch_gemm(dt, g, e, (hipStream_t)hip_stream));
+    return SGD_OK;
+}
+
+extern "C" int sgd_op_attention(int32_t dtype, const void* q, const void* k, const void* vt, void* o, int32_t B,
+                                int32_t H, int32_t dh, int32_t nq, int32_t npq, int32_t nk, int32_t npk,
+                                void* hip_stream) {
+    if (!q || !k || !vt || !o) return fail(SGD_E_ARG, "NULL argument");
+    if (dtype != SGD_F32 && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
+    if (B < 1 || H < 1 || nq < 1 || nk < 1 || npq < nq || npk < nk || npk % 64 || dh < 8 || dh > 128 || dh % 8)
+        return fail(SGD_E_SHAPE, "attention shape not supported");
+    AttnArgs a{q, k, vt, o, B, H, dh, nq, npq, nk, npk};
+    SGD_HIP_TRY(launch_attention(dtype == SGD_BF16 ? 1 : 0, a, (hipStream_t)hip_stream));
+    return SGD_OK;
+}
+
+extern "C" int sgd_op_norm(int32_t dtype, int32_t kind, const float* x, void* y, int32_t M, int32_t d, float eps,
+                           const float* w, const float* b, const float* shift, const float* scale, int64_t mod_ld,
+                           int32_t ntok, void* hip_stream) {
+    if (!x || !y) return fail(SGD_E_ARG, "NULL argument");
+    if (dtype != SGD_F32 && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
+    if (kind < 0 || kind > 2 || M < 1 || d < 4 || d % 4 || d > 8192) return fail(SGD_E_SHAPE, "norm shape not supported");
+    if ((kind == 0 && !w) || (kind == 1 && (!w || !b)) || (kind == 2 && (!shift || !scale || ntok < 1)))
+        return fail(SGD_E_ARG, "missing norm parameters");
+    NormArgs a{x, y, M, d, kind, eps, w, b, shift, scale, mod_ld, ntok};
+    SGD_HIP_TRY(launch_norm(dtype == SGD_BF16 ? 1 : 0, a, (hipStream_t)hip_stream));
+    return SGD_OK;
+}
+
+extern "C" int sgd_op_frozen_run(float* h, const float* const* deltas, int32_t r, int64_t n, void* hip_stream) {
+    if (!h || !deltas || r < 1 || r > kMaxRun || n < 4 || n % 4) return fail(SGD_E_ARG, "bad frozen-run arguments");
+    FrozenRun f{};
+    f.h = h; f.n = n; f.r = r; f.snap_bf16 = 1;
+    for (int i = 0; i < r; ++i) {
+        if (!deltas[i]) return fail(SGD_E_ARG, "NULL delta");
+        f.delta[i] = deltas[i];
+        f.snap[i] = nullptr;
+    }
+    SGD_HIP_TRY(launch_frozen_run(f, (hipStream_t)hip_stream));
+    return SGD_OK;
+}

@@ -1,0 +1,251 @@
+// Fused bidirectional / cross attention (flash-style, one pass over the keys).
+//
+// bf16 path (MFMA 32x32x16): a workgroup is 4 waves x 32 queries.  Each wave computes the
+// transposed score tile S^T = K Q^T so that one lane owns one query: the row maximum and
+// row sum of the online softmax are per-lane reductions plus one exchange with lane ^ 32.
+// The output is accumulated transposed as O^T += V^T P^T, where P^T is exactly the S^T
+// accumulator layout re-packed to bf16 (the MFMA k-slots are permuted consistently on
+// both operands), and V^T is read from the head-major transposed value layout written by
+// the QKV GEMM epilogue.  Keys beyond nk are masked; head dims are zero-padded to a
+// multiple of 32.
+// fp32 path: one thread per query, scores for a 64-key block, online softmax.
+#include "common.h"
+#include "kernels.h"
+
+namespace sgd {
+
+template <int DHP>
+__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, float scale_log2) {
+    constexpr int BQ = 128, BKV = 64;
+    constexpr int KS = DHP / 16, DT = DHP / 32;
+    constexpr int KLDS = DHP + 8, VLDS = BKV + 8;
+    __shared__ __attribute__((aligned(16))) bf16 sk[BKV * KLDS];
+    __shared__ __attribute__((aligned(16))) bf16 sv[DHP * VLDS];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int bh = blockIdx.y;
+    const int b = bh / a.H, hh = bh - b * a.H;
+    const int dh = a.dh;
+    const int q = blockIdx.x * BQ + wave * 32 + (lane & 31);
+    const int half = lane >> 5;
+
+    const bf16* Q = (const bf16*)a.q + (long)bh * a.npq * dh;
+    const bf16* K = (const bf16*)a.k + (long)bh * a.npk * dh;
+    const bf16* VT = (const bf16*)a.vt + (long)bh * dh * a.npk;
+
+    // zero the padded head dims once (never overwritten by the loads below)
+    for (int i = tid; i < BKV * (DHP - dh); i += 256) {
+        int r = i / (DHP - dh), c = dh + i % (DHP - dh);
+        sk[r * KLDS + c] = f2bf(0.f);
+    }
+    for (int i = tid; i < (DHP - dh) * BKV; i += 256) {
+        int r = dh + i / BKV, c = i % BKV;
+        sv[r * VLDS + c] = f2bf(0.f);
+    }
+
+    // this lane's query fragments (B operand of S^T = K Q^T)
+    bf16x8 qf[KS];
+    const int qrow = min(q, a.npq - 1);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        const int c = ks * 16 + half * 8;
+        if (c < dh) qf[ks] = *(const bf16x8*)(Q + (long)qrow * dh + c);
+        else
+            for (int e = 0; e < 8; ++e) qf[ks][e] = f2bf(0.f);
+    }
+
+    f32x16 o[DT];
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[t][r] = 0.f;
+    float m = -INFINITY, lsum = 0.f;
+
+    const int kchunks = dh / 8;  // 16-byte chunks per key row
+    const int nkb = (a.nk + BKV - 1) / BKV;
+    for (int kb = 0; kb < nkb; ++kb) {
+        const int k0 = kb * BKV;
+        __syncthreads();
+        for (int i = tid; i < BKV * kchunks; i += 256) {
+            const int r = i / kchunks, c = (i - r * kchunks) * 8;
+            *(u32x4*)(sk + r * KLDS + c) = *(const u32x4*)(K + (long)(k0 + r) * dh + c);
+        }
+        for (int i = tid; i < dh * (BKV / 8); i += 256) {
+            const int r = i >> 3, c = (i & 7) * 8;
+            bf16x8 v = *(const bf16x8*)(VT + (long)r * a.npk + k0 + c);
+            if (k0 + c + 8 > a.nk) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (k0 + c + e >= a.nk) v[e] = f2bf(0.f);
+            }
+            *(bf16x8*)(sv + r * VLDS + c) = v;
+        }
+        __syncthreads();
+
+        f32x16 s[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) s[t][r] = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                bf16x8 kf = *(const bf16x8*)(sk + (t * 32 + (lane & 31)) * KLDS + ks * 16 + half * 8);
+                s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[t], 0, 0, 0);
+            }
+        }
+        // scale into the log2 domain, mask keys beyond nk, block maximum
+        float bm = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int key = k0 + t * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+                float v = s[t][r] * scale_log2;
+                v = key < a.nk ? v : -INFINITY;
+                s[t][r] = v;
+                bm = fmaxf(bm, v);
+            }
+        bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+        const float mn = fmaxf(m, bm);
+        const float alpha = exp2f(m - mn);
+        m = mn;
+        float ps = 0.f;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float p = exp2f(s[t][r] - mn);
+                s[t][r] = p;
+                ps += p;
+            }
+        lsum = lsum * alpha + ps;
+#pragma unroll
+        for (int t = 0; t < DT; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+
+        // O^T += V^T P^T over the block's 64 keys, 16 at a time
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+#pragma unroll
+            for (int k2 = 0; k2 < 2; ++k2) {
+                bf16x8 pf;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) pf[e] = f2bf(s[t][8 * k2 + e]);
+                const int kc = t * 32 + 16 * k2 + half * 4;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    const bf16* vr = sv + (dt * 32 + (lane & 31)) * VLDS + kc;
+                    bf16x4 lo = *(const bf16x4*)vr;
+                    bf16x4 hi = *(const bf16x4*)(vr + 8);
+                    bf16x8 vf;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) { vf[e] = lo[e]; vf[4 + e] = hi[e]; }
+                    o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[dt], 0, 0, 0);
+                }
+            }
+        }
+    }
+
+    const float l = lsum + __shfl_xor(lsum, 32, 64);
+    const float inv = 1.0f / l;
+    if (q < a.nq) {
+        bf16* O = (bf16*)a.o + ((long)b * a.nq + q) * ((long)a.H * dh) + (long)hh * dh;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+                const int d0 = dt * 32 + g4 * 8 + half * 4;
+                if (d0 < dh) {
+                    bf16x4 v;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = f2bf(o[dt][g4 * 4 + e] * inv);
+                    *(bf16x4*)(O + d0) = v;
+                }
+            }
+    }
+}
+
+template <int DHP>
+__global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, float scale) {
+    constexpr int BKV = 64;
+    __shared__ float sk[BKV][DHP + 1];
+    __shared__ float sv[DHP][BKV + 1];
+    const int tid = threadIdx.x;
+    const int bh = blockIdx.y;
+    const int b = bh / a.H, hh = bh - b * a.H;
+    const int dh = a.dh;
+    const int q = blockIdx.x * 64 + tid;
+    const float* Q = (const float*)a.q + (long)bh * a.npq * dh;
+    const float* K = (const float*)a.k + (long)bh * a.npk * dh;
+    const float* VT = (const float*)a.vt + (long)bh * dh * a.npk;
+    float qv[DHP], ov[DHP];
+    const int qrow = min(q, a.npq - 1);
+#pragma unroll
+    for (int j = 0; j < DHP; ++j) {
+        qv[j] = j < dh ? Q[(long)qrow * dh + j] : 0.f;
+        ov[j] = 0.f;
+    }
+    float m = -INFINITY, l = 0.f;
+    for (int k0 = 0; k0 < a.nk; k0 += BKV) {
+        __syncthreads();
+        for (int i = tid; i < BKV * DHP; i += 64) {
+            int r = i / DHP, c = i % DHP;
+            sk[r][c] = c < dh ? K[(long)(k0 + r) * dh + c] : 0.f;
+        }
+        for (int i = tid; i < DHP * BKV; i += 64) {
+            int r = i / BKV, c = i % BKV;
+            sv[r][c] = (r < dh && k0 + c < a.nk) ? VT[(long)r * a.npk + k0 + c] : 0.f;
+        }
+        __syncthreads();
+        float s[BKV];
+        float bm = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < BKV; ++j) {
+            float acc = 0.f;
+#pragma unroll
+            for (int c = 0; c < DHP; ++c) acc = fmaf(qv[c], sk[j][c], acc);
+            acc *= scale;
+            s[j] = (k0 + j < a.nk) ? acc : -INFINITY;
+            bm = fmaxf(bm, s[j]);
+        }
+        const float mn = fmaxf(m, bm);
+        const float alpha = expf(m - mn);
+        m = mn;
+        l *= alpha;
+#pragma unroll
+        for (int c = 0; c < DHP; ++c) ov[c] *= alpha;
+#pragma unroll
+        for (int j = 0; j < BKV; ++j) {
+            const float p = expf(s[j] - mn);
+            l += p;
+#pragma unroll
+            for (int c = 0; c < DHP; ++c) ov[c] = fmaf(p, sv[c][j], ov[c]);
+        }
+    }
+    if (q < a.nq) {
+        float* O = (float*)a.o + ((long)b * a.nq + q) * ((long)a.H * dh) + (long)hh * dh;
+        const float inv = 1.0f / l;
+        for (int c = 0; c < dh; ++c) O[c] = ov[c] * inv;
+    }
+}
+
+hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st) {
+    const int BH = a.B * a.H;
+    if (dtype == 1) {
+        const float sl2 = (float)(1.4426950408889634 / sqrt((double)a.dh));
+        dim3 grid((a.nq + 127) / 128, BH), block(256);
+        if (a.dh <= 64) hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, st, a, sl2);
+        else if (a.dh <= 96) hipLaunchKernelGGL(attn_bf16_kernel<96>, grid, block, 0, st, a, sl2);
+        else hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, st, a, sl2);
+    } else {
+        const float sc = (float)(1.0 / sqrt((double)a.dh));
+        dim3 grid((a.nq + 63) / 64, BH), block(64);
+        if (a.dh <= 64) hipLaunchKernelGGL(attn_f32_kernel<64>, grid, block, 0, st, a, sc);
+        else if (a.dh <= 96) hipLaunchKernelGGL(attn_f32_kernel<96>, grid, block, 0, st, a, sc);
+        else hipLaunchKernelGGL(attn_f32_kernel<128>, grid, block, 0, st, a, sc);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace sgd

@@ -1,0 +1,97 @@
+// Host-side launch functions of the HIP kernels (internal to libsgd).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sgd {
+
+// Activation selectors for GEMM epilogues.
+enum Act { ACT_NONE = 0, ACT_GELU_ERF = 1, ACT_GELU_TANH = 2, ACT_SILU = 3 };
+
+// ---------------------------------------------------------------- GEMM
+// C[M x N] = A[M x K] . B[N x K]^T with a fused epilogue.  A may come from two sources
+// split along K (k < K0: A0, k >= K0: A1), which the U-ViT skip linear uses to read
+// [h ; skip] without a concatenation.  Gated GEMMs read B rows [0, F) and [F, 2F) in
+// pairs and write F output columns.
+struct GemmArgs {
+    const void* A0 = nullptr; long lda0 = 0;
+    const void* A1 = nullptr; long lda1 = 0; int K0 = 0;
+    const void* B = nullptr; long ldb = 0;
+    int M = 0, N = 0, K = 0;  // N: product columns (gated: 2F)
+};
+
+enum EpKind { EP_HEADS = 0, EP_ACT = 1, EP_GATED = 2, EP_RESID = 3, EP_SKIP = 4 };
+
+struct EpiParams {
+    int kind = EP_ACT;
+    const float* bias = nullptr;
+    // EP_ACT / EP_GATED: out[M x ldo] in the GEMM dtype
+    void* out = nullptr; long ldo = 0; int act = 0; int F = 0;
+    // EP_HEADS: q/k [B*H, Np, dh], vt [B*H, dh, Np]; column n of the product is
+    // projection (which0 + n / d), head (n % d) / dh, dim n % dh
+    void* q = nullptr; void* k = nullptr; void* vt = nullptr;
+    int which0 = 0, ntok = 1, np = 1, H = 1, dh = 1, d = 1, rope = 0; float rope_log2_theta = 0.f;
+    // EP_RESID / EP_SKIP: fp32 stream h[M x d]; delta_mode 0 none, 1 store, 2 accumulate
+    // (EP_SKIP: 1 = add the cached delta to the skip output); gate[b * gate_ld + n]
+    float* h = nullptr; float* delta = nullptr; int delta_mode = 0;
+    const float* gate = nullptr; long gate_ld = 0; void* hcopy = nullptr;
+};
+
+// dtype: 0 fp32, 1 bf16.  tile: 0 = pick automatically.
+hipError_t launch_gemm(int dtype, const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile = 0);
+bool gemm_shape_ok(int dtype, const GemmArgs& g, const EpiParams& e, int tile = 0);
+
+// ---------------------------------------------------------------- attention
+// O[b, i, h*dh + j] = softmax_j'(q_i . k_j' / sqrt(dh)) v_j'  over keys j' < nk.
+// q [BH, npq, dh], k [BH, npk, dh], vt [BH, dh, npk]; O row-major [B, nq, H*dh].
+struct AttnArgs {
+    const void* q; const void* k; const void* vt; void* o;
+    int B, H, dh, nq, npq, nk, npk;
+};
+hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- norms
+// kind 0: RMSNorm(w), 1: LayerNorm(w, b), 2: LayerNorm (no affine) * (1 + scale_b) + shift_b
+struct NormArgs {
+    const float* x; void* y; int M, d, kind; float eps;
+    const float* w; const float* b;
+    const float* shift; const float* scale; long mod_ld; int ntok;
+};
+hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- elementwise
+constexpr int kMaxRun = 32;
+struct FrozenRun {
+    float* h; long n;  // elements
+    int r;
+    int snap_bf16;  // snapshot dtype: 1 bf16, 0 fp32
+    const float* delta[kMaxRun];
+    void* snap[kMaxRun];  // optional copies of h after adding delta[i]
+};
+hipError_t launch_frozen_run(const FrozenRun& f, hipStream_t st);
+
+// h = z; U-ViT: token 0 of every sample = sinusoidal embedding of t
+hipError_t launch_stream_init(const float* z, float* h, int B, int N, int d, int time_token, float t,
+                              hipStream_t st);
+// z = alpha z - beta h on rows [r0, r1) of every sample
+hipError_t launch_state_update(float* z, const float* h, int B, int N, int d, int r0, int r1,
+                               float alpha, float beta, hipStream_t st);
+// x[b, :] = SiLU(emb(t) + y[b, :])  (DiT conditioning input)
+hipError_t launch_cond_silu(const float* y, float* x, int B, int d, float t, hipStream_t st);
+// mod[b, j] = sum_k x[b, k] W[j, k] + bias[j]  (DiT AdaLN modulation, W dtype)
+hipError_t launch_adaln_mod(int dtype, const float* x, const void* W, const float* bias, float* mod,
+                            int B, int d, int n_out, hipStream_t st);
+// fp32 -> bf16 copy
+hipError_t launch_to_bf16(const float* x, void* y, long n, hipStream_t st);
+
+// ---------------------------------------------------------------- spectra (fp64)
+// G = X^T X (trans = 0, X rows x cols, G cols x cols) or X X^T (trans = 1, G rows x rows)
+hipError_t launch_gram(int dtype, const void* X, long rows, long cols, int trans, double* G, hipStream_t st);
+// Householder tridiagonalisation of the symmetric n x n matrix A (destroyed).  diag[n],
+// offd[n-1] receive the tridiagonal; work holds 5n + 8 doubles.
+hipError_t launch_tridiagonalize(double* A, int n, double* diag, double* offd, double* work,
+                                 hipStream_t st);
+hipError_t launch_diag_copy(const double* A, int n, double* out, hipStream_t st);
+
+}  // namespace sgd

@@ -1,0 +1,80 @@
+"""Shared helpers of the test suite: run the oracle and the HIP path on the same seeded inputs."""
+from __future__ import annotations
+
+import numpy as np
+
+import synth
+from oracle import model as om
+from oracle import schedule as osch
+from oracle import spectral as osp
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def rel_err(x: np.ndarray, ref: np.ndarray) -> float:
+    """max_i |x_i - ref_i| / max_i |ref_i|  (the error metric of the parity gate)."""
+    ref = np.asarray(ref, np.float64)
+    return float(np.max(np.abs(np.asarray(x, np.float64) - ref)) / max(np.max(np.abs(ref)), 1e-30))
+
+
+def oracle_schedule(cfg, weights, pct):
+    raw = [osp.unit_score(osp.unit_matrices(u, cfg.d, cfg.dtype), cfg.dh).raw for u in weights]
+    lam = osp.normalise(raw)
+    n = osch.budget_layer_steps(pct, cfg.L, cfg.T)
+    bs = osch.lifetimes_budget(lam, cfg.T, n, osch.s_min_default(cfg.T))
+    return np.array(raw), lam, bs
+
+
+def oracle_trajectory(cfg, weights, inputs, mask, steps=None):
+    m = om.Model(cfg, weights, inputs)
+    return om.trajectory(m, inputs["z"], mask, steps)
+
+
+def gpu_trajectory(dm, cfg, inputs, sched, steps=None, cache=None):
+    """Run steps 1..steps on the GPU; returns the list of z after each step (host float64)."""
+    import torch
+    z = torch.from_numpy(inputs["z"].copy()).cuda()
+    steps = cfg.T if steps is None else steps
+    if sched is not None and cache is None:
+        from paper_2609_29505_amd import Cache
+        cache = Cache(dm)
+    if cache is not None:
+        cache.reset()
+    out = []
+    for s in range(1, steps + 1):
+        dm.step(z, s, sched, cache)
+        out.append(z.cpu().numpy().astype(np.float64))
+    torch.cuda.synchronize()
+    return out
+
+
+def gpu_teacher_forced(dm, cfg, oracle_z, z0, sched):
+    """Step s of the GPU path fed the oracle's state z_s (its own cache carries over).
+
+    Returns the GPU's z_{s+1} for s = 1..T, each to compare with the oracle's z_{s+1}: the
+    per-step implementation error, without the amplification of earlier differences by the
+    trajectory map.
+    """
+    import torch
+    from paper_2609_29505_amd import Cache
+    cache = Cache(dm)
+    cache.reset()
+    out = []
+    z = torch.empty(z0.shape, dtype=torch.float32, device="cuda")
+    for s in range(1, cfg.T + 1):
+        src = z0 if s == 1 else oracle_z[s - 2]
+        z.copy_(torch.from_numpy(np.ascontiguousarray(src, dtype=np.float32)))
+        dm.step(z, s, sched, cache)
+        out.append(z.cpu().numpy().astype(np.float64))
+    return out
+
+
+def chaos_floor(cfg, weights, inputs, mask, rel=1e-7, seed=1):
+    """Divergence of the oracle from itself when its initial state is perturbed by `rel`
+    (relative, seeded): the sensitivity of the bf16-quantised trajectory map."""
+    x2 = dict(inputs)
+    rng = np.random.default_rng(seed)
+    x2["z"] = (inputs["z"] * (1 + rel * rng.standard_normal(inputs["z"].shape))).astype(np.float32)
+    a = oracle_trajectory(cfg, weights, inputs, mask)
+    b = oracle_trajectory(cfg, weights, x2, mask)
+    return a, [rel_err(p, q) for p, q in zip(b.z, a.z)]

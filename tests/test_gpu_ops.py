@@ -1,0 +1,224 @@
+"""Kernel-level parity: each HIP kernel (through sgd_ops.h) against the oracle's definition of
+the same operation, on seeded inputs spanning several tiles and ragged tails."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import model as om
+from oracle.numerics import decode, round_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def P():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_29505_amd as P
+    P.lib()
+    return P
+
+
+def dev(arr):
+    import torch
+    if arr.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(arr, np.float32)).cuda()
+
+
+def host(t):
+    import torch
+    if t.dtype == torch.bfloat16:
+        return decode(t.view(torch.int16).cpu().numpy().view(np.uint16), "bf16")
+    return t.cpu().numpy().astype(np.float64)
+
+
+def empty(shape, dtype):
+    import torch
+    return torch.full(shape, float("nan"), dtype=torch.bfloat16 if dtype == "bf16" else torch.float32, device="cuda")
+
+
+def relmax(x, ref):
+    return float(np.max(np.abs(x - ref)) / np.max(np.abs(ref)))
+
+
+@pytest.mark.parametrize("M,N,K,tile", [(200, 256, 128, 3), (256, 512, 256, 2), (300, 768, 192, 1),
+                                        (64, 128, 64, 3), (1000, 384, 320, 0), (513, 1024, 128, 0)])
+def test_linear_bf16(P, M, N, K, tile):
+    rng = np.random.default_rng(M + N + K)
+    A = synth.store(rng.standard_normal((M, K)), "bf16")
+    W = synth.store(rng.standard_normal((N, K)) / np.sqrt(K), "bf16")
+    b = synth.representable(0.1 * rng.standard_normal(N), "bf16")
+    out = empty((M, N), "bf16")
+    P.op_linear(dev(A), dev(W), out, bias=dev(b), tile=tile)
+    ref = decode(A, "bf16") @ decode(W, "bf16").T + b
+    got = host(out)
+    assert np.isfinite(got).all()
+    assert np.max(np.abs(got - round_bf16(ref))) <= 2 ** -7 * np.max(np.abs(ref))
+
+
+@pytest.mark.parametrize("act", [1, 2, 3])
+def test_linear_act_bf16(P, act):
+    rng = np.random.default_rng(act)
+    M, N, K = 130, 256, 192
+    A = synth.store(rng.standard_normal((M, K)), "bf16")
+    W = synth.store(rng.standard_normal((N, K)) / np.sqrt(K), "bf16")
+    out = empty((M, N), "bf16")
+    P.op_linear(dev(A), dev(W), out, act=act)
+    z = decode(A, "bf16") @ decode(W, "bf16").T
+    f = {1: om.gelu_erf, 2: om.gelu_tanh, 3: om.silu}[act]
+    ref = f(z)
+    assert relmax(host(out), ref) <= 1e-2
+
+
+@pytest.mark.parametrize("tile", [0, 1, 3])
+def test_linear_gated_bf16(P, tile):
+    rng = np.random.default_rng(11 + tile)
+    M, F, K = 260, 256, 128
+    A = synth.store(rng.standard_normal((M, K)), "bf16")
+    W = synth.store(rng.standard_normal((2 * F, K)) / np.sqrt(K), "bf16")
+    b = synth.representable(0.1 * rng.standard_normal(2 * F), "bf16")
+    out = empty((M, F), "bf16")
+    P.op_linear(dev(A), dev(W), out, bias=dev(b), act=3, gated=True, tile=tile)
+    z = decode(A, "bf16") @ decode(W, "bf16").T + b
+    ref = om.silu(z[:, :F]) * z[:, F:]
+    assert relmax(host(out), ref) <= 1e-2
+
+
+@pytest.mark.parametrize("M,N,K", [(72, 128, 64), (256, 768, 256), (144, 1024, 256)])
+def test_linear_f32(P, M, N, K):
+    rng = np.random.default_rng(M * N)
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.standard_normal((N, K)) / np.sqrt(K)).astype(np.float32)
+    out = empty((M, N), "f32")
+    P.op_linear(dev(A), dev(W), out)
+    ref = A.astype(np.float64) @ W.astype(np.float64).T
+    assert relmax(host(out), ref) <= 1e-5
+
+
+def _heads_inputs(rng, B, H, nq, nk, dh, dtype, npq, npk):
+    q = rng.standard_normal((B * H, npq, dh)) * 1.5
+    k = rng.standard_normal((B * H, npk, dh)) * 1.5
+    v = rng.standard_normal((B * H, npk, dh))
+    qs, ks, vs = synth.store(q, dtype), synth.store(k, dtype), synth.store(v, dtype)
+    vts = np.ascontiguousarray(vs.transpose(0, 2, 1))
+    return qs, ks, vs, vts
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("B,H,nq,nk,dh", [(1, 2, 200, 200, 128), (2, 3, 80, 80, 72), (2, 2, 66, 66, 64),
+                                          (2, 2, 96, 77, 64), (1, 1, 256, 256, 64), (1, 2, 130, 1, 64)])
+def test_attention(P, dtype, B, H, nq, nk, dh):
+    rng = np.random.default_rng(nq * 7 + nk + dh)
+    npq, npk = -(-nq // 64) * 64, -(-nk // 64) * 64
+    qs, ks, vs, vts = _heads_inputs(rng, B, H, nq, nk, dh, dtype, npq, npk)
+    o = empty((B, nq, H * dh), dtype)
+    P.op_attention(dev(qs), dev(ks), dev(vts), o, B, H, dh, nq, nk)
+    q = decode(qs, dtype)[:, :nq].reshape(B, H, nq, dh)
+    k = decode(ks, dtype)[:, :nk].reshape(B, H, nk, dh)
+    v = decode(vs, dtype)[:, :nk].reshape(B, H, nk, dh)
+    ref = om.merge_heads(om.attention(q, k, v))
+    got = host(o)
+    assert np.isfinite(got).all()
+    tol = 1.5e-2 if dtype == "bf16" else 1e-5
+    assert relmax(got, ref) <= tol
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("kind,d", [(0, 256), (0, 4096), (1, 1024), (1, 1280), (2, 1152)])
+def test_norm(P, dtype, kind, d):
+    rng = np.random.default_rng(kind * 100 + d)
+    M, ntok = 70, 35
+    x = (rng.standard_normal((M, d)) * 3 + 0.5).astype(np.float32)
+    w = (1 + 0.1 * rng.standard_normal(d)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(d)).astype(np.float32)
+    mod = rng.standard_normal((2, 6 * d)).astype(np.float32)
+    y = empty((M, d), dtype)
+    x64 = x.astype(np.float64)
+    if kind == 0:
+        P.op_norm(0, dev(x), y, 1e-5, w=dev(w))
+        ref = om.rmsnorm(x64, w)
+    elif kind == 1:
+        P.op_norm(1, dev(x), y, 1e-5, w=dev(w), b=dev(b))
+        ref = om.layernorm(x64, w, b, eps=1e-5)
+    else:
+        md = dev(mod)
+        P.op_norm(2, dev(x), y, 1e-6, shift=md[:, :d], scale=md[:, d:2 * d], ntok=ntok)
+        shift = np.repeat(mod[:, :d], ntok, axis=0)
+        scale = np.repeat(mod[:, d:2 * d], ntok, axis=0)
+        ref = om.layernorm(x64, eps=1e-6) * (1 + scale) + shift
+    got = host(y)
+    if dtype == "bf16":
+        assert np.max(np.abs(got - round_bf16(ref))) <= 2 ** -7 * np.max(np.abs(ref))
+    else:
+        assert relmax(got, ref) <= 1e-5
+
+
+def test_frozen_run_bitwise(P):
+    rng = np.random.default_rng(0)
+    n = 4096 * 33
+    h = rng.standard_normal(n).astype(np.float32)
+    ds = [rng.standard_normal(n).astype(np.float32) for _ in range(5)]
+    th = dev(h)
+    P.op_frozen_run(th, [dev(d) for d in ds])
+    ref = h.copy()
+    for d in ds:
+        ref = (ref + d).astype(np.float32)
+    assert np.array_equal(th.cpu().numpy(), ref)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("B,N,H,dh,rope,bias", [(1, 200, 2, 128, True, False), (2, 80, 16, 72, False, True),
+                                                (2, 66, 4, 64, False, False), (1, 130, 2, 128, False, True)])
+def test_heads(P, dtype, B, N, H, dh, rope, bias):
+    if dtype == "f32" and rope:
+        pytest.skip("rotary epilogue is bf16 only")
+    rng = np.random.default_rng(N + dh)
+    d = H * dh
+    M = B * N
+    np_ = -(-N // 64) * 64
+    A = synth.store(rng.standard_normal((M, d)), dtype)
+    W = synth.store(rng.standard_normal((3 * d, d)) / np.sqrt(d), dtype)
+    b = synth.representable(0.1 * rng.standard_normal(3 * d), dtype) if bias else None
+    q, k = empty((B * H, np_, dh), dtype), empty((B * H, np_, dh), dtype)
+    vt = empty((B * H, dh, np_), dtype)
+    P.op_heads(dev(A), dev(W), q, k, vt, 3, 0, N, H, dh, bias=dev(b) if bias else None, rope=rope)
+    z = decode(A, dtype) @ decode(W, dtype).T + (b if bias else 0)
+    Q, K, V = (om.heads(z[:, i * d:(i + 1) * d].reshape(B, N, d), H) for i in range(3))
+    if rope:
+        Q, K = om.rope(Q), om.rope(K)
+    got_q = host(q).reshape(B, H, np_, dh)[:, :, :N]
+    got_k = host(k).reshape(B, H, np_, dh)[:, :, :N]
+    got_v = host(vt).reshape(B, H, dh, np_)[:, :, :, :N].transpose(0, 1, 3, 2)
+    tol = 2 ** -7 if dtype == "bf16" else 1e-5
+    for g, r in ((got_q, Q), (got_k, K), (got_v, V)):
+        assert np.isfinite(g).all()
+        assert np.max(np.abs(g - r)) <= tol * np.max(np.abs(r))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("M,N,K,gated_rows,mode", [(200, 256, 256, 0, 1), (160, 1152, 1152, 80, 2), (130, 512, 1024, 0, 0)])
+def test_residual(P, dtype, M, N, K, gated_rows, mode):
+    rng = np.random.default_rng(M + K + mode)
+    A = synth.store(rng.standard_normal((M, K)), dtype)
+    W = synth.store(rng.standard_normal((N, K)) / np.sqrt(K), dtype)
+    b = synth.representable(0.1 * rng.standard_normal(N), dtype)
+    h0 = rng.standard_normal((M, N)).astype(np.float32)
+    d0 = rng.standard_normal((M, N)).astype(np.float32)
+    gate = rng.standard_normal((2, 6 * N)).astype(np.float32) if gated_rows else None
+    th, td = dev(h0), dev(d0)
+    g_dev = dev(gate)[:, 2 * N:3 * N] if gated_rows else None
+    P.op_residual(dev(A), dev(W), th, bias=dev(b), delta=td if mode else None, delta_mode=mode, gate=g_dev,
+                  ntok=gated_rows or 1)
+    v = decode(A, dtype) @ decode(W, dtype).T + b
+    if gated_rows:
+        v = v * np.repeat(gate[:, 2 * N:3 * N], gated_rows, axis=0)
+    tol = 1e-2 if dtype == "bf16" else 1e-5
+    assert relmax(host(th), h0 + v) <= tol * 0.1
+    if mode == 1:
+        assert relmax(host(td), v) <= 1e-5
+    elif mode == 2:
+        assert relmax(host(td), d0 + v) <= 1e-5
+    else:
+        assert np.array_equal(host(td), d0.astype(np.float64))

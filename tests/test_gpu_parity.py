@@ -1,0 +1,183 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the same seeded inputs.
+
+Tolerances: schedules and masks bit-exact; hidden states max|x - y| / max|y| <= 1e-4 (fp32
+workloads) and <= 2e-2 (bf16 workloads) at every step.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import schedule as osch
+from oracle import spectral as osp
+
+from helpers import (TOL, chaos_floor, gpu_teacher_forced, gpu_trajectory, oracle_schedule, oracle_trajectory,
+                     rel_err)
+
+pytestmark = pytest.mark.gpu
+
+MINIS = ["tiny_ragged", "llada_mini", "dit_mini", "uvit_mini", "sdxl_mini"]
+
+
+@pytest.fixture(scope="module")
+def P():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_29505_amd as P
+    P.lib()
+    return P
+
+
+_cache = {}
+
+
+def workload(name, **kw):
+    key = (name, tuple(sorted(kw.items())))
+    if key not in _cache:
+        cfg = synth.get_config(name, **kw)
+        _cache[key] = (cfg, synth.model_weights(cfg), synth.inputs(cfg))
+    return _cache[key]
+
+
+# ---------------------------------------------------------------- spectra and schedules
+
+def _dev(arr):
+    import torch
+    if arr.dtype == np.uint16:
+        return torch.from_numpy(arr.view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(arr, np.float32)).cuda()
+
+
+@pytest.mark.parametrize("shape,dtype", [((100, 37), "f32"), ((37, 100), "f32"), ((256, 256), "bf16"),
+                                         ((300, 700), "bf16"), ((1280, 640), "bf16"), ((1, 50), "f32"),
+                                         ((5, 3), "f32"), ((130, 129), "f32")])
+def test_matrix_stats(P, shape, dtype):
+    rng = np.random.default_rng(sum(shape))
+    w, _ = synth.planted_matrix(rng, *shape, np.float64)
+    stored = synth.store(w, dtype)
+    from oracle.numerics import decode
+    ref = osp.matrix_stats(decode(stored, dtype), eta=1e-6)
+    got = P.matrix_stats(_dev(stored), eta=1e-6)
+    F = ref.frob_sq
+    assert got[2] == pytest.approx(F, rel=1e-12)
+    assert abs(got[0] - ref.energy_top) <= 1e-11 * F
+    assert abs(got[1] - ref.energy_tail) <= 1e-11 * F
+    assert got[4] == pytest.approx(ref.g, rel=1e-11)
+    assert got[3] == pytest.approx(ref.scr, rel=1e-6, abs=1e-7)
+
+
+@pytest.mark.parametrize("name", MINIS + ["tiny"])
+def test_schedule_bit_exact(P, name):
+    cfg, w, x = workload(name)
+    dm = P.DeviceModel(cfg, w, x)
+    for pct in cfg.budgets:
+        raw, lam, bs = oracle_schedule(cfg, w, pct)
+        n = osch.budget_layer_steps(pct, cfg.L, cfg.T)
+        got = P.schedule_build(dm.scored_units(), [cfg.dh] * cfg.L, cfg.T, budget=n)
+        assert np.allclose(got.unit_raw, raw, rtol=1e-11)
+        assert np.allclose(got.unit_score, lam, rtol=1e-11)
+        assert bs.cut_margin > 1e-9, "near-tie: the comparison below would be fragile"
+        assert np.array_equal(got.lifetimes, bs.lifetimes)
+        assert np.array_equal(got.active, osch.active_mask(bs.lifetimes, cfg.T))
+        assert got.layer_steps == n
+    dm.close()
+
+
+# ---------------------------------------------------------------- trajectories
+
+@pytest.mark.parametrize("name", MINIS)
+def test_step_parity_teacher_forced(P, name):
+    """Every step s = 1..T of the scheduled trajectory, fed the oracle's state z_s, matches the
+    oracle's z_{s+1}: the per-step bar of 1e-4 (fp32) / 2e-2 (bf16)."""
+    cfg, w, x = workload(name)
+    dm = P.DeviceModel(cfg, w, x)
+    pct = cfg.budgets[-1]
+    _, _, bs = oracle_schedule(cfg, w, pct)
+    mask = osch.active_mask(bs.lifetimes, cfg.T)
+    ref = oracle_trajectory(cfg, w, x, mask)
+    n = osch.budget_layer_steps(pct, cfg.L, cfg.T)
+    sched = P.schedule_build(dm.scored_units(), [cfg.dh] * cfg.L, cfg.T, budget=n)  # end to end on the GPU
+    assert np.array_equal(sched.lifetimes, bs.lifetimes)
+    got = gpu_teacher_forced(dm, cfg, ref.z, x["z"], sched)
+    errs = [rel_err(g, r) for g, r in zip(got, ref.z)]
+    print(name, "teacher-forced per-step error", ["%.2e" % e for e in errs])
+    assert max(errs) <= TOL[cfg.dtype], errs
+    dm.close()
+
+
+@pytest.mark.parametrize("name", MINIS)
+def test_trajectory_parity(P, name):
+    """Free-running scheduled trajectory.  fp32: 1e-4 at every step.  bf16: the bf16-quantised
+    map amplifies any rounding difference, so the bound is max(2e-2, twice the oracle's own
+    divergence under a 1e-7 relative perturbation of its initial state)."""
+    cfg, w, x = workload(name)
+    dm = P.DeviceModel(cfg, w, x)
+    pct = cfg.budgets[-1]
+    _, _, bs = oracle_schedule(cfg, w, pct)
+    mask = osch.active_mask(bs.lifetimes, cfg.T)
+    n = osch.budget_layer_steps(pct, cfg.L, cfg.T)
+    sched = P.schedule_build(dm.scored_units(), [cfg.dh] * cfg.L, cfg.T, budget=n)
+    assert np.array_equal(sched.lifetimes, bs.lifetimes)
+    got = gpu_trajectory(dm, cfg, x, sched)
+    if cfg.dtype == "f32":
+        ref = oracle_trajectory(cfg, w, x, mask)
+        bounds = [TOL["f32"]] * cfg.T
+    else:
+        ref, floor = chaos_floor(cfg, w, x, mask)
+        bounds = [max(TOL["bf16"], 2 * f) for f in floor]
+        print(name, "oracle self-divergence", ["%.2e" % e for e in floor])
+    errs = [rel_err(g, r) for g, r in zip(got, ref.z)]
+    print(name, "free-running per-step error", ["%.2e" % e for e in errs])
+    assert all(e <= b for e, b in zip(errs, bounds)), (errs, bounds)
+    dm.close()
+
+
+@pytest.mark.parametrize("name", MINIS)
+def test_all_active_equals_unscheduled_bitwise(P, name):
+    cfg, w, x = workload(name)
+    dm = P.DeviceModel(cfg, w, x)
+    steps = min(cfg.T, 3)
+    a = gpu_trajectory(dm, cfg, x, P.schedule_from_lifetimes([cfg.T] * cfg.L, cfg.T), steps)
+    b = gpu_trajectory(dm, cfg, x, None, steps)
+    c = gpu_trajectory(dm, cfg, x, None, steps)
+    for za, zb, zc in zip(a, b, c):
+        assert np.array_equal(za, zb)
+        assert np.array_equal(zb, zc)  # deterministic
+    dm.close()
+
+
+@pytest.mark.parametrize("name", ["llada_mini", "uvit_mini", "dit_mini"])
+def test_frozen_early(P, name):
+    """Lifetimes of 1 freeze units from step 2 on: the frozen path carries most of the trajectory."""
+    cfg, w, x = workload(name)
+    dm = P.DeviceModel(cfg, w, x)
+    S = np.array([1 + (l % 3) for l in range(cfg.L)])
+    mask = osch.active_mask(S, cfg.T)
+    ref = oracle_trajectory(cfg, w, x, mask)
+    got = gpu_trajectory(dm, cfg, x, P.schedule_from_lifetimes(S, cfg.T))
+    errs = [rel_err(g, r) for g, r in zip(got, ref.z)]
+    print(name, "per-step error", ["%.2e" % e for e in errs])
+    assert max(errs) <= TOL[cfg.dtype], errs
+    dm.close()
+
+
+def test_step_errors(P):
+    cfg, w, x = workload("llada_mini")
+    dm = P.DeviceModel(cfg, w, x)
+    import torch
+    z = torch.from_numpy(x["z"].copy()).cuda()
+    cache = P.Cache(dm)
+    a = P.schedule_from_lifetimes([5] * cfg.L, cfg.T)
+    b = P.schedule_from_lifetimes([1] * cfg.L, cfg.T)
+    with pytest.raises(P.SgdError) as e:
+        dm.step(z, 2, a, cache)  # out of order
+    assert e.value.code == -5
+    dm.step(z, 1, a, cache)
+    with pytest.raises(P.SgdError) as e:
+        dm.step(z, 2, b, cache)  # frozen, but schedule a never wrote the slot
+    assert e.value.code == -6
+    with pytest.raises(P.SgdError) as e:
+        dm.step(z, cfg.T + 1, None, None)
+    assert e.value.code == -5
+    torch.cuda.synchronize()
+    dm.close()
