@@ -60,6 +60,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-units", type=int, default=2, help="oracle sample: units of one all-active step")
     ap.add_argument("--profile-kernel", default="gemm_w1")
+    ap.add_argument("--save-lifetimes", default="", help="write the built lifetimes (JSON) here")
+    ap.add_argument("--lifetimes", default="", help="reuse lifetimes saved by --save-lifetimes "
+                    "instead of rebuilding the spectra (e.g. under a kernel tracer)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md, 'Sharding').",
@@ -84,7 +87,9 @@ def main() -> int:
     log(f"config {cfg.name}: B={cfg.B} N={cfg.N} d={cfg.d} F={cfg.F} L={L} T={T}; generating weights")
     t0 = time.time()
     cache_dir = os.environ.get("SGD_SYNTH_CACHE") or "/tmp/sgd_synth_cache"
-    weights = synth.model_weights(cfg, workers=min(16, os.cpu_count() or 1), cache_dir=cache_dir)
+    done = []
+    weights = synth.model_weights(cfg, workers=min(16, os.cpu_count() or 1), cache_dir=cache_dir,
+                                  progress=lambda u: (done.append(u), log(f"unit {u} ready ({len(done)}/{L})")))
     inputs = synth.inputs(cfg)
     log(f"weights ready in {time.time() - t0:.1f}s; uploading")
     torch.cuda.set_device(0)
@@ -94,11 +99,25 @@ def main() -> int:
 
     t0 = time.time()
     scheds = {}
+    n_head = P.budget_layer_steps(head, L, T)
+    if args.lifetimes:
+        saved = json.load(open(args.lifetimes))
+        for pct in budgets:
+            scheds[pct] = P.schedule_from_lifetimes(saved[str(pct)], T)
+    else:
+        scheds[head] = P.schedule_build(dm.scored_units(), [cfg.dh] * L, T, budget=n_head)
+    t_build = time.time() - t0
     for pct in budgets:
-        n = P.budget_layer_steps(pct, L, T)
-        scheds[pct] = P.schedule_build(dm.scored_units(), [cfg.dh] * L, T, budget=n)
-        log(f"budget {pct}%: N*={n} lifetimes={list(scheds[pct].lifetimes)} margin={scheds[pct].cut_margin:.3g}")
-    log(f"schedules built in {time.time() - t0:.1f}s (offline, not timed)")
+        if args.lifetimes:
+            continue
+        if pct != head:  # same spectra, lifetimes at another budget
+            scheds[pct] = P.schedule_from_scores(scheds[head].unit_score, T, budget=P.budget_layer_steps(pct, L, T))
+        log(f"budget {pct}%: N*={scheds[pct].layer_steps} lifetimes={scheds[pct].lifetimes.tolist()} "
+            f"margin={scheds[pct].cut_margin:.3g}")
+    log(f"schedule ready in {t_build:.1f}s (spectra of {sum(len(u) for u in dm.scored_units())} matrices; "
+        f"offline, not timed)")
+    if args.save_lifetimes:
+        json.dump({str(p): scheds[p].lifetimes.tolist() for p in budgets}, open(args.save_lifetimes, "w"))
     all_active = P.schedule_from_lifetimes([T] * L, T)
 
     z0 = torch.from_numpy(inputs["z"]).cuda()

@@ -21,7 +21,7 @@ enum sgd_act { SGD_ACT_NONE = 0, SGD_ACT_GELU_ERF = 1, SGD_ACT_GELU_TANH = 2, SG
 /* out[M x N] = act(A[M x K] W[N x K]^T + bias) in dtype (the branch GEMM of an MLP input
  * projection).  gated != 0: W is [2N x K] = [W_gate; W_up] and out = act(A W_gate^T +
  * b[:N]) * (A W_up^T + b[N:]).  lda/ldw/ldo are row strides in elements.  tile selects a
- * block tile for bf16 (0 auto, 1: 256x256, 2: 256x128, 3: 128x128).  Shape limits:
+ * bf16 kernel variant (0 auto; 1..7 fixed block tiles, for tests and sweeps).  Shape limits:
  * K % 64 == 0 and N % tile width == 0 (bf16), K % 16 == 0 and N % 64 == 0 (fp32). */
 int sgd_op_linear(int32_t dtype, const void* A, int64_t lda, const void* W, int64_t ldw, const float* bias,
                   void* out, int64_t ldo, int32_t M, int32_t N, int32_t K, int32_t act, int32_t gated,

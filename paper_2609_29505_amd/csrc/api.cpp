@@ -487,7 +487,7 @@ extern "C" int sgd_op_linear(int32_t dtype, const void* A, int64_t lda, const vo
                              int32_t act, int32_t gated, int32_t tile, void* hip_stream) {
     if (!A || !W || !out) return fail(SGD_E_ARG, "NULL argument");
     if (dtype != SGD_F32 && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
-    if (act < 0 || act > 3 || tile < 0 || tile > 3) return fail(SGD_E_ARG, "bad act or tile");
+    if (act < 0 || act > 3 || tile < 0 || tile > 13) return fail(SGD_E_ARG, "bad act or tile");
     if (gated && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "gated GEMMs are bf16 only");
     GemmArgs g;
     g.A0 = A; g.lda0 = lda; g.B = W; g.ldb = ldw; g.M = M; g.N = gated ? 2 * N : N; g.K = K;

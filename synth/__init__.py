@@ -313,18 +313,25 @@ def unit_weights(cfg: Config, unit: int, keep_planted: bool = False) -> Dict[str
     return out
 
 
-def model_weights(cfg: Config, workers: int = 0, cache_dir: Optional[str] = None
-                  ) -> List[Dict[str, np.ndarray]]:
+def model_weights(cfg: Config, workers: int = 0, cache_dir: Optional[str] = None,
+                  progress=None) -> List[Dict[str, np.ndarray]]:
     """Weights of every unit.
 
     ``workers > 1`` generates units in a thread pool.  ``cache_dir`` (or the
     ``SGD_SYNTH_CACHE`` environment variable) names a directory where each
     unit is stored as an uncompressed ``.npz`` after its first generation.
+    ``progress(unit)`` is called after each unit is ready.
     """
     import os
     cache_dir = cache_dir or os.environ.get("SGD_SYNTH_CACHE") or None
 
     def one(u: int) -> Dict[str, np.ndarray]:
+        w = _one(u)
+        if progress is not None:
+            progress(u)
+        return w
+
+    def _one(u: int) -> Dict[str, np.ndarray]:
         if cache_dir:
             path = os.path.join(cache_dir, f"{cfg.name}_{cfg.cfg_id}_{cfg.d}_{cfg.F}_u{u}.npz")
             if os.path.exists(path):
