@@ -14,13 +14,30 @@
 
 namespace sgd {
 
-template <int DHP>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, float scale_log2) {
-    constexpr int BQ = 128, BKV = 64;
+// {v[l], v[l ^ 32]} combined across the two 32-lane halves of the wave (one lane swap)
+__device__ __forceinline__ float pair_max(float v) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float v) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Lazy rescaling: the running reference m of a lane is raised only when its block maximum
+// exceeds it by more than 2^8 (checked for the whole wave at once); probabilities are then
+// exp2(s - m) <= 256, exact in fp32 and in bf16's 8-bit exponent range.
+constexpr float kRescaleSlack = 8.0f;
+
+template <int DHP, int NW>
+__global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float scale_log2) {
+    constexpr int BQ = 32 * NW, BKV = 64, NT = NW * 64;
     constexpr int KS = DHP / 16, DT = DHP / 32;
-    constexpr int KLDS = DHP + 8, VLDS = BKV + 8;
-    __shared__ __attribute__((aligned(16))) bf16 sk[BKV * KLDS];
-    __shared__ __attribute__((aligned(16))) bf16 sv[DHP * VLDS];
+    constexpr int KLDS = DHP + 8, VLDS = BKV + 8;        // padded rows: conflict-free fragment reads
+    constexpr int K_CH = BKV * (DHP / 8) / NT;            // 16-byte chunks per thread per block (upper bound)
+    constexpr int V_CH = DHP * (BKV / 8) / NT;
+    __shared__ __attribute__((aligned(16))) bf16 sk[2][BKV * KLDS];
+    __shared__ __attribute__((aligned(16))) bf16 sv[2][DHP * VLDS];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int bh = blockIdx.y;
@@ -33,14 +50,14 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, float scale_
     const bf16* K = (const bf16*)a.k + (long)bh * a.npk * dh;
     const bf16* VT = (const bf16*)a.vt + (long)bh * dh * a.npk;
 
-    // zero the padded head dims once (never overwritten by the loads below)
-    for (int i = tid; i < BKV * (DHP - dh); i += 256) {
-        int r = i / (DHP - dh), c = dh + i % (DHP - dh);
-        sk[r * KLDS + c] = f2bf(0.f);
+    // zero the padded head dims of both buffers once (the loads below never write them)
+    for (int i = tid; i < 2 * BKV * (DHP - dh); i += NT) {
+        const int buf = i / (BKV * (DHP - dh)), j = i % (BKV * (DHP - dh));
+        sk[buf][(j / (DHP - dh)) * KLDS + dh + j % (DHP - dh)] = f2bf(0.f);
     }
-    for (int i = tid; i < (DHP - dh) * BKV; i += 256) {
-        int r = dh + i / BKV, c = i % BKV;
-        sv[r * VLDS + c] = f2bf(0.f);
+    for (int i = tid; i < 2 * (DHP - dh) * BKV; i += NT) {
+        const int buf = i / ((DHP - dh) * BKV), j = i % ((DHP - dh) * BKV);
+        sv[buf][(dh + j / BKV) * VLDS + j % BKV] = f2bf(0.f);
     }
 
     // this lane's query fragments (B operand of S^T = K Q^T)
@@ -54,6 +71,59 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, float scale_
             for (int e = 0; e < 8; ++e) qf[ks][e] = f2bf(0.f);
     }
 
+    // register prefetch of one key/value block
+    const int kchunks = dh / 8;  // 16-byte chunks per key row
+    u32x4 rk[K_CH], rv[V_CH];
+    auto gload = [&](int k0) {
+#pragma unroll
+        for (int t = 0; t < K_CH; ++t) {
+            const int i = tid + t * NT;
+            if (i < BKV * kchunks) {
+                const int r = i / kchunks, c = (i - r * kchunks) * 8;
+                rk[t] = *(const u32x4*)(K + (long)(k0 + r) * dh + c);
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < V_CH; ++t) {
+            const int i = tid + t * NT;
+            if (i < dh * (BKV / 8)) {
+                const int r = i >> 3, c = (i & 7) * 8;
+                rv[t] = *(const u32x4*)(VT + (long)r * a.npk + k0 + c);
+            }
+        }
+    };
+    auto lstore = [&](int k0, int buf) {
+#pragma unroll
+        for (int t = 0; t < K_CH; ++t) {
+            const int i = tid + t * NT;
+            if (i < BKV * kchunks) {
+                const int r = i / kchunks, c = (i - r * kchunks) * 8;
+                *(u32x4*)(&sk[buf][r * KLDS + c]) = rk[t];
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < V_CH; ++t) {
+            const int i = tid + t * NT;
+            if (i < dh * (BKV / 8)) {
+                const int r = i >> 3, c = (i & 7) * 8;
+                bf16x8 v = __builtin_bit_cast(bf16x8, rv[t]);
+                if (k0 + c + 8 > a.nk) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (k0 + c + e >= a.nk) v[e] = f2bf(0.f);
+                }
+                // key order inside a 16-key group: 0-3, 8-11, 4-7, 12-15, so the keys
+                // {0-3, 8-11} (lanes 0-31) and {4-7, 12-15} (lanes 32-63) are contiguous
+                const int g16 = c & ~15, hi8 = (c & 8) ? 4 : 0;
+                bf16x4 v0, v1;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) { v0[e] = v[e]; v1[e] = v[4 + e]; }
+                *(bf16x4*)(&sv[buf][r * VLDS + g16 + hi8]) = v0;
+                *(bf16x4*)(&sv[buf][r * VLDS + g16 + 8 + hi8]) = v1;
+            }
+        }
+    };
+
     f32x16 o[DT];
 #pragma unroll
     for (int t = 0; t < DT; ++t)
@@ -61,26 +131,15 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, float scale_
         for (int r = 0; r < 16; ++r) o[t][r] = 0.f;
     float m = -INFINITY, lsum = 0.f;
 
-    const int kchunks = dh / 8;  // 16-byte chunks per key row
     const int nkb = (a.nk + BKV - 1) / BKV;
+    gload(0);
+    __syncthreads();  // padding zeroed
+    lstore(0, 0);
+    __syncthreads();
     for (int kb = 0; kb < nkb; ++kb) {
         const int k0 = kb * BKV;
-        __syncthreads();
-        for (int i = tid; i < BKV * kchunks; i += 256) {
-            const int r = i / kchunks, c = (i - r * kchunks) * 8;
-            *(u32x4*)(sk + r * KLDS + c) = *(const u32x4*)(K + (long)(k0 + r) * dh + c);
-        }
-        for (int i = tid; i < dh * (BKV / 8); i += 256) {
-            const int r = i >> 3, c = (i & 7) * 8;
-            bf16x8 v = *(const bf16x8*)(VT + (long)r * a.npk + k0 + c);
-            if (k0 + c + 8 > a.nk) {
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    if (k0 + c + e >= a.nk) v[e] = f2bf(0.f);
-            }
-            *(bf16x8*)(sv + r * VLDS + c) = v;
-        }
-        __syncthreads();
+        const int buf = kb & 1;
+        if (kb + 1 < nkb) gload(k0 + BKV);  // in flight while this block computes
 
         f32x16 s[2];
 #pragma unroll
@@ -89,40 +148,52 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, float scale_
             for (int r = 0; r < 16; ++r) s[t][r] = 0.f;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                bf16x8 kf = *(const bf16x8*)(sk + (t * 32 + (lane & 31)) * KLDS + ks * 16 + half * 8);
+                bf16x8 kf = *(const bf16x8*)(&sk[buf][(t * 32 + (lane & 31)) * KLDS + ks * 16 + half * 8]);
                 s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[t], 0, 0, 0);
             }
         }
-        // scale into the log2 domain, mask keys beyond nk, block maximum
+        // scale into the log2 domain (masking keys beyond nk in the tail block only), block max
         float bm = -INFINITY;
+        if (k0 + BKV <= a.nk) {
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+            for (int t = 0; t < 2; ++t)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int key = k0 + t * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-                float v = s[t][r] * scale_log2;
-                v = key < a.nk ? v : -INFINITY;
-                s[t][r] = v;
-                bm = fmaxf(bm, v);
-            }
-        bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
-        const float mn = fmaxf(m, bm);
-        const float alpha = exp2f(m - mn);
-        m = mn;
+                for (int r = 0; r < 16; ++r) {
+                    s[t][r] *= scale_log2;
+                    bm = fmaxf(bm, s[t][r]);
+                }
+        } else {
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int key = k0 + t * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+                    const float v = key < a.nk ? s[t][r] * scale_log2 : -INFINITY;
+                    s[t][r] = v;
+                    bm = fmaxf(bm, v);
+                }
+        }
+        bm = pair_max(bm);
+        if (__builtin_amdgcn_ballot_w64(bm > m + kRescaleSlack)) {
+            const float mn = fmaxf(m, bm);
+            const float alpha = __builtin_amdgcn_exp2f(m - mn);
+            m = mn;
+            lsum *= alpha;
+#pragma unroll
+            for (int t = 0; t < DT; ++t)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+        }
         float ps = 0.f;
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const float p = exp2f(s[t][r] - mn);
+                const float p = __builtin_amdgcn_exp2f(s[t][r] - m);
                 s[t][r] = p;
                 ps += p;
             }
-        lsum = lsum * alpha + ps;
-#pragma unroll
-        for (int t = 0; t < DT; ++t)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+        lsum += ps;
 
         // O^T += V^T P^T over the block's 64 keys, 16 at a time
 #pragma unroll
@@ -132,22 +203,19 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a, float scale_
                 bf16x8 pf;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) pf[e] = f2bf(s[t][8 * k2 + e]);
-                const int kc = t * 32 + 16 * k2 + half * 4;
+                const int kc = t * 32 + 16 * k2 + half * 8;  // permuted key order (see lstore)
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) {
-                    const bf16* vr = sv + (dt * 32 + (lane & 31)) * VLDS + kc;
-                    bf16x4 lo = *(const bf16x4*)vr;
-                    bf16x4 hi = *(const bf16x4*)(vr + 8);
-                    bf16x8 vf;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) { vf[e] = lo[e]; vf[4 + e] = hi[e]; }
+                    const bf16x8 vf = *(const bf16x8*)(&sv[buf][(dt * 32 + (lane & 31)) * VLDS + kc]);
                     o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[dt], 0, 0, 0);
                 }
             }
         }
+        if (kb + 1 < nkb) lstore(k0 + BKV, buf ^ 1);  // the other buffer: nobody reads it now
+        __syncthreads();
     }
 
-    const float l = lsum + __shfl_xor(lsum, 32, 64);
+    const float l = pair_sum(lsum);
     const float inv = 1.0f / l;
     if (q < a.nq) {
         bf16* O = (bf16*)a.o + ((long)b * a.nq + q) * ((long)a.H * dh) + (long)hh * dh;
@@ -234,10 +302,19 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st) {
     const int BH = a.B * a.H;
     if (dtype == 1) {
         const float sl2 = (float)(1.4426950408889634 / sqrt((double)a.dh));
-        dim3 grid((a.nq + 127) / 128, BH), block(256);
-        if (a.dh <= 64) hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, st, a, sl2);
-        else if (a.dh <= 96) hipLaunchKernelGGL(attn_bf16_kernel<96>, grid, block, 0, st, a, sl2);
-        else hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, st, a, sl2);
+        // two-wave workgroups when four-wave ones would leave CUs without a second workgroup
+        const bool small = (long)((a.nq + 127) / 128) * BH < 1024;
+        if (small) {
+            dim3 grid((a.nq + 63) / 64, BH), block(128);
+            if (a.dh <= 64) hipLaunchKernelGGL((attn_bf16_kernel<64, 2>), grid, block, 0, st, a, sl2);
+            else if (a.dh <= 96) hipLaunchKernelGGL((attn_bf16_kernel<96, 2>), grid, block, 0, st, a, sl2);
+            else hipLaunchKernelGGL((attn_bf16_kernel<128, 2>), grid, block, 0, st, a, sl2);
+        } else {
+            dim3 grid((a.nq + 127) / 128, BH), block(256);
+            if (a.dh <= 64) hipLaunchKernelGGL((attn_bf16_kernel<64, 4>), grid, block, 0, st, a, sl2);
+            else if (a.dh <= 96) hipLaunchKernelGGL((attn_bf16_kernel<96, 4>), grid, block, 0, st, a, sl2);
+            else hipLaunchKernelGGL((attn_bf16_kernel<128, 4>), grid, block, 0, st, a, sl2);
+        }
     } else {
         const float sc = (float)(1.0 / sqrt((double)a.dh));
         dim3 grid((a.nq + 63) / 64, BH), block(64);
