@@ -223,11 +223,12 @@ def cpu_baseline(cfg, weights, inputs, sched, n_units):
     import dataclasses
     small = dataclasses.replace(cfg, L=n_units)
     log(f"cpu baseline: oracle on {n_units} units of an all-active step ({threads} threads)")
-    m = om.Model(small, sub, inputs)
+    m = om.Model(small, sub, inputs, lazy=True)
     h = om.initial_stream(m, inputs["z"], 1)
     t0 = time.time()
     for l in range(n_units):
-        h, _ = m.unit_active(l, h, om.timestep_value(1, cfg.T))
+        cross = m.cross_kv(m.units[l]) if cfg.arch == "sdxl" else None
+        h, _ = m.unit_active(l, h, om.timestep_value(1, cfg.T), cross)
     dt = time.time() - t0
     per_unit = dt / n_units
     mean_active = float(np.asarray(sched.active, np.float64).sum(axis=1).mean())

@@ -126,28 +126,47 @@ def merge_heads(x: np.ndarray) -> np.ndarray:
 # model
 # --------------------------------------------------------------------------
 
+def _decode_unit(w: Dict[str, np.ndarray], dt: str) -> Dict[str, np.ndarray]:
+    u = {}
+    for name, arr in w.items():
+        if name.startswith("_"):
+            continue
+        u[name] = decode(arr, dt) if name.startswith("w") else np.asarray(arr, np.float64)
+    return u
+
+
+class _LazyUnits:
+    def __init__(self, weights, dt):
+        self.weights, self.dt = weights, dt
+
+    def __len__(self):
+        return len(self.weights)
+
+    def __getitem__(self, l):
+        return _decode_unit(self.weights[l], self.dt)
+
+    def __iter__(self):
+        return (self[l] for l in range(len(self)))
+
+
 class Model:
     """One workload's weights decoded to float64, plus its architecture rules."""
 
-    def __init__(self, cfg, weights: List[Dict[str, np.ndarray]], inputs: Dict[str, np.ndarray]):
+    def __init__(self, cfg, weights: List[Dict[str, np.ndarray]], inputs: Dict[str, np.ndarray],
+                 lazy: bool = False):
+        """``lazy`` decodes a unit's weights each time the unit runs instead of keeping every
+        unit in float64 (for the full-size workloads)."""
         self.cfg = cfg
         self.arch = cfg.arch
         self.prec = Precision(cfg.dtype == "bf16")
-        dt = cfg.dtype
-        self.units = []
-        for w in weights:
-            u = {}
-            for name, arr in w.items():
-                if name.startswith("_"):
-                    continue
-                u[name] = decode(arr, dt) if name.startswith("w") else np.asarray(arr, np.float64)
-            self.units.append(u)
+        self._raw = weights
+        self.units = _LazyUnits(weights, cfg.dtype) if lazy else [_decode_unit(w, cfg.dtype) for w in weights]
         self.class_emb = inputs.get("class_emb")
         if self.class_emb is not None:
             self.class_emb = np.asarray(self.class_emb, np.float64)
         self.ctx = inputs.get("ctx")
         if self.ctx is not None:
-            self.ctx = decode(self.ctx, dt)
+            self.ctx = decode(self.ctx, cfg.dtype)
 
     # ---- U-ViT structure ------------------------------------------------
     def skip_source(self, l: int) -> int:
