@@ -21,8 +21,10 @@ enum sgd_act { SGD_ACT_NONE = 0, SGD_ACT_GELU_ERF = 1, SGD_ACT_GELU_TANH = 2, SG
 /* out[M x N] = act(A[M x K] W[N x K]^T + bias) in dtype (the branch GEMM of an MLP input
  * projection).  gated != 0: W is [2N x K] = [W_gate; W_up] and out = act(A W_gate^T +
  * b[:N]) * (A W_up^T + b[N:]).  lda/ldw/ldo are row strides in elements.  tile selects a
- * bf16 kernel variant (0 auto; 1..7 fixed block tiles, for tests and sweeps).  Shape limits:
- * K % 64 == 0 and N % tile width == 0 (bf16), K % 16 == 0 and N % 64 == 0 (fp32). */
+ * bf16 kernel variant (0 auto; 1..4 fixed block tiles, for tests and sweeps: 1 256x256,
+ * 2 256x128, 3 128x256, 4 128x128, rows x columns).  Shape limits (bf16): K % 64 == 0,
+ * N % 4 == 0, gated N a multiple of the tile width, operand rows and bias 16-byte aligned;
+ * (fp32): K % 16 == 0, N % 64 == 0. */
 int sgd_op_linear(int32_t dtype, const void* A, int64_t lda, const void* W, int64_t ldw, const float* bias,
                   void* out, int64_t ldo, int32_t M, int32_t N, int32_t K, int32_t act, int32_t gated,
                   int32_t tile, void* hip_stream);
@@ -44,17 +46,20 @@ int sgd_op_norm(int32_t dtype, int32_t kind, const float* x, void* y, int32_t M,
  * (+ bias), column n of P belongs to projection which0 + n / d (0: q, 1: k, 2: v^T), head
  * (n % d) / dh, dim n % dh; row r is token r % ntok of sample r / ntok.  q, k are
  * [B*H, np, dh], vt is [B*H, dh, np].  rope != 0 rotates the q and k pairs (i, i + dh/2) of
- * token t by t * 10000^(-2i/dh) (dh must be 128).  Padded tokens (>= ntok) are not written. */
+ * token t by t * 10000^(-2i/dh) (bf16 only; every block tile must hold whole heads: H*dh a
+ * multiple of the tile width, dh a multiple of 8 dividing it).  Padded tokens (>= ntok) are not
+ * written.  tile as for sgd_op_linear. */
 int sgd_op_heads(int32_t dtype, const void* A, const void* W, const float* bias, void* q, void* k, void* vt,
                  int32_t M, int32_t K, int32_t n_proj, int32_t which0, int32_t ntok, int32_t np, int32_t H,
-                 int32_t dh, int32_t rope, void* hip_stream);
+                 int32_t dh, int32_t rope, int32_t tile, void* hip_stream);
 
 /* Residual projection of a branch (the O and W2 GEMMs): v = (A[M x K] W[N x K]^T + bias),
  * v *= gate[r / ntok] if gate != NULL (rows gate_ld apart), then h += v (fp32 [M x N]);
- * delta_mode 1 stores v into delta, 2 adds v to delta (the cached update of Sec. 3.1). */
+ * delta_mode 1 stores v into delta, 2 adds v to delta (the cached update of Sec. 3.1).  tile as
+ * for sgd_op_linear. */
 int sgd_op_residual(int32_t dtype, const void* A, int64_t lda, const void* W, const float* bias, float* h,
                     float* delta, int32_t delta_mode, const float* gate, int64_t gate_ld, int32_t ntok,
-                    int32_t M, int32_t N, int32_t K, void* hip_stream);
+                    int32_t M, int32_t N, int32_t K, int32_t tile, void* hip_stream);
 
 /* h <- h + delta[0] + ... + delta[r-1] elementwise over n fp32 values (n % 4 == 0), in
  * that order (the frozen-unit update of Sec. 3.1 for a run of r frozen units). */

@@ -114,8 +114,8 @@ def lib() -> C.CDLL:
             "sgd_op_attention": [i32, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp],
             "sgd_op_norm": [i32, i32, vp, vp, i32, i32, C.c_float, vp, vp, vp, vp, i64, i32, vp],
             "sgd_op_frozen_run": [vp, C.POINTER(vp), i32, i64, vp],
-            "sgd_op_heads": [i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, i32, vp],
-            "sgd_op_residual": [i32, vp, i64, vp, vp, vp, vp, i32, vp, i64, i32, i32, i32, i32, vp],
+            "sgd_op_heads": [i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, vp],
+            "sgd_op_residual": [i32, vp, i64, vp, vp, vp, vp, i32, vp, i64, i32, i32, i32, i32, i32, vp],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -273,19 +273,19 @@ def op_norm(kind, x, y, eps, w=None, b=None, shift=None, scale=None, ntok=1, str
                              mod_ld, ntok, C.c_void_p(_stream_ptr(stream))))
 
 
-def op_heads(A, W, q, k, vt, n_proj, which0, ntok, H, dh, bias=None, rope=False, stream=None) -> None:
+def op_heads(A, W, q, k, vt, n_proj, which0, ntok, H, dh, bias=None, rope=False, tile=0, stream=None) -> None:
     M, K = A.shape
     np_ = (q if q is not None else k).shape[-2]
     _check(lib().sgd_op_heads(_dtype_code(A), _p(A), _p(W), _p(bias), _p(q), _p(k), _p(vt), M, K, n_proj, which0,
-                              ntok, np_, H, dh, int(rope), C.c_void_p(_stream_ptr(stream))))
+                              ntok, np_, H, dh, int(rope), tile, C.c_void_p(_stream_ptr(stream))))
 
 
-def op_residual(A, W, h, bias=None, delta=None, delta_mode=0, gate=None, ntok=1, stream=None) -> None:
+def op_residual(A, W, h, bias=None, delta=None, delta_mode=0, gate=None, ntok=1, tile=0, stream=None) -> None:
     M, K = A.shape
     N = h.shape[1]
     gate_ld = gate.stride(0) if gate is not None else 0
     _check(lib().sgd_op_residual(_dtype_code(A), _p(A), A.stride(0), _p(W), _p(bias), _p(h), _p(delta), delta_mode,
-                                 _p(gate), gate_ld, ntok, M, N, K, C.c_void_p(_stream_ptr(stream))))
+                                 _p(gate), gate_ld, ntok, M, N, K, tile, C.c_void_p(_stream_ptr(stream))))
 
 
 def op_frozen_run(h, deltas, stream=None) -> None:

@@ -487,7 +487,7 @@ extern "C" int sgd_op_linear(int32_t dtype, const void* A, int64_t lda, const vo
                              int32_t act, int32_t gated, int32_t tile, void* hip_stream) {
     if (!A || !W || !out) return fail(SGD_E_ARG, "NULL argument");
     if (dtype != SGD_F32 && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
-    if (act < 0 || act > 3 || tile < 0 || tile > 13) return fail(SGD_E_ARG, "bad act or tile");
+    if (act < 0 || act > 3 || tile < 0 || tile > kGemmTiles) return fail(SGD_E_ARG, "bad act or tile");
     if (gated && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "gated GEMMs are bf16 only");
     GemmArgs g;
     g.A0 = A; g.lda0 = lda; g.B = W; g.ldb = ldw; g.M = M; g.N = gated ? 2 * N : N; g.K = K;
@@ -501,7 +501,8 @@ extern "C" int sgd_op_linear(int32_t dtype, const void* A, int64_t lda, const vo
 
 extern "C" int sgd_op_heads(int32_t dtype, const void* A, const void* W, const float* bias, void* q, void* k,
                             void* vt, int32_t M, int32_t K, int32_t n_proj, int32_t which0, int32_t ntok, int32_t np,
-                            int32_t H, int32_t dh, int32_t rope, void* hip_stream) {
+                            int32_t H, int32_t dh, int32_t rope, int32_t tile, void* hip_stream) {
+    if (tile < 0 || tile > kGemmTiles) return fail(SGD_E_ARG, "bad tile");
     if (!A || !W || (which0 == 0 && !q) || (which0 + n_proj > 1 && !k) || (which0 + n_proj > 2 && !vt))
         return fail(SGD_E_ARG, "NULL argument");
     if (dtype != SGD_F32 && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
@@ -513,14 +514,15 @@ extern "C" int sgd_op_heads(int32_t dtype, const void* A, const void* W, const f
     e.kind = EP_HEADS; e.bias = bias; e.q = q; e.k = k; e.vt = vt; e.which0 = which0; e.ntok = ntok; e.np = np;
     e.H = H; e.dh = dh; e.d = H * dh; e.rope = rope; e.rope_log2_theta = (float)std::log2(10000.0);
     const int dt = dtype == SGD_BF16 ? 1 : 0;
-    if (!gemm_shape_ok(dt, g, e)) return fail(SGD_E_SHAPE, "GEMM shape not supported");
-    SGD_HIP_TRY(launch_gemm(dt, g, e, (hipStream_t)hip_stream));
+    if (!gemm_shape_ok(dt, g, e, tile)) return fail(SGD_E_SHAPE, "GEMM shape not supported");
+    SGD_HIP_TRY(launch_gemm(dt, g, e, (hipStream_t)hip_stream, tile));
     return SGD_OK;
 }
 
 extern "C" int sgd_op_residual(int32_t dtype, const void* A, int64_t lda, const void* W, const float* bias, float* h,
                                float* delta, int32_t delta_mode, const float* gate, int64_t gate_ld, int32_t ntok,
-                               int32_t M, int32_t N, int32_t K, void* hip_stream) {
+                               int32_t M, int32_t N, int32_t K, int32_t tile, void* hip_stream) {
+    if (tile < 0 || tile > kGemmTiles) return fail(SGD_E_ARG, "bad tile");
     if (!A || !W || !h || (delta_mode && !delta)) return fail(SGD_E_ARG, "NULL argument");
     if (dtype != SGD_F32 && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
     if (delta_mode < 0 || delta_mode > 2 || ntok < 1) return fail(SGD_E_ARG, "bad delta_mode or ntok");
@@ -530,8 +532,8 @@ extern "C" int sgd_op_residual(int32_t dtype, const void* A, int64_t lda, const 
     e.kind = EP_RESID; e.bias = bias; e.h = h; e.d = N; e.delta = delta; e.delta_mode = delta_mode; e.gate = gate;
     e.gate_ld = gate_ld; e.ntok = ntok;
     const int dt = dtype == SGD_BF16 ? 1 : 0;
-    if (!gemm_shape_ok(dt, g, e)) return fail(SGD_E_SHAPE, "GEMM shape not supported");
-    SGD_HIP_TRY(launch_gemm(dt, g, e, (hipStream_t)hip_stream));
+    if (!gemm_shape_ok(dt, g, e, tile)) return fail(SGD_E_SHAPE, "GEMM shape not supported");
+    SGD_HIP_TRY(launch_gemm(dt, g, e, (hipStream_t)hip_stream, tile));
     return SGD_OK;
 }
 

@@ -38,9 +38,14 @@ struct EpiParams {
     const float* gate = nullptr; long gate_ld = 0; void* hcopy = nullptr;
 };
 
-// dtype: 0 fp32, 1 bf16.  tile: 0 = pick automatically.
+// dtype: 0 fp32, 1 bf16.  tile: 0 = pick automatically; 1..kGemmTiles a fixed bf16 block
+// tile (1: 256x256, 2: 256x128, 3: 128x256, 4: 128x128).
+constexpr int kGemmTiles = 4;
 hipError_t launch_gemm(int dtype, const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile = 0);
 bool gemm_shape_ok(int dtype, const GemmArgs& g, const EpiParams& e, int tile = 0);
+hipError_t launch_gemm_bf16(const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile);
+bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile);
+int gemm_bf16_auto_tile(const GemmArgs& g, const EpiParams& e);
 
 // ---------------------------------------------------------------- attention
 // O[b, i, h*dh + j] = softmax_j'(q_i . k_j' / sqrt(dh)) v_j'  over keys j' < nk.

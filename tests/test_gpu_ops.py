@@ -43,11 +43,13 @@ def relmax(x, ref):
     return float(np.max(np.abs(x - ref)) / np.max(np.abs(ref)))
 
 
-@pytest.mark.parametrize("tile", [0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13])
-@pytest.mark.parametrize("M,N,K", [(200, 256, 128), (300, 768, 192), (64, 1024, 64), (1000, 512, 320), (513, 1024, 448)])
+TILES = [0, 1, 2, 3, 4]
+
+
+@pytest.mark.parametrize("tile", TILES)
+@pytest.mark.parametrize("M,N,K", [(200, 256, 128), (300, 768, 192), (64, 1024, 64), (1000, 512, 320), (513, 1024, 448),
+                                   (130, 200, 64), (257, 580, 128)])
 def test_linear_bf16(P, M, N, K, tile):
-    if N % (256 if tile in (1, 7, 8) else 128):
-        pytest.skip("N not a multiple of the tile width")
     rng = np.random.default_rng(M + N + K)
     A = synth.store(rng.standard_normal((M, K)), "bf16")
     W = synth.store(rng.standard_normal((N, K)) / np.sqrt(K), "bf16")
@@ -74,7 +76,7 @@ def test_linear_act_bf16(P, act):
     assert relmax(host(out), ref) <= 1e-2
 
 
-@pytest.mark.parametrize("tile", [0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13])
+@pytest.mark.parametrize("tile", TILES)
 def test_linear_gated_bf16(P, tile):
     rng = np.random.default_rng(11 + tile)
     M, F, K = 260, 256, 128
@@ -170,12 +172,23 @@ def test_frozen_run_bitwise(P):
     assert np.array_equal(th.cpu().numpy(), ref)
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def _tile_cases():
+    out = []
+    for dtype in ("bf16", "f32"):
+        for tile in (TILES if dtype == "bf16" else [0]):
+            out.append((dtype, tile))
+    return out
+
+
+@pytest.mark.parametrize("dtype,tile", _tile_cases())
 @pytest.mark.parametrize("B,N,H,dh,rope,bias", [(1, 200, 2, 128, True, False), (2, 80, 16, 72, False, True),
-                                                (2, 66, 4, 64, False, False), (1, 130, 2, 128, False, True)])
-def test_heads(P, dtype, B, N, H, dh, rope, bias):
+                                                (2, 66, 4, 64, False, False), (1, 130, 2, 128, False, True),
+                                                (3, 77, 4, 128, True, True)])
+def test_heads(P, dtype, tile, B, N, H, dh, rope, bias):
     if dtype == "f32" and rope:
         pytest.skip("rotary epilogue is bf16 only")
+    if rope and tile in (1, 3) and (H * dh) % 256:
+        pytest.skip("rotary pairs need whole heads in every 256-wide tile")
     rng = np.random.default_rng(N + dh)
     d = H * dh
     M = B * N
@@ -185,7 +198,7 @@ def test_heads(P, dtype, B, N, H, dh, rope, bias):
     b = synth.representable(0.1 * rng.standard_normal(3 * d), dtype) if bias else None
     q, k = empty((B * H, np_, dh), dtype), empty((B * H, np_, dh), dtype)
     vt = empty((B * H, dh, np_), dtype)
-    P.op_heads(dev(A), dev(W), q, k, vt, 3, 0, N, H, dh, bias=dev(b) if bias else None, rope=rope)
+    P.op_heads(dev(A), dev(W), q, k, vt, 3, 0, N, H, dh, bias=dev(b) if bias else None, rope=rope, tile=tile)
     z = decode(A, dtype) @ decode(W, dtype).T + (b if bias else 0)
     Q, K, V = (om.heads(z[:, i * d:(i + 1) * d].reshape(B, N, d), H) for i in range(3))
     if rope:
@@ -199,9 +212,9 @@ def test_heads(P, dtype, B, N, H, dh, rope, bias):
         assert np.max(np.abs(g - r)) <= tol * np.max(np.abs(r))
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype,tile", _tile_cases())
 @pytest.mark.parametrize("M,N,K,gated_rows,mode", [(200, 256, 256, 0, 1), (160, 1152, 1152, 80, 2), (130, 512, 1024, 0, 0)])
-def test_residual(P, dtype, M, N, K, gated_rows, mode):
+def test_residual(P, dtype, tile, M, N, K, gated_rows, mode):
     rng = np.random.default_rng(M + K + mode)
     A = synth.store(rng.standard_normal((M, K)), dtype)
     W = synth.store(rng.standard_normal((N, K)) / np.sqrt(K), dtype)
@@ -212,7 +225,7 @@ def test_residual(P, dtype, M, N, K, gated_rows, mode):
     th, td = dev(h0), dev(d0)
     g_dev = dev(gate)[:, 2 * N:3 * N] if gated_rows else None
     P.op_residual(dev(A), dev(W), th, bias=dev(b), delta=td if mode else None, delta_mode=mode, gate=g_dev,
-                  ntok=gated_rows or 1)
+                  ntok=gated_rows or 1, tile=tile)
     v = decode(A, dtype) @ decode(W, dtype).T + b
     if gated_rows:
         v = v * np.repeat(gate[:, 2 * N:3 * N], gated_rows, axis=0)
@@ -224,3 +237,24 @@ def test_residual(P, dtype, M, N, K, gated_rows, mode):
         assert relmax(host(td), d0 + v) <= 1e-5
     else:
         assert np.array_equal(host(td), d0.astype(np.float64))
+
+
+@pytest.mark.parametrize("tile", TILES)
+def test_heads_kv_only(P, tile):
+    """Key/value projection of a context (which0 = 1): columns [0, d) are k, [d, 2d) are v^T."""
+    rng = np.random.default_rng(77 + tile)
+    B, N, H, dh, K = 3, 77, 5, 64, 192
+    d = H * dh
+    M = B * N
+    np_ = -(-N // 64) * 64
+    A = synth.store(rng.standard_normal((M, K)), "bf16")
+    W = synth.store(rng.standard_normal((2 * d, K)) / np.sqrt(K), "bf16")
+    k, vt = empty((B * H, np_, dh), "bf16"), empty((B * H, dh, np_), "bf16")
+    P.op_heads(dev(A), dev(W), None, k, vt, 2, 1, N, H, dh, tile=tile)
+    z = decode(A, "bf16") @ decode(W, "bf16").T
+    Kr, Vr = (om.heads(z[:, i * d:(i + 1) * d].reshape(B, N, d), H) for i in range(2))
+    got_k = host(k).reshape(B, H, np_, dh)[:, :, :N]
+    got_v = host(vt).reshape(B, H, dh, np_)[:, :, :, :N].transpose(0, 1, 3, 2)
+    for g, r in ((got_k, Kr), (got_v, Vr)):
+        assert np.isfinite(g).all()
+        assert np.max(np.abs(g - r)) <= 2 ** -7 * np.max(np.abs(r))
