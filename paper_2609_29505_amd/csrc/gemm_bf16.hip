@@ -17,6 +17,8 @@
 // vectorised and coalesced and paired columns (gate/up of a gated MLP, the rotary pairs
 // (i, i + dh/2) of a head) are read from LDS whatever the wave layout.  V^T columns of a
 // head projection are written by a column-major pass (consecutive tokens per thread).
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -28,9 +30,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uns
 
 template <bool B> struct BoolC { static constexpr bool value = B; };
 
-template <int BM_, int BN_, int WGM_, int WGN_, int BK_, int STAGES_>
+template <int BM_, int BN_, int WGM_, int WGN_, int BK_, int STAGES_, int OCC_ = 2>
 struct TileCfg {
     static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, BK = BK_, STAGES = STAGES_;
+    static constexpr int OCC = OCC_;                     // waves per SIMD the registers allow
     static constexpr int NW = WGM * WGN;
     static constexpr int NT = NW * 64;
     static constexpr int WM = BM / WGM, WN = BN / WGN;   // wave tile
@@ -41,9 +44,9 @@ struct TileCfg {
     static constexpr int A_BYTES = BM * ROWB, B_BYTES = BN * ROWB;
     static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
     static constexpr int KSTEPS = BK / 16;
-    static constexpr int EPR = WM;                       // epilogue chunk: one wave row
+    static constexpr int EPR = WGM * 32;                 // epilogue chunk: one MFMA row block per wave row
     static constexpr int EPS = BN + 8;                   // fp32 row stride of the staged chunk
-    static constexpr int EPI_BYTES = EPR * EPS * 4;
+    static constexpr int EPI_BYTES = (EPR * EPS + BN) * 4;  // + one row of bias columns
     static constexpr int LDS_BYTES = STAGE_BYTES * STAGES > EPI_BYTES ? STAGE_BYTES * STAGES : EPI_BYTES;
     static_assert(TM >= 1 && TN >= 1 && WM % 32 == 0 && WN % 32 == 0, "wave tile");
     static_assert(BK == 64, "128-byte operand rows: one L2 line per row and chunk-swizzled LDS rows");
@@ -52,185 +55,262 @@ struct TileCfg {
 };
 
 // --------------------------------------------------------------------------- epilogue
+//
+// Every item loop below has a compile-time trip count and runs in two phases, all loads
+// (LDS values, bias, gate, h, delta) first and all stores after: a loop that alternated a
+// global store with the next load made the compiler wait for each store's completion
+// before reusing its registers, one memory round trip per item.
 
-struct Epi4 {
-    EpiParams p;
-    int N;  // product columns
+__device__ __forceinline__ void store_bf16x4(bf16* dst, const float v[4]) {
+    bf16x4 s;
+    s[0] = f2bf(v[0]); s[1] = f2bf(v[1]); s[2] = f2bf(v[2]); s[3] = f2bf(v[3]);
+    *(bf16x4*)dst = s;
+}
+__device__ __forceinline__ f32x4 ld4(const float* p) { return *(const f32x4*)p; }
 
-    __device__ __forceinline__ static void store4(bf16* dst, const float v[4]) {
-        bf16x4 s;
-        s[0] = f2bf(v[0]); s[1] = f2bf(v[1]); s[2] = f2bf(v[2]); s[3] = f2bf(v[3]);
-        *(bf16x4*)dst = s;
-    }
-    __device__ __forceinline__ void add_bias(int n, float v[4]) const {
-        if (p.bias) {
-            const f32x4 b = *(const f32x4*)(p.bias + n);
-            v[0] += b[0]; v[1] += b[1]; v[2] += b[2]; v[3] += b[3];
-        }
-    }
+template <int ACT>
+__device__ __forceinline__ float act_fn(float x) {
+    if (ACT == ACT_GELU_ERF) return gelu_erf(x);
+    if (ACT == ACT_GELU_TANH) return gelu_tanh(x);
+    if (ACT == ACT_SILU) return silu(x);
+    return x;
+}
 
-    // EP_ACT: out[row, n..n+3] = act(v + bias)
-    __device__ __forceinline__ void act(int row, int n, float v[4]) const {
-        add_bias(n, v);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) v[c] = apply_act(p.act, v[c]);
-        store4((bf16*)p.out + (long)row * p.ldo + n, v);
+// calls f(BoolC-like tag) with the activation as a compile-time constant
+template <class Fn>
+__device__ __forceinline__ void with_act(int act, Fn&& f) {
+    switch (act) {
+        case ACT_GELU_ERF: f(std::integral_constant<int, ACT_GELU_ERF>{}); break;
+        case ACT_GELU_TANH: f(std::integral_constant<int, ACT_GELU_TANH>{}); break;
+        case ACT_SILU: f(std::integral_constant<int, ACT_SILU>{}); break;
+        default: f(std::integral_constant<int, ACT_NONE>{}); break;
     }
-    // EP_GATED: out[row, on..on+3] = act(g + b_g) * (u + b_u)
-    __device__ __forceinline__ void gated(int row, int on, float g[4], float u[4]) const {
-        if (p.bias) {
-            const f32x4 bg = *(const f32x4*)(p.bias + on);
-            const f32x4 bu = *(const f32x4*)(p.bias + p.F + on);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) { g[c] += bg[c]; u[c] += bu[c]; }
-        }
-        float o[4];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) o[c] = apply_act(p.act, g[c]) * u[c];
-        store4((bf16*)p.out + (long)row * p.ldo + on, o);
-    }
-    // EP_RESID: v = (acc + bias) [* gate]; h += v; delta = v | delta += v; hcopy = bf16(h)
-    __device__ __forceinline__ void resid(int row, int n, float v[4]) const {
-        add_bias(n, v);
-        if (p.gate) {
-            const f32x4 gt = *(const f32x4*)(p.gate + (long)(row / p.ntok) * p.gate_ld + n);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) v[c] *= gt[c];
-        }
-        const long idx = (long)row * p.d + n;
-        f32x4 hv = *(const f32x4*)(p.h + idx);
-        float hn[4];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) { hn[c] = hv[c] + v[c]; hv[c] = hn[c]; }
-        *(f32x4*)(p.h + idx) = hv;
-        if (p.delta_mode == 1) {
-            *(f32x4*)(p.delta + idx) = f32x4{v[0], v[1], v[2], v[3]};
-        } else if (p.delta_mode == 2) {
-            f32x4 dv = *(const f32x4*)(p.delta + idx);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) dv[c] = dv[c] + v[c];
-            *(f32x4*)(p.delta + idx) = dv;
-        }
-        if (p.hcopy) store4((bf16*)p.hcopy + idx, hn);
-    }
-    // EP_SKIP: h = acc + bias [+ cached delta]; hcopy = bf16(h)
-    __device__ __forceinline__ void skip(int row, int n, float v[4]) const {
-        add_bias(n, v);
-        const long idx = (long)row * p.d + n;
-        if (p.delta_mode == 1) {
-            const f32x4 dv = *(const f32x4*)(p.delta + idx);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) v[c] = v[c] + dv[c];
-        }
-        *(f32x4*)(p.h + idx) = f32x4{v[0], v[1], v[2], v[3]};
-        if (p.hcopy) store4((bf16*)p.hcopy + idx, v);
-    }
-};
+}
 
-// --------------------------------------------------------------------------- epilogue stage
-
-// Stage one wave row of the accumulator tile at a time in LDS, then store it with the
-// epilogue of ep.kind (every thread handles four consecutive columns of a row).
+// Stage the accumulator tile in LDS one MFMA row block per wave row at a time, then store
+// it with the epilogue of ep.kind.  Every thread keeps the same four columns for all its
+// items (NT is a multiple of the items per row), and the tile's bias columns sit in an LDS
+// row of their own, so the q/k/v, activation and gated epilogues issue no global loads.
 template <class C>
 __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds, const GemmArgs& g,
                                          const EpiParams& ep, int m0, int tn, int wm, int wn0) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int lrow = lane & 31, lhalf = lane >> 5;
-    __syncthreads();  // every wave is done with the stage buffers
+    constexpr int RI = C::BN / 4;                        // four-column items per row
+    constexpr int RPT = C::NT / RI;                      // chunk rows per pass of the block
+    constexpr int PER = C::EPR / RPT;                    // items per thread per chunk
+    constexpr int RIG = RI / 2, RPTG = C::NT / RIG, PERG = C::EPR / RPTG;  // gated: gate half
+    constexpr int EB = PER < 4 ? PER : 4;                // residual items per load group
+    static_assert(C::NT % RI == 0 && C::EPR % RPT == 0 && C::EPR % RPTG == 0 && PER % EB == 0, "epilogue split");
     float* st = (float*)lds;
-    Epi4 e{ep, g.N};
+    float* sbias = st + C::EPR * C::EPS;                 // the tile's bias columns
     const int n0 = tn * C::BN;
-    for (int ch = 0; ch < C::WGM; ++ch) {
-        if (wm == ch) {
+    const bool gated = ep.kind == EP_GATED;
+    __syncthreads();  // every wave is done with the stage buffers
+    for (int c = tid; c < C::BN; c += C::NT) {
+        float b = 0.f;
+        if (ep.bias) {
+            if (gated) b = ep.bias[c < C::BN / 2 ? tn * (C::BN / 2) + c : ep.F + tn * (C::BN / 2) + c - C::BN / 2];
+            else if (n0 + c < g.N) b = ep.bias[n0 + c];
+        }
+        sbias[c] = b;
+    }
+    // operand pointers and the token split held in registers before any store (a pointer
+    // picked from the argument block later would be a memory load, and waiting for it
+    // would wait for every store issued before)
+    bf16* const qptr = (bf16*)ep.q;
+    bf16* const kptr = (bf16*)ep.k;
+    // sample of a row: floor((row + 0.5) / ntok) in fp32 is exact while row < 2^21
+    const float rntok = 1.0f / (float)ep.ntok;
+    auto sample_of = [&](int row) { return (int)(((float)row + 0.5f) * rntok); };
+    const int c = (tid % RI) * 4, rr0 = tid / RI;        // this thread's columns and first row
+    const int cg = (tid % RIG) * 4, rrg0 = tid / RIG;    // gated
+    const int n = n0 + c;
+    // q/k columns: projection, head and dims of this thread's columns (fixed), rotary
+    // inverse frequencies of its four dims
+    const int vstart = ep.kind == EP_HEADS ? (2 - ep.which0) * ep.d : 0;
+    int proj = 0, hh = 0, j = 0;
+    float inv[4] = {0.f, 0.f, 0.f, 0.f};
+    if (ep.kind == EP_HEADS && n < g.N && n < vstart) {
+        proj = ep.which0 + n / ep.d;
+        const int nn = n - (proj - ep.which0) * ep.d;
+        hh = nn / ep.dh;
+        j = nn - hh * ep.dh;
+        if (ep.rope) {
+            const int jb = j < ep.dh / 2 ? j : j - ep.dh / 2;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) inv[q] = exp2f(-(2.0f * (float)(jb + q) / (float)ep.dh) * ep.rope_log2_theta);
+        }
+    }
+    // V^T columns straight from the accumulators: in the MFMA output layout lane l holds
+    // column l % 32 of a 32 x 32 block and, for register group q, rows q * 8 + (l / 32) * 4
+    // + 0..3, i.e. four consecutive tokens of one V^T row (d % 32 == 0: a block is all V or
+    // none)
+    if (ep.kind == EP_HEADS) {
+        bf16* vt = (bf16*)ep.vt;
+#pragma unroll
+        for (int jj = 0; jj < C::TN; ++jj) {
+            const int nb = n0 + wn0 + jj * 32;  // first product column of the block
+            if (nb < vstart || nb >= g.N) continue;
+            const int nv = nb + lrow - vstart;
+            const int vh = nv / ep.dh, vj = nv - vh * ep.dh;
+            const float bv = ep.bias ? ep.bias[nb + lrow] : 0.f;
 #pragma unroll
             for (int i = 0; i < C::TM; ++i)
 #pragma unroll
-                for (int j = 0; j < C::TN; ++j)
+                for (int q = 0; q < 4; ++q) {
+                    const int row0 = m0 + wm * C::WM + i * 32 + q * 8 + lhalf * 4;
+                    if (row0 >= g.M) continue;
+                    const int bs0 = sample_of(row0), tok0 = row0 - bs0 * ep.ntok;
+                    float o[4];
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int row = i * 32 + (r >> 2) * 8 + lhalf * 4 + (r & 3);
-                        st[row * C::EPS + wn0 + j * 32 + lrow] = acc[i][j][r];
+                    for (int u = 0; u < 4; ++u) o[u] = acc[i][jj][q * 4 + u] + bv;
+                    if (tok0 % 4 == 0 && tok0 + 3 < ep.ntok && row0 + 3 < g.M) {
+                        store_bf16x4(vt + (((long)bs0 * ep.H + vh) * ep.dh + vj) * ep.np + tok0, o);
+                    } else {
+                        for (int u = 0; u < 4; ++u) {
+                            const int row = row0 + u;
+                            if (row >= g.M) break;
+                            const int bs = sample_of(row), tok = row - bs * ep.ntok;
+                            vt[(((long)bs * ep.H + vh) * ep.dh + vj) * ep.np + tok] = f2bf(o[u]);
+                        }
                     }
+                }
+        }
+    }
+    // chunk ch holds MFMA row block ch of every wave row, so each wave's accumulators die
+    // chunk by chunk; chunk row rr is tile row (rr / 32) * WM + ch * 32 + rr % 32
+#pragma unroll 1
+    for (int ch = 0; ch < C::TM; ++ch) {
+        // static register indices: the chunk loop itself is not unrolled
+#pragma unroll
+        for (int i = 0; i < C::TM; ++i) {
+            if (i != ch) continue;
+#pragma unroll
+            for (int jj = 0; jj < C::TN; ++jj)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int row = wm * 32 + (r >> 2) * 8 + lhalf * 4 + (r & 3);
+                    st[row * C::EPS + wn0 + jj * 32 + lrow] = acc[i][jj][r];
+                }
         }
         __syncthreads();
-        const int r0 = m0 + ch * C::EPR;  // first output row of the chunk
+        auto grow = [&](int rr) { return m0 + (rr >> 5) * C::WM + ch * 32 + (rr & 31); };
         if (ep.kind == EP_GATED) {
-            constexpr int IT = C::EPR * (C::BN / 8);
-            for (int it = tid; it < IT; it += C::NT) {
-                const int rr = it / (C::BN / 8), c = (it % (C::BN / 8)) * 4;
-                const int row = r0 + rr;
-                if (row >= g.M) continue;
-                const f32x4 gv = *(const f32x4*)(st + rr * C::EPS + c);
-                const f32x4 uv = *(const f32x4*)(st + rr * C::EPS + C::BN / 2 + c);
-                float gg[4] = {gv[0], gv[1], gv[2], gv[3]}, uu[4] = {uv[0], uv[1], uv[2], uv[3]};
-                e.gated(row, tn * (C::BN / 2) + c, gg, uu);
+            const f32x4 bg = ld4(sbias + cg), bu = ld4(sbias + C::BN / 2 + cg);
+            with_act(ep.act, [&](auto actc) {
+                constexpr int ACT = decltype(actc)::value;
+#pragma unroll 2
+                for (int u = 0; u < PERG; ++u) {
+                    const int rr = rrg0 + u * RPTG, row = grow(rr);
+                    const f32x4 gv = ld4(st + rr * C::EPS + cg), uv = ld4(st + rr * C::EPS + C::BN / 2 + cg);
+                    if (row >= g.M) continue;
+                    float o[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) o[q] = act_fn<ACT>(gv[q] + bg[q]) * (uv[q] + bu[q]);
+                    store_bf16x4((bf16*)ep.out + (long)row * ep.ldo + tn * (C::BN / 2) + cg, o);
+                }
+            });
+        } else if (ep.kind == EP_ACT) {
+            const f32x4 bb = ld4(sbias + c);
+            with_act(ep.act, [&](auto actc) {
+                constexpr int ACT = decltype(actc)::value;
+#pragma unroll 2
+                for (int u = 0; u < PER; ++u) {
+                    const int rr = rr0 + u * RPT, row = grow(rr);
+                    const f32x4 v = ld4(st + rr * C::EPS + c);
+                    if (row >= g.M || n >= g.N) continue;
+                    float o[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) o[q] = act_fn<ACT>(v[q] + bb[q]);
+                    store_bf16x4((bf16*)ep.out + (long)row * ep.ldo + n, o);
+                }
+            });
+        } else if (ep.kind == EP_RESID || ep.kind == EP_SKIP) {
+            // EP_RESID: v = (acc + bias) [* gate]; h += v; delta = v | delta += v; hcopy = bf16(h)
+            // EP_SKIP:  h = acc + bias [+ cached delta]; hcopy = bf16(h)
+            // The global operands of a group of EB items are loaded before any of its stores.
+            const bool resid = ep.kind == EP_RESID;
+            const bool rd_delta = resid ? ep.delta_mode == 2 : ep.delta_mode == 1;
+            const f32x4 bb = ld4(sbias + c);
+            const int nl = min(n, g.N - 4);  // load column (N % 4 == 0)
+#pragma unroll 1
+            for (int u0 = 0; u0 < PER; u0 += EB) {
+                f32x4 hv[EB], dv[EB], gt[EB];
+#pragma unroll
+                for (int w = 0; w < EB; ++w) {
+                    // clamped row and column: every load stays inside the operands
+                    const int row = min(grow(rr0 + (u0 + w) * RPT), g.M - 1);
+                    const long idx = (long)row * ep.d + nl;
+                    hv[w] = resid ? ld4(ep.h + idx) : f32x4{0.f, 0.f, 0.f, 0.f};
+                    dv[w] = rd_delta ? ld4(ep.delta + idx) : f32x4{0.f, 0.f, 0.f, 0.f};
+                    gt[w] = ep.gate ? ld4(ep.gate + (long)sample_of(row) * ep.gate_ld + nl) : f32x4{1.f, 1.f, 1.f, 1.f};
+                }
+#pragma unroll
+                for (int w = 0; w < EB; ++w) {
+                    const int rr = rr0 + (u0 + w) * RPT, row = grow(rr);
+                    const f32x4 v = ld4(st + rr * C::EPS + c);
+                    if (row >= g.M || n >= g.N) continue;
+                    const long idx = (long)row * ep.d + n;
+                    float x[4], hn[4];
+                    if (resid) {
+                        float dn[4];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            x[q] = v[q] + bb[q];
+                            if (ep.gate) x[q] *= gt[w][q];
+                            hn[q] = hv[w][q] + x[q];
+                            dn[q] = dv[w][q] + x[q];
+                        }
+                        *(f32x4*)(ep.h + idx) = f32x4{hn[0], hn[1], hn[2], hn[3]};
+                        if (ep.delta_mode == 1) *(f32x4*)(ep.delta + idx) = f32x4{x[0], x[1], x[2], x[3]};
+                        else if (ep.delta_mode == 2) *(f32x4*)(ep.delta + idx) = f32x4{dn[0], dn[1], dn[2], dn[3]};
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            hn[q] = v[q] + bb[q];
+                            if (ep.delta_mode == 1) hn[q] = hn[q] + dv[w][q];
+                        }
+                        *(f32x4*)(ep.h + idx) = f32x4{hn[0], hn[1], hn[2], hn[3]};
+                    }
+                    if (ep.hcopy) store_bf16x4((bf16*)ep.hcopy + idx, hn);
+                }
             }
         } else if (ep.kind == EP_HEADS) {
             // q/k columns row-major (a thread stores four dims of one token), with the rotary
-            // pair read from LDS; V^T columns column-major (four tokens of one dim)
-            const int vstart = (2 - ep.which0) * ep.d;  // first product column of V
+            // pair read from LDS
             const int hd = ep.dh / 2;
-            constexpr int IT = C::EPR * (C::BN / 4);
-            for (int it = tid; it < IT; it += C::NT) {
-                const int rr = it / (C::BN / 4), c = (it % (C::BN / 4)) * 4;
-                const int row = r0 + rr, n = n0 + c;
-                if (row >= g.M || n >= g.N || n >= vstart) continue;
-                const int proj = ep.which0 + n / ep.d;
-                const int nn = n - (proj - ep.which0) * ep.d;
-                const int hh = nn / ep.dh, j = nn - hh * ep.dh;
-                const int b = row / ep.ntok, tok = row - b * ep.ntok;
-                const f32x4 x = *(const f32x4*)(st + rr * C::EPS + c);
-                float v[4] = {x[0], x[1], x[2], x[3]};
-                e.add_bias(n, v);
-                if (ep.rope) {
-                    const bool lo = j < hd;
-                    const int pc = lo ? c + hd : c - hd;  // partner columns in this tile
-                    const f32x4 y = *(const f32x4*)(st + rr * C::EPS + pc);
-                    float pv[4] = {y[0], y[1], y[2], y[3]};
-                    e.add_bias(lo ? n + hd : n - hd, pv);
-                    const int jb = lo ? j : j - hd;
+            if (n < g.N && n < vstart) {
+                const bool lo = j < hd;
+                const int pc = lo ? c + hd : c - hd;  // partner columns, same tile
+                const f32x4 bb = ld4(sbias + c);
+                const f32x4 pb = ep.rope ? ld4(sbias + pc) : f32x4{0.f, 0.f, 0.f, 0.f};
+                bf16* const base = proj == 0 ? qptr : kptr;
+#pragma unroll 2
+                for (int u = 0; u < PER; ++u) {
+                    const int rr = rr0 + u * RPT, row = grow(rr);
+                    const f32x4 v = ld4(st + rr * C::EPS + c);
+                    const f32x4 pv = ep.rope ? ld4(st + rr * C::EPS + pc) : f32x4{0.f, 0.f, 0.f, 0.f};
+                    if (row >= g.M) continue;
+                    const int bs = sample_of(row), tok = row - bs * ep.ntok;
+                    float o[4];
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        const float inv = exp2f(-(2.0f * (float)(jb + u) / (float)ep.dh) * ep.rope_log2_theta);
-                        float s, co;
-                        sincosf((float)tok * inv, &s, &co);
-                        v[u] = lo ? v[u] * co - pv[u] * s : v[u] * co + pv[u] * s;
-                    }
-                }
-                bf16* base = (bf16*)(proj == 0 ? ep.q : ep.k);
-                Epi4::store4(base + (((long)b * ep.H + hh) * ep.np + tok) * ep.dh + j, v);
-            }
-            const int vc0 = vstart > n0 ? vstart - n0 : 0;  // first V column of the tile
-            const int vcols = min(C::BN, g.N - n0) - vc0;
-            if (vcols > 0) {
-                const int ITV = vcols * (C::EPR / 4);
-                for (int it = tid; it < ITV; it += C::NT) {
-                    const int c = vc0 + it / (C::EPR / 4), rg = (it % (C::EPR / 4)) * 4;
-                    const int n = n0 + c;
-                    const int nn = n - vstart;
-                    const int hh = nn / ep.dh, j = nn - hh * ep.dh;
-                    const float bv = ep.bias ? ep.bias[n] : 0.f;
+                    for (int q = 0; q < 4; ++q) o[q] = v[q] + bb[q];
+                    if (ep.rope) {
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        const int row = r0 + rg + u;
-                        if (row >= g.M) break;
-                        const int b = row / ep.ntok, tok = row - b * ep.ntok;
-                        ((bf16*)ep.vt)[(((long)b * ep.H + hh) * ep.dh + j) * ep.np + tok] =
-                            f2bf(st[(rg + u) * C::EPS + c] + bv);
+                        for (int q = 0; q < 4; ++q) {
+                            // hardware sine/cosine (v_sin_f32 / v_cos_f32) of the angle reduced
+                            // to its fractional turn: ~1e-4 rad of fp32 rounding at 1024 tokens,
+                            // far below the bf16 resolution of the output
+                            const float turns = (float)tok * inv[q] * 0.159154943091895336f;
+                            const float ang = (turns - rintf(turns)) * 6.28318530717958648f;
+                            const float sn = __sinf(ang), cs = __cosf(ang);
+                            const float pq = pv[q] + pb[q];
+                            o[q] = lo ? o[q] * cs - pq * sn : o[q] * cs + pq * sn;
+                        }
                     }
+                    store_bf16x4(base + (((long)bs * ep.H + hh) * ep.np + tok) * ep.dh + j, o);
                 }
-            }
-        } else {
-            constexpr int IT = C::EPR * (C::BN / 4);
-            for (int it = tid; it < IT; it += C::NT) {
-                const int rr = it / (C::BN / 4), c = (it % (C::BN / 4)) * 4;
-                const int row = r0 + rr, n = n0 + c;
-                if (row >= g.M || n >= g.N) continue;
-                const f32x4 x = *(const f32x4*)(st + rr * C::EPS + c);
-                float v[4] = {x[0], x[1], x[2], x[3]};
-                if (ep.kind == EP_ACT) e.act(row, n, v);
-                else if (ep.kind == EP_RESID) e.resid(row, n, v);
-                else e.skip(row, n, v);
             }
         }
         __syncthreads();
@@ -247,7 +327,7 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
 // texture unit nor the LDS sees a burst and both SIMD waves keep issuing MFMAs.
 
 template <class C>
-__global__ __launch_bounds__(C::NT, 2) void gemm_bf16_kernel(GemmArgs g, EpiParams ep) {
+__global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, EpiParams ep) {
     static_assert(C::STAGES == 2, "two LDS stages plus the register stage");
     __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
 
@@ -409,7 +489,8 @@ __global__ __launch_bounds__(C::NT, 2) void gemm_bf16_kernel(GemmArgs g, EpiPara
 // --------------------------------------------------------------------------- dispatch
 
 namespace {
-// block tiles (BM, BN); eight waves, 64-deep k tiles, two LDS stages plus the register stage
+// block tiles (BM, BN); eight waves, 64-deep k tiles, two LDS stages plus the register stage.
+// (Four waves of 128 x 128, one per SIMD, measured 10-20 % slower on every branch shape.)
 using T256x256 = TileCfg<256, 256, 4, 2, 64, 2>;  // 64 x 128 wave tiles
 using T256x128 = TileCfg<256, 128, 4, 2, 64, 2>;  // 64 x 64
 using T128x256 = TileCfg<128, 256, 2, 4, 64, 2>;  // 64 x 64
@@ -458,13 +539,14 @@ bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
         return false;
     const Shape s = tile_shape(tile);
     if (!s.bm) return false;
+    if (g.M >= (1 << 21)) return false;  // the epilogue's fp32 row -> sample split is exact below
     if (g.K % 64 || (g.A1 && g.K0 % 64)) return false;
     if (g.N % 4 || g.lda0 % 8 || (g.A1 && g.lda1 % 8) || g.ldb % 8) return false;  // 16-byte rows
     if (e.kind == EP_GATED && (g.N % s.bn || e.ldo % 4)) return false;
     if (e.kind == EP_ACT && e.ldo % 4) return false;
     if ((e.kind == EP_RESID || e.kind == EP_SKIP) && (g.N != e.d)) return false;
     if (e.kind == EP_HEADS) {
-        if (e.d % 4 || e.dh % 4) return false;
+        if (e.d % 32 || e.dh % 4) return false;  // V^T from whole 32-column MFMA blocks
         if (e.rope && (e.dh % 8 || s.bn % e.dh || e.d % s.bn)) return false;  // whole heads per tile
     }
     if ((long)g.M * g.lda0 * 2 >= (1L << 32) || (g.A1 && (long)g.M * g.lda1 * 2 >= (1L << 32)) ||
