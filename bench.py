@@ -28,6 +28,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16 = 2.5e15      # dense MFMA bf16, FLOP/s
 PEAK_F32 = 157.3e12     # fp32 vector
 PEAK_HBM = 8.0e12       # bytes/s
+MAX_RUN = 32            # frozen units fused into one launch at most (kMaxRun of the launcher)
 
 
 def log(msg: str) -> None:
@@ -50,6 +51,30 @@ def unit_flops(cfg) -> dict:
     return f
 
 
+def frozen_launch_bytes(cfg, active_row) -> list:
+    """Algorithmic HBM bytes of every frozen-run launch of one step (Sec. 3.1 frozen rule).
+
+    The launcher fuses a maximal run of consecutive frozen units (at most MAX_RUN; U-ViT
+    out-blocks, whose skip linear always runs, end a run) into one pass that reads h and the
+    r cached updates and writes h: (2 + r) M d fp32 values, plus, for U-ViT in-blocks, a
+    bf16 copy of h after every unit of the run (the long-skip inputs)."""
+    L = cfg.L
+    es = 2 if cfg.dtype == "bf16" else 4
+    half = L // 2
+    out, l = [], 0
+    while l < L:
+        if active_row[l] or (cfg.arch == "uvit" and l > half):
+            l += 1
+            continue
+        r = 0
+        while l < L and not active_row[l] and not (cfg.arch == "uvit" and l > half) and r < MAX_RUN:
+            r += 1
+            l += 1
+        snaps = r if cfg.arch == "uvit" else 0
+        out.append((2 + r) * cfg.M * cfg.d * 4 + snaps * cfg.M * cfg.d * es)
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -58,7 +83,8 @@ def main() -> int:
     ap.add_argument("--config", default="llada")
     ap.add_argument("--budget", type=int, default=0, help="headline budget in percent (default: smallest)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-units", type=int, default=2, help="oracle sample: units of one all-active step")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="oracle sample: units of one all-active step, run until this much CPU time")
     ap.add_argument("--profile-kernel", default="gemm_w1")
     ap.add_argument("--save-lifetimes", default="", help="write the built lifetimes (JSON) here")
     ap.add_argument("--lifetimes", default="", help="reuse lifetimes saved by --save-lifetimes "
@@ -153,7 +179,8 @@ def main() -> int:
 
     results = {}
     for pct in budgets:
-        ms, prof = timed(scheds[pct], args.profile_kernel if pct == head else None)
+        # the headline run times the frozen-run kernel (the all-active run has none)
+        ms, prof = timed(scheds[pct], "frozen" if pct == head else None)
         results[pct] = (ms, prof)
         log(f"budget {pct}%: {K} steps in {ms:.2f} ms -> {K * 1000.0 / ms:.2f} steps/s")
     ms_all, prof_all = timed(all_active, args.profile_kernel)
@@ -175,9 +202,23 @@ def main() -> int:
                 "avg_launch_us": kavg * 1e6, "launches": kn,
                 "flop_per_launch": fl.get(kern, 0.0)}
 
+    # frozen path: algorithmic bytes of every frozen-run launch of the timed steps / their time
+    act = np.asarray(scheds[head].active, bool)
+    fbytes = sum(sum(frozen_launch_bytes(cfg, act[(i % T)])) for i in range(K))
+    fms, fn = prof_head if prof_head else (0.0, 0)
+    frozen = None
+    if fn:
+        frozen = {"bound": "hbm", "kernel": "frozen_run", "achieved": fbytes / (fms / 1000.0) / 1e9,
+                  "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": fbytes / (fms / 1000.0) / PEAK_HBM,
+                  "launches": fn, "avg_launch_us": fms * 1000.0 / fn, "bytes": fbytes,
+                  "note": "h and the cached updates; h may be served from the 256 MB Infinity Cache"}
+    tr = committed_traffic(kern, cfg)
+    roofline["traffic"] = tr["total_bytes"] if tr else None
+    roofline["traffic_detail"] = tr
+
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, weights, inputs, scheds[head], args.cpu_units)
+        cpu = cpu_baseline(cfg, weights, inputs, scheds[head], args.cpu_seconds)
 
     lay = {pct: scheds[pct].layer_steps for pct in budgets}
     line = {
@@ -202,6 +243,7 @@ def main() -> int:
         "budgets": {str(p): {"steps_per_s": round(K * 1000.0 / results[p][0], 3), "layer_steps": lay[p],
                              "speedup": round((K * 1000.0 / results[p][0]) / all_rate, 4)} for p in budgets},
         "roofline": roofline,
+        "frozen_path": frozen,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
@@ -209,34 +251,55 @@ def main() -> int:
     return 0
 
 
-def cpu_baseline(cfg, weights, inputs, sched, n_units):
-    """Oracle (numpy float64) on a bounded sample: n_units units of an all-active step.
+def cpu_baseline(cfg, weights, inputs, sched, seconds):
+    """Oracle (numpy float64) on a bounded sample: units of one all-active step, in stack order,
+    until `seconds` have passed (at least two units, at most the whole stack).
 
     Scaled to steps/s of the scheduled trajectory: the oracle's time per step is its time per
     active unit times the mean active units per step (frozen units cost an addition each).
     """
+    import dataclasses
+
     import numpy as np
     from oracle import model as om
 
     threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
-    sub = [weights[l] for l in range(n_units)]
-    import dataclasses
-    small = dataclasses.replace(cfg, L=n_units)
-    log(f"cpu baseline: oracle on {n_units} units of an all-active step ({threads} threads)")
-    m = om.Model(small, sub, inputs, lazy=True)
+    log(f"cpu baseline: oracle on units of an all-active step, about {seconds:.0f}s ({threads} threads)")
+    m = om.Model(dataclasses.replace(cfg), weights, inputs, lazy=True)
     h = om.initial_stream(m, inputs["z"], 1)
     t0 = time.time()
-    for l in range(n_units):
-        cross = m.cross_kv(m.units[l]) if cfg.arch == "sdxl" else None
-        h, _ = m.unit_active(l, h, om.timestep_value(1, cfg.T), cross)
+    n = 0
+    while n < cfg.L and (n < 2 or time.time() - t0 < seconds):
+        cross = m.cross_kv(m.units[n]) if cfg.arch == "sdxl" else None
+        if cfg.arch == "uvit" and n > cfg.L // 2:
+            break  # out-blocks need the skip inputs of the whole in-stack; in-blocks suffice
+        h, _ = m.unit_active(n, h, om.timestep_value(1, cfg.T), cross)
+        n += 1
     dt = time.time() - t0
-    per_unit = dt / n_units
+    per_unit = dt / n
     mean_active = float(np.asarray(sched.active, np.float64).sum(axis=1).mean())
     per_step = per_unit * mean_active
-    log(f"cpu baseline: {per_unit:.2f}s per active unit -> {per_step:.1f}s per scheduled step")
+    log(f"cpu baseline: {n} units in {dt:.1f}s, {per_unit:.2f}s per active unit -> {per_step:.1f}s per scheduled step")
     return {"value": round(1.0 / per_step, 6), "unit": "steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n_units} of {cfg.L} units of one all-active step at full size ({dt:.1f}s), "
+            "sample": f"{n} of {cfg.L} units of one all-active step at full size ({dt:.1f}s), "
                       f"scaled by {mean_active:.2f} mean active units per scheduled step"}
+
+
+def committed_traffic(kern: str, cfg):
+    """HBM bytes per launch of the timed kernel from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE passes (profiles/<kernel>_<workload>_traffic.json), scaled by the copy-kernel
+    calibration recorded there; None unless the record was taken on this exact kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{kern}_{cfg.name}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = os.path.join(ROOT, rec.get("source", ""))
+    if not os.path.exists(src) or hashlib.sha256(open(src, "rb").read()).hexdigest() != rec.get("sha256"):
+        return None
+    return {"fetch_bytes": rec["fetch_bytes"], "write_bytes": rec["write_bytes"],
+            "total_bytes": rec["fetch_bytes"] + rec["write_bytes"],
+            "algorithmic_bytes": rec.get("algorithmic_bytes"), "profile": os.path.relpath(path, ROOT)}
 
 
 if __name__ == "__main__":

@@ -7,26 +7,45 @@ namespace sgd {
 
 // h <- (((h + D_1) + D_2) + ... + D_r), one coalesced float4 pass for a maximal run of
 // consecutive frozen units; optional bf16 snapshots of h after individual units (U-ViT
-// in-blocks feed their output to a long skip connection).
+// in-blocks feed their output to a long skip connection).  The cached updates are read four
+// at a time, so every wave keeps four loads in flight per element group instead of one; the
+// additions stay in stack order (bitwise the same result).
+__device__ __forceinline__ void frozen_snap(const FrozenRun& f, int u, long i, const float4& v) {
+    if (!f.snap[u]) return;
+    if (f.snap_bf16) {
+        bf16x4 s;
+        s[0] = f2bf(v.x); s[1] = f2bf(v.y); s[2] = f2bf(v.z); s[3] = f2bf(v.w);
+        ((bf16x4*)f.snap[u])[i] = s;
+    } else {
+        ((float4*)f.snap[u])[i] = v;
+    }
+}
+
 __global__ __launch_bounds__(256) void frozen_run_kernel(FrozenRun f) {
     const long n4 = f.n / 4;
     for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n4; i += (long)gridDim.x * 256) {
         float4 v = ((const float4*)f.h)[i];
-        for (int u = 0; u < f.r; ++u) {
+        int u = 0;
+        for (; u + 4 <= f.r; u += 4) {
+            float4 d[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) d[k] = ((const float4*)f.delta[u + k])[i];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                v.x = v.x + d[k].x;
+                v.y = v.y + d[k].y;
+                v.z = v.z + d[k].z;
+                v.w = v.w + d[k].w;
+                frozen_snap(f, u + k, i, v);
+            }
+        }
+        for (; u < f.r; ++u) {
             const float4 d = ((const float4*)f.delta[u])[i];
             v.x = v.x + d.x;
             v.y = v.y + d.y;
             v.z = v.z + d.z;
             v.w = v.w + d.w;
-            if (f.snap[u]) {
-                if (f.snap_bf16) {
-                    bf16x4 s;
-                    s[0] = f2bf(v.x); s[1] = f2bf(v.y); s[2] = f2bf(v.z); s[3] = f2bf(v.w);
-                    ((bf16x4*)f.snap[u])[i] = s;
-                } else {
-                    ((float4*)f.snap[u])[i] = v;
-                }
-            }
+            frozen_snap(f, u, i, v);
         }
         ((float4*)f.h)[i] = v;
     }
