@@ -33,12 +33,27 @@ template <> struct ElemIO<bf16> {
     __device__ static __forceinline__ void store(bf16* p, float v) { *p = f2bf(v); }
 };
 
-__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
+// Activations of the MLP epilogues, built on the hardware exponential (v_exp_f32) and
+// reciprocal (v_rcp_f32); errors are a few 1e-7 absolute, far below the bf16 outputs'
+// resolution and the fp32 workload's tolerance.
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+// erf by Abramowitz & Stegun, Handbook of Mathematical Functions, 7.1.26 (|error| <= 1.5e-7):
+// erf(x) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-x^2), t = 1 / (1 + p x), x >= 0
+__device__ __forceinline__ float erf_as(float x) {
+    const float ax = fabsf(x);
+    const float t = fast_rcp(1.0f + 0.3275911f * ax);
+    const float poly = t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+    const float y = 1.0f - poly * __expf(-ax * ax);
+    return copysignf(y, x);
+}
+// tanh(x) = 1 - 2 / (exp(2x) + 1): exact limits +-1 when exp overflows or underflows
+__device__ __forceinline__ float tanh_exp(float x) { return 1.0f - 2.0f * fast_rcp(__expf(2.0f * x) + 1.0f); }
+__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erf_as(x * 0.70710678118654752f)); }
 __device__ __forceinline__ float gelu_tanh(float x) {
     const float k0 = 0.79788456080286536f;  // sqrt(2/pi)
-    return 0.5f * x * (1.0f + tanhf(k0 * (x + 0.044715f * x * x * x)));
+    return 0.5f * x * (1.0f + tanh_exp(k0 * (x + 0.044715f * x * x * x)));
 }
-__device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
+__device__ __forceinline__ float silu(float x) { return x * fast_rcp(1.0f + __expf(-x)); }
 
 __device__ __forceinline__ float warp_sum(float v) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
