@@ -37,7 +37,8 @@ int sgd_op_attention(int32_t dtype, const void* q, const void* k, const void* vt
 
 /* Pre-norm of M rows of width d from fp32 x into y (dtype).  kind 0: RMSNorm with gain w;
  * 1: LayerNorm with gain w and shift b; 2: LayerNorm without affine parameters followed by
- * y * (1 + scale[r / ntok]) + shift[r / ntok] (rows of scale/shift mod_ld apart). */
+ * y * (1 + scale[r / ntok]) + shift[r / ntok] (rows of scale/shift mod_ld apart).  x, w, b,
+ * shift, scale 16-byte aligned (mod_ld % 4 == 0), y 16-byte (fp32) or 8-byte (bf16) aligned. */
 int sgd_op_norm(int32_t dtype, int32_t kind, const float* x, void* y, int32_t M, int32_t d, float eps,
                 const float* w, const float* b, const float* shift, const float* scale, int64_t mod_ld,
                 int32_t ntok, void* hip_stream);

@@ -100,6 +100,12 @@ int check_unit(const sgd_model_desc& d, const sgd_unit_weights& w, int l) {
             (rc = need(w.w_xkv, "w_xkv")) || (rc = need(w.w_xo, "w_xo")))
             return rc;
     }
+    // the kernels read weights, biases, gains and shifts in 16-byte vectors
+    const void* ptrs[] = {w.norm1_w, w.norm1_b, w.w_qkv, w.b_qkv, w.w_o, w.b_o, w.norm2_w, w.norm2_b, w.w1, w.b1,
+                          w.w2, w.b2, w.normx_w, w.normx_b, w.w_xq, w.w_xkv, w.w_xo, w.b_xo, w.w_ada, w.b_ada,
+                          w.w_skip, w.b_skip};
+    for (const void* p : ptrs)
+        if ((uintptr_t)p % 16) return fail(SGD_E_ARG, "unit " + std::to_string(l) + ": weights must be 16-byte aligned");
     return SGD_OK;
 }
 
@@ -557,6 +563,9 @@ extern "C" int sgd_op_norm(int32_t dtype, int32_t kind, const float* x, void* y,
     if (kind < 0 || kind > 2 || M < 1 || d < 4 || d % 4 || d > 8192) return fail(SGD_E_SHAPE, "norm shape not supported");
     if ((kind == 0 && !w) || (kind == 1 && (!w || !b)) || (kind == 2 && (!shift || !scale || ntok < 1)))
         return fail(SGD_E_ARG, "missing norm parameters");
+    if ((uintptr_t)x % 16 || (uintptr_t)w % 16 || (uintptr_t)b % 16 || (uintptr_t)shift % 16 || (uintptr_t)scale % 16 ||
+        mod_ld % 4 || (uintptr_t)y % (dtype == SGD_BF16 ? 8 : 16))
+        return fail(SGD_E_ARG, "norm operands must be 16-byte aligned (bf16 output: 8)");
     NormArgs a{x, y, M, d, kind, eps, w, b, shift, scale, mod_ld, ntok};
     SGD_HIP_TRY(launch_norm(dtype == SGD_BF16 ? 1 : 0, a, (hipStream_t)hip_stream));
     return SGD_OK;

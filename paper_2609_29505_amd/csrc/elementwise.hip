@@ -145,53 +145,117 @@ hipError_t launch_cond_silu(const float* y, float* x, int B, int d, float t, hip
 // AdaLN modulation: mod[b, j] = sum_k x[b, k] W[j, k] + bias[j] for j < n_out.
 // A workgroup owns 64 output features for every sample; the weight rows stream through
 // LDS once in 64-wide k chunks.
+// mod[b, j] = sum_k x[b, k] W[j, k] + bias[j]: the DiT AdaLN modulation (6 d outputs per
+// sample) in fp32 from the fp32 SiLU(c) rows and the stored weights.  A workgroup computes a
+// 64-feature x 32-sample tile; thread (f, s) holds features 4f..4f+3 of samples s, s + 16, so
+// each 4-deep k step is six 16-byte LDS reads for 32 FMAs.  LDS rows are padded to 68 floats
+// (16-byte aligned, conflict-free 16-byte reads); the next k chunk is prefetched into
+// registers (weights 16 bytes per thread, activations two float4 per thread).
+template <typename WT> struct Wvec;
+template <> struct Wvec<bf16> {
+    typedef u32x4 raw;  // 8 weights
+    static constexpr int PER = 8;
+    __device__ static void expand(const raw& r, float* o) {
+        for (int e = 0; e < 4; ++e) {
+            o[2 * e] = __uint_as_float(r[e] << 16);
+            o[2 * e + 1] = __uint_as_float(r[e] & 0xffff0000u);
+        }
+    }
+};
+template <> struct Wvec<float> {
+    typedef f32x4 raw;  // 4 weights
+    static constexpr int PER = 4;
+    __device__ static void expand(const raw& r, float* o) {
+        for (int e = 0; e < 4; ++e) o[e] = r[e];
+    }
+};
+
 template <typename WT>
 __global__ __launch_bounds__(256) void adaln_mod_kernel(const float* x, const WT* W, const float* bias,
                                                         float* mod, int B, int d, int n_out) {
-    constexpr int FJ = 64, KC = 64, SB = 32;  // features, k chunk, samples per pass
-    __shared__ float sw[FJ][KC + 1];
-    __shared__ float sx[SB][KC + 1];
+    constexpr int FJ = 64, SB = 32, KC = 64, LD = KC + 4;
+    constexpr int WV = Wvec<WT>::PER;                     // weights per vector load
+    constexpr int WLOADS = FJ * KC / WV / 256;            // weight vectors per thread per chunk
+    __shared__ __attribute__((aligned(16))) float sw[FJ * LD];
+    __shared__ __attribute__((aligned(16))) float sx[SB * LD];
     const int tid = threadIdx.x;
-    const int j0 = blockIdx.x * FJ;
-    const int f = tid & 63, sg = tid >> 6;  // feature, sample group (4 groups)
-    for (int b0 = 0; b0 < B; b0 += SB) {
-        float acc[SB / 4];
+    const int j0 = blockIdx.x * FJ, b0 = blockIdx.y * SB;
+    const int f4 = (tid & 15) * 4, s0 = tid >> 4;  // features f4..f4+3, samples s0, s0 + 16
+
+    typename Wvec<WT>::raw rw[WLOADS];
+    f32x4 rx[2];
+    auto gload = [&](int k0) {
 #pragma unroll
-        for (int i = 0; i < SB / 4; ++i) acc[i] = 0.f;
-        for (int k0 = 0; k0 < d; k0 += KC) {
-            __syncthreads();
-            for (int i = tid; i < FJ * KC; i += 256) {
-                const int r = i / KC, c = i % KC;
-                const int jj = j0 + r, kk = k0 + c;
-                sw[r][c] = (jj < n_out && kk < d) ? ElemIO<WT>::load(W + (long)jj * d + kk) : 0.f;
-            }
-            for (int i = tid; i < SB * KC; i += 256) {
-                const int r = i / KC, c = i % KC;
-                const int bb = b0 + r, kk = k0 + c;
-                sx[r][c] = (bb < B && kk < d) ? x[(long)bb * d + kk] : 0.f;
-            }
-            __syncthreads();
-#pragma unroll 4
-            for (int c = 0; c < KC; ++c) {
-                const float w = sw[f][c];
-#pragma unroll
-                for (int i = 0; i < SB / 4; ++i) acc[i] = fmaf(sx[sg + 4 * i][c], w, acc[i]);
-            }
+        for (int t = 0; t < WLOADS; ++t) {
+            const int i = tid + t * 256;
+            const int r = i / (KC / WV), c = (i % (KC / WV)) * WV;
+            const int jj = min(j0 + r, n_out - 1);  // clamped rows are never stored
+            rw[t] = *(const typename Wvec<WT>::raw*)(W + (long)jj * d + k0 + c);
         }
-        const int j = j0 + f;
-        if (j < n_out) {
 #pragma unroll
-            for (int i = 0; i < SB / 4; ++i) {
-                const int bb = b0 + sg + 4 * i;
-                if (bb < B) mod[(long)bb * n_out + j] = acc[i] + (bias ? bias[j] : 0.f);
-            }
+        for (int t = 0; t < 2; ++t) {
+            const int i = tid + t * 256;
+            const int r = i / (KC / 4), c = (i % (KC / 4)) * 4;
+            const int bb = min(b0 + r, B - 1);
+            rx[t] = *(const f32x4*)(x + (long)bb * d + k0 + c);
+        }
+    };
+    auto lstore = [&]() {
+#pragma unroll
+        for (int t = 0; t < WLOADS; ++t) {
+            const int i = tid + t * 256;
+            const int r = i / (KC / WV), c = (i % (KC / WV)) * WV;
+            float w[WV];
+            Wvec<WT>::expand(rw[t], w);
+#pragma unroll
+            for (int e = 0; e < WV; e += 4) *(f32x4*)(sw + r * LD + c + e) = f32x4{w[e], w[e + 1], w[e + 2], w[e + 3]};
+        }
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const int i = tid + t * 256;
+            const int r = i / (KC / 4), c = (i % (KC / 4)) * 4;
+            *(f32x4*)(sx + r * LD + c) = rx[t];
+        }
+    };
+
+    float acc[4][2] = {};
+    gload(0);
+    for (int k0 = 0; k0 < d; k0 += KC) {
+        __syncthreads();  // the previous chunk has been consumed
+        lstore();
+        __syncthreads();
+        if (k0 + KC < d) gload(k0 + KC);
+#pragma unroll 4
+        for (int c = 0; c < KC; c += 4) {
+            f32x4 w[4], xv[2];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) w[q] = *(const f32x4*)(sw + (f4 + q) * LD + c);
+            xv[0] = *(const f32x4*)(sx + s0 * LD + c);
+            xv[1] = *(const f32x4*)(sx + (s0 + 16) * LD + c);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int s = 0; s < 2; ++s)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[q][s] = fmaf(xv[s][e], w[q][e], acc[q][s]);
+        }
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        const int bb = b0 + s0 + 16 * s;
+        if (bb >= B) continue;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int j = j0 + f4 + q;
+            if (j < n_out) mod[(long)bb * n_out + j] = acc[q][s] + (bias ? bias[j] : 0.f);
         }
     }
 }
 
 hipError_t launch_adaln_mod(int dtype, const float* x, const void* W, const float* bias, float* mod, int B,
                             int d, int n_out, hipStream_t st) {
-    dim3 grid((n_out + 63) / 64), block(256);
+    if (d % 64) return hipErrorInvalidValue;  // whole 64-deep k chunks (the model requires d % 128 == 0)
+    dim3 grid((n_out + 63) / 64, (B + 31) / 32), block(256);
     if (dtype == 1)
         hipLaunchKernelGGL(adaln_mod_kernel<bf16>, grid, block, 0, st, x, (const bf16*)W, bias, mod, B, d, n_out);
     else
