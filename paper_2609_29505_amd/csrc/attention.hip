@@ -1,8 +1,9 @@
 // Fused bidirectional / cross attention (flash-style, one pass over the keys).
 //
-// bf16 path (MFMA 32x32x16): a workgroup is 4 waves x 32 queries.  Each wave computes the
-// transposed score tile S^T = K Q^T so that one lane owns one query: the row maximum and
-// row sum of the online softmax are per-lane reductions plus one exchange with lane ^ 32.
+// bf16 path (MFMA 32x32x16): a wave owns 32 queries (of one key half in the split variant)
+// and computes the transposed score tile S^T = K Q^T, so that one lane owns one query: the
+// row maximum and row sum of the online softmax are per-lane reductions plus one exchange
+// with lane ^ 32.
 // The output is accumulated transposed as O^T += V^T P^T, where P^T is exactly the S^T
 // accumulator layout re-packed to bf16 (the MFMA k-slots are permuted consistently on
 // both operands), and V^T is read from the head-major transposed value layout written by
@@ -234,6 +235,247 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
     }
 }
 
+// The workgroup's waves form two halves of NQG waves; wave w serves query group w % NQG and
+// key half w / NQG: half h takes the key blocks 2 i + h, each half with one LDS buffer (K
+// block and V^T block) refilled from a register prefetch.  Splitting the keys doubles the
+// waves per query range (a 1024-query, 32-head problem has only 1024 query groups of 32),
+// so two waves share each SIMD and one half's softmax overlaps the other's MFMAs.  At the
+// end half 1 leaves (m, partial sums, O^T) in LDS and half 0 merges them:
+// O = O_0 2^(m_0 - m) + O_1 2^(m_1 - m) with m = max(m_0, m_1).
+template <int DHP, int NQG>
+__global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnArgs a, float scale_log2) {
+    constexpr int BQ = 32 * NQG, BKV = 64, HT = NQG * 64, NT = 2 * HT;
+    constexpr int KS = DHP / 16, DT = DHP / 32;
+    constexpr int KLDS = DHP + 8, VLDS = BKV + 8;        // padded rows: conflict-free fragment reads
+    constexpr int K_CH = BKV * (DHP / 8) / HT;            // 16-byte chunks per thread per block (upper bound)
+    constexpr int V_CH = DHP * (BKV / 8) / HT;
+    constexpr int HALF_BYTES = (BKV * KLDS + DHP * VLDS) * 2;
+    constexpr int MERGE_BYTES = NQG * (DT * 16 + 2) * 64 * 4;  // half 1's state, lane-major
+    static_assert(MERGE_BYTES <= 2 * HALF_BYTES, "merge area");
+    __shared__ __attribute__((aligned(16))) char smem[2 * HALF_BYTES];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int kh = wave / NQG, qg = wave % NQG, htid = tid - kh * HT;
+    bf16* sk = (bf16*)(smem + kh * HALF_BYTES);
+    bf16* sv = sk + BKV * KLDS;
+    const int bh = blockIdx.y;
+    const int b = bh / a.H, hh = bh - b * a.H;
+    const int dh = a.dh;
+    const int q = blockIdx.x * BQ + qg * 32 + (lane & 31);
+    const int half = lane >> 5;
+
+    const bf16* Q = (const bf16*)a.q + (long)bh * a.npq * dh;
+    const bf16* K = (const bf16*)a.k + (long)bh * a.npk * dh;
+    const bf16* VT = (const bf16*)a.vt + (long)bh * dh * a.npk;
+
+    // zero the padded head dims of this half's buffers once (the loads never write them)
+    for (int i = htid; i < BKV * (DHP - dh); i += HT) sk[(i / (DHP - dh)) * KLDS + dh + i % (DHP - dh)] = f2bf(0.f);
+    for (int i = htid; i < (DHP - dh) * BKV; i += HT) sv[(dh + i / BKV) * VLDS + i % BKV] = f2bf(0.f);
+
+    // this lane's query fragments (B operand of S^T = K Q^T)
+    bf16x8 qf[KS];
+    const int qrow = min(q, a.npq - 1);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+        const int c = ks * 16 + half * 8;
+        if (c < dh) qf[ks] = *(const bf16x8*)(Q + (long)qrow * dh + c);
+        else
+            for (int e = 0; e < 8; ++e) qf[ks][e] = f2bf(0.f);
+    }
+
+    // register prefetch of one key/value block of this half
+    const int kchunks = dh / 8;  // 16-byte chunks per key row
+    u32x4 rk[K_CH], rv[V_CH];
+    auto gload = [&](int k0) {
+#pragma unroll
+        for (int t = 0; t < K_CH; ++t) {
+            const int i = htid + t * HT;
+            if (i < BKV * kchunks) {
+                const int r = i / kchunks, c = (i - r * kchunks) * 8;
+                rk[t] = *(const u32x4*)(K + (long)(k0 + r) * dh + c);
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < V_CH; ++t) {
+            const int i = htid + t * HT;
+            if (i < dh * (BKV / 8)) {
+                const int r = i >> 3, c = (i & 7) * 8;
+                rv[t] = *(const u32x4*)(VT + (long)r * a.npk + k0 + c);
+            }
+        }
+    };
+    auto lstore = [&](int k0) {
+#pragma unroll
+        for (int t = 0; t < K_CH; ++t) {
+            const int i = htid + t * HT;
+            if (i < BKV * kchunks) {
+                const int r = i / kchunks, c = (i - r * kchunks) * 8;
+                *(u32x4*)(&sk[r * KLDS + c]) = rk[t];
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < V_CH; ++t) {
+            const int i = htid + t * HT;
+            if (i < dh * (BKV / 8)) {
+                const int r = i >> 3, c = (i & 7) * 8;
+                bf16x8 v = __builtin_bit_cast(bf16x8, rv[t]);
+                if (k0 + c + 8 > a.nk) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (k0 + c + e >= a.nk) v[e] = f2bf(0.f);
+                }
+                // key order inside a 16-key group: 0-3, 8-11, 4-7, 12-15, so the keys
+                // {0-3, 8-11} (lanes 0-31) and {4-7, 12-15} (lanes 32-63) are contiguous
+                const int g16 = c & ~15, hi8 = (c & 8) ? 4 : 0;
+                bf16x4 v0, v1;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) { v0[e] = v[e]; v1[e] = v[4 + e]; }
+                *(bf16x4*)(&sv[r * VLDS + g16 + hi8]) = v0;
+                *(bf16x4*)(&sv[r * VLDS + g16 + 8 + hi8]) = v1;
+            }
+        }
+    };
+
+    f32x16 o[DT];
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[t][r] = 0.f;
+    float m = -INFINITY, lsum = 0.f;
+
+    const int nkb = (a.nk + BKV - 1) / BKV;
+    const int nit = (nkb + 1) / 2;  // block pairs: half h takes block 2 it + h
+    if (kh < nkb) gload(kh * BKV);
+    __syncthreads();  // padding zeroed
+    if (kh < nkb) lstore(kh * BKV);
+    __syncthreads();
+    for (int it = 0; it < nit; ++it) {
+        const int kb = 2 * it + kh;
+        const int k0 = kb * BKV;
+        const bool mine = kb < nkb;
+        if (kb + 2 < nkb) gload(k0 + 2 * BKV);  // in flight while this block computes
+        if (mine) {
+            f32x16 s[2];
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) s[t][r] = 0.f;
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    bf16x8 kf = *(const bf16x8*)(&sk[(t * 32 + (lane & 31)) * KLDS + ks * 16 + half * 8]);
+                    s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[t], 0, 0, 0);
+                }
+            }
+            // scale into the log2 domain (masking keys beyond nk in the tail block only), block max
+            float bm = -INFINITY;
+            if (k0 + BKV <= a.nk) {
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        s[t][r] *= scale_log2;
+                        bm = fmaxf(bm, s[t][r]);
+                    }
+            } else {
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int key = k0 + t * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+                        const float v = key < a.nk ? s[t][r] * scale_log2 : -INFINITY;
+                        s[t][r] = v;
+                        bm = fmaxf(bm, v);
+                    }
+            }
+            bm = pair_max(bm);
+            if (__builtin_amdgcn_ballot_w64(bm > m + kRescaleSlack)) {
+                const float mn = fmaxf(m, bm);
+                const float alpha = __builtin_amdgcn_exp2f(m - mn);
+                m = mn;
+                lsum *= alpha;
+#pragma unroll
+                for (int t = 0; t < DT; ++t)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+            }
+            float ps = 0.f;
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const float p = __builtin_amdgcn_exp2f(s[t][r] - m);
+                    s[t][r] = p;
+                    ps += p;
+                }
+            lsum += ps;
+
+            // O^T += V^T P^T over the block's 64 keys, 16 at a time
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+#pragma unroll
+                for (int k2 = 0; k2 < 2; ++k2) {
+                    bf16x8 pf;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) pf[e] = f2bf(s[t][8 * k2 + e]);
+                    const int kc = t * 32 + 16 * k2 + half * 8;  // permuted key order (see lstore)
+#pragma unroll
+                    for (int dt = 0; dt < DT; ++dt) {
+                        const bf16x8 vf = *(const bf16x8*)(&sv[(dt * 32 + (lane & 31)) * VLDS + kc]);
+                        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[dt], 0, 0, 0);
+                    }
+                }
+            }
+        }
+        if (it + 1 < nit) {
+            __syncthreads();  // both halves are done with their buffers
+            if (kb + 2 < nkb) lstore(k0 + 2 * BKV);
+            __syncthreads();
+        }
+    }
+
+    // merge the two key halves through LDS (lane-major: conflict-free)
+    __syncthreads();
+    float* mg = (float*)smem + qg * (DT * 16 + 2) * 64;
+    if (kh == 1) {
+#pragma unroll
+        for (int t = 0; t < DT; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mg[(t * 16 + r) * 64 + lane] = o[t][r];
+        mg[DT * 16 * 64 + lane] = m;
+        mg[(DT * 16 + 1) * 64 + lane] = lsum;
+    }
+    __syncthreads();
+    if (kh == 1) return;
+    {
+        const float m1 = mg[DT * 16 * 64 + lane], l1 = mg[(DT * 16 + 1) * 64 + lane];
+        const float mn = fmaxf(m, m1);  // half 0 always holds block 0, so mn is finite
+        const float a0 = __builtin_amdgcn_exp2f(m - mn), a1 = __builtin_amdgcn_exp2f(m1 - mn);
+        lsum = lsum * a0 + l1 * a1;
+#pragma unroll
+        for (int t = 0; t < DT; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) o[t][r] = o[t][r] * a0 + mg[(t * 16 + r) * 64 + lane] * a1;
+    }
+
+    const float l = pair_sum(lsum);
+    const float inv = 1.0f / l;
+    if (q < a.nq) {
+        bf16* O = (bf16*)a.o + ((long)b * a.nq + q) * ((long)a.H * dh) + (long)hh * dh;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+                const int d0 = dt * 32 + g4 * 8 + half * 4;
+                if (d0 < dh) {
+                    bf16x4 v;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = f2bf(o[dt][g4 * 4 + e] * inv);
+                    *(bf16x4*)(O + d0) = v;
+                }
+            }
+    }
+}
+
 template <int DHP>
 __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, float scale) {
     constexpr int BKV = 64;
@@ -302,9 +544,23 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st) {
     const int BH = a.B * a.H;
     if (dtype == 1) {
         const float sl2 = (float)(1.4426950408889634 / sqrt((double)a.dh));
-        // two-wave workgroups when four-wave ones would leave CUs without a second workgroup
-        const bool small = (long)((a.nq + 127) / 128) * BH < 1024;
-        if (small) {
+        const long qg128 = (long)((a.nq + 127) / 128) * BH;  // 128-query workgroups
+        const int nkb = (a.nk + 63) / 64;
+        if (nkb >= 8 && qg128 < 1024) {
+            // long key range, few query groups: split the keys between two wave halves
+            if (qg128 >= 256) {
+                dim3 grid((a.nq + 127) / 128, BH), block(512);
+                if (a.dh <= 64) hipLaunchKernelGGL((attn_split_bf16_kernel<64, 4>), grid, block, 0, st, a, sl2);
+                else if (a.dh <= 96) hipLaunchKernelGGL((attn_split_bf16_kernel<96, 4>), grid, block, 0, st, a, sl2);
+                else hipLaunchKernelGGL((attn_split_bf16_kernel<128, 4>), grid, block, 0, st, a, sl2);
+            } else {
+                dim3 grid((a.nq + 63) / 64, BH), block(256);
+                if (a.dh <= 64) hipLaunchKernelGGL((attn_split_bf16_kernel<64, 2>), grid, block, 0, st, a, sl2);
+                else if (a.dh <= 96) hipLaunchKernelGGL((attn_split_bf16_kernel<96, 2>), grid, block, 0, st, a, sl2);
+                else hipLaunchKernelGGL((attn_split_bf16_kernel<128, 2>), grid, block, 0, st, a, sl2);
+            }
+        } else if ((long)((a.nq + 127) / 128) * BH < 1024) {
+            // two-wave workgroups when four-wave ones would leave CUs without a second workgroup
             dim3 grid((a.nq + 63) / 64, BH), block(128);
             if (a.dh <= 64) hipLaunchKernelGGL((attn_bf16_kernel<64, 2>), grid, block, 0, st, a, sl2);
             else if (a.dh <= 96) hipLaunchKernelGGL((attn_bf16_kernel<96, 2>), grid, block, 0, st, a, sl2);

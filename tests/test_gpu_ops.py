@@ -112,7 +112,11 @@ def _heads_inputs(rng, B, H, nq, nk, dh, dtype, npq, npk):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("B,H,nq,nk,dh", [(1, 2, 200, 200, 128), (2, 3, 80, 80, 72), (2, 2, 66, 66, 64),
-                                          (2, 2, 96, 77, 64), (1, 1, 256, 256, 64), (1, 2, 130, 1, 64)])
+                                          (2, 2, 96, 77, 64), (1, 1, 256, 256, 64), (1, 2, 130, 1, 64),
+                                          # >= 8 key blocks: keys split between two wave halves
+                                          # (odd block count, ragged tail, padded head dim)
+                                          (1, 2, 300, 600, 128), (1, 3, 150, 1000, 64), (2, 2, 130, 700, 72),
+                                          (1, 2, 64, 513, 128)])
 def test_attention(P, dtype, B, H, nq, nk, dh):
     rng = np.random.default_rng(nq * 7 + nk + dh)
     npq, npk = -(-nq // 64) * 64, -(-nk // 64) * 64
