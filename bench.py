@@ -89,6 +89,8 @@ def main() -> int:
     ap.add_argument("--save-lifetimes", default="", help="write the built lifetimes (JSON) here")
     ap.add_argument("--lifetimes", default="", help="reuse lifetimes saved by --save-lifetimes "
                     "instead of rebuilding the spectra (e.g. under a kernel tracer)")
+    ap.add_argument("--taus", default="0.5,1,2",
+                    help="tau-mode schedules (Eq. schedule at a fixed tau) timed beside the budgets; '' for none")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md, 'Sharding').",
@@ -130,8 +132,10 @@ def main() -> int:
         saved = json.load(open(args.lifetimes))
         for pct in budgets:
             scheds[pct] = P.schedule_from_lifetimes(saved[str(pct)], T)
+        scores = saved.get("scores")
     else:
         scheds[head] = P.schedule_build(dm.scored_units(), [cfg.dh] * L, T, budget=n_head)
+        scores = scheds[head].unit_score.tolist()
     t_build = time.time() - t0
     for pct in budgets:
         if args.lifetimes:
@@ -143,7 +147,11 @@ def main() -> int:
     log(f"schedule ready in {t_build:.1f}s (spectra of {sum(len(u) for u in dm.scored_units())} matrices; "
         f"offline, not timed)")
     if args.save_lifetimes:
-        json.dump({str(p): scheds[p].lifetimes.tolist() for p in budgets}, open(args.save_lifetimes, "w"))
+        rec = {str(p): scheds[p].lifetimes.tolist() for p in budgets}
+        rec["scores"] = scores
+        json.dump(rec, open(args.save_lifetimes, "w"))
+    taus = [float(t) for t in args.taus.split(",") if t] if scores is not None else []
+    tau_scheds = {t: P.schedule_from_scores(scores, T, tau=t) for t in taus}
     all_active = P.schedule_from_lifetimes([T] * L, T)
 
     z0 = torch.from_numpy(inputs["z"]).cuda()
@@ -185,6 +193,11 @@ def main() -> int:
         log(f"budget {pct}%: {K} steps in {ms:.2f} ms -> {K * 1000.0 / ms:.2f} steps/s")
     ms_all, prof_all = timed(all_active, args.profile_kernel)
     log(f"all-active: {K} steps in {ms_all:.2f} ms -> {K * 1000.0 / ms_all:.2f} steps/s")
+    tau_res = {}
+    for t, sch in tau_scheds.items():
+        ms, _ = timed(sch)
+        tau_res[t] = ms
+        log(f"tau {t:g}: {sch.layer_steps} layer-steps, {K} steps in {ms:.2f} ms -> {K * 1000.0 / ms:.2f} steps/s")
 
     ms_head, prof_head = results[head]
     value = K * 1000.0 / ms_head
@@ -242,6 +255,9 @@ def main() -> int:
         "skipped_layer_step_fraction": round(1 - lay[head] / (L * T), 4),
         "budgets": {str(p): {"steps_per_s": round(K * 1000.0 / results[p][0], 3), "layer_steps": lay[p],
                              "speedup": round((K * 1000.0 / results[p][0]) / all_rate, 4)} for p in budgets},
+        "tau": {f"{t:g}": {"steps_per_s": round(K * 1000.0 / ms, 3), "layer_steps": tau_scheds[t].layer_steps,
+                           "frac_layer_steps": round(tau_scheds[t].layer_steps / (L * T), 4),
+                           "speedup": round((K * 1000.0 / ms) / all_rate, 4)} for t, ms in tau_res.items()},
         "roofline": roofline,
         "frozen_path": frozen,
         "cpu_baseline": cpu,
