@@ -86,6 +86,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="oracle sample: units of one all-active step, run until this much CPU time")
     ap.add_argument("--profile-kernel", default="gemm_w1")
+    ap.add_argument("--no-kernel-table", action="store_true",
+                    help="skip the per-kernel-class timing passes of the all-active schedule")
     ap.add_argument("--save-lifetimes", default="", help="write the built lifetimes (JSON) here")
     ap.add_argument("--lifetimes", default="", help="reuse lifetimes saved by --save-lifetimes "
                     "instead of rebuilding the spectra (e.g. under a kernel tracer)")
@@ -174,7 +176,7 @@ def main() -> int:
         run(sched, W, 1)
         torch.cuda.synchronize()
         if profile:
-            dm.profile_begin(profile, 8192)
+            dm.profile_begin(profile, 16384)
         ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         ev0.record(stream)
@@ -193,6 +195,7 @@ def main() -> int:
         log(f"budget {pct}%: {K} steps in {ms:.2f} ms -> {K * 1000.0 / ms:.2f} steps/s")
     ms_all, prof_all = timed(all_active, args.profile_kernel)
     log(f"all-active: {K} steps in {ms_all:.2f} ms -> {K * 1000.0 / ms_all:.2f} steps/s")
+    kernels = {} if args.no_kernel_table else kernel_table(cfg, K, T, lambda c: timed(all_active, c)[1])
     tau_res = {}
     for t, sch in tau_scheds.items():
         ms, _ = timed(sch)
@@ -259,12 +262,52 @@ def main() -> int:
                            "frac_layer_steps": round(tau_scheds[t].layer_steps / (L * T), 4),
                            "speedup": round((K * 1000.0 / ms) / all_rate, 4)} for t, ms in tau_res.items()},
         "roofline": roofline,
+        "kernels": kernels,
         "frozen_path": frozen,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
     dm.close()
     return 0
+
+
+def kernel_table(cfg, K, T, profile) -> dict:
+    """Average launch duration of every kernel class of the all-active step (HIP events around
+    each launch on the step's stream, one timed pass per class) with its algorithmic work:
+    FLOP against the MFMA peak of the workload's dtype, bytes against HBM for the norms."""
+    M, d, F, H, dh, N, B = cfg.M, cfg.d, cfg.F, cfg.H, cfg.dh, cfg.N, cfg.B
+    es = 2 if cfg.dtype == "bf16" else 4
+    peak = PEAK_BF16 if cfg.dtype == "bf16" else PEAK_F32
+    fl = unit_flops(cfg)
+    classes = ["gemm_qkv", "attn", "gemm_o", "gemm_w1", "gemm_w2", "norm"]
+    if cfg.arch == "sdxl":
+        classes += ["gemm_x", "attn_x"]
+    if cfg.arch == "uvit":
+        classes += ["gemm_skip"]
+        fl["gemm_skip"] = 2.0 * M * d * 2 * d
+    if cfg.arch == "dit":
+        classes += ["cond"]
+    out = {}
+    for c in classes:
+        ms, n = profile(c)
+        if not n:
+            continue
+        rec = {"launches": n, "avg_us": round(ms * 1000.0 / n, 2)}
+        if c == "norm":
+            nbytes = M * d * (4 + es)  # fp32 stream in, normalised rows out
+            rec.update({"GB/s": round(nbytes * n / (ms / 1000.0) / 1e9, 1),
+                        "frac_hbm": round(nbytes * n / (ms / 1000.0) / PEAK_HBM, 4)})
+        elif c == "gemm_x":
+            # cross q / o projections every step, context k / v once per trajectory and unit
+            n_ctx = cfg.L * ((K + T - 1) // T)
+            total = (n - n_ctx) * 2.0 * M * d * d + n_ctx * 2.0 * B * cfg.ctx_len * 2 * d * cfg.ctx_dim
+            rec.update({"TFLOP/s": round(total / (ms / 1000.0) / 1e12, 1),
+                        "frac_peak": round(total / (ms / 1000.0) / peak, 4)})
+        elif c in fl:
+            rec.update({"TFLOP/s": round(fl[c] * n / (ms / 1000.0) / 1e12, 1),
+                        "frac_peak": round(fl[c] * n / (ms / 1000.0) / peak, 4)})
+        out[c] = rec
+    return out
 
 
 def cpu_baseline(cfg, weights, inputs, sched, seconds):
