@@ -134,14 +134,16 @@ def test_attention(P, dtype, B, H, nq, nk, dh):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("kind,d", [(0, 256), (0, 4096), (1, 1024), (1, 1280), (2, 1152)])
-def test_norm(P, dtype, kind, d):
-    rng = np.random.default_rng(kind * 100 + d)
-    M, ntok = 70, 35
+@pytest.mark.parametrize("kind,d,M", [(0, 256, 70), (0, 4096, 70), (1, 1024, 70), (1, 1280, 70), (2, 1152, 70),
+                                      # many rows: one wave per row, ragged last workgroup
+                                      (0, 256, 4099), (1, 1280, 4099), (2, 1152, 4099)])
+def test_norm(P, dtype, kind, d, M):
+    rng = np.random.default_rng(kind * 100 + d + M)
+    ntok = 35 if M == 70 else 4099
     x = (rng.standard_normal((M, d)) * 3 + 0.5).astype(np.float32)
     w = (1 + 0.1 * rng.standard_normal(d)).astype(np.float32)
     b = (0.1 * rng.standard_normal(d)).astype(np.float32)
-    mod = rng.standard_normal((2, 6 * d)).astype(np.float32)
+    mod = rng.standard_normal((-(-M // ntok), 6 * d)).astype(np.float32)
     y = empty((M, d), dtype)
     x64 = x.astype(np.float64)
     if kind == 0:
@@ -153,8 +155,8 @@ def test_norm(P, dtype, kind, d):
     else:
         md = dev(mod)
         P.op_norm(2, dev(x), y, 1e-6, shift=md[:, :d], scale=md[:, d:2 * d], ntok=ntok)
-        shift = np.repeat(mod[:, :d], ntok, axis=0)
-        scale = np.repeat(mod[:, d:2 * d], ntok, axis=0)
+        shift = np.repeat(mod[:, :d], ntok, axis=0)[:M]
+        scale = np.repeat(mod[:, d:2 * d], ntok, axis=0)[:M]
         ref = om.layernorm(x64, eps=1e-6) * (1 + scale) + shift
     got = host(y)
     if dtype == "bf16":
