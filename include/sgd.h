@@ -134,8 +134,10 @@ typedef struct {
 
 /* Alg. 1: score every matrix of every unit on the GPU (fp64 Gram of the short side,
  * Householder tridiagonalisation, host implicit-QL eigenvalues), then set lifetimes.
- * Synchronises hip_stream before returning.  Errors: SGD_E_ARG, SGD_E_DTYPE,
- * SGD_E_BUDGET, SGD_E_NUMERIC, SGD_E_HIP. */
+ * Offline, once per model: up to 16 host worker threads, each with its own stream and a
+ * temporary fp64 device workspace (allocated here and freed before returning; the step
+ * path allocates nothing).  Synchronises hip_stream before returning.  Errors: SGD_E_ARG,
+ * SGD_E_DTYPE, SGD_E_BUDGET, SGD_E_NUMERIC, SGD_E_HIP. */
 int sgd_schedule_build(const sgd_unit* units, int32_t L, const sgd_sched_params* params,
                        void* hip_stream, sgd_schedule* out);
 
@@ -177,7 +179,8 @@ typedef struct {
  * in-blocks, unit L/2 the mid block, unit l > L/2 takes the skip of in-block L-1-l;
  * token 0 of each sample is the time token, rewritten every step.
  * Shape limits: d % 128 == 0, F % 64 == 0, ctx_dim % 64 == 0, head_dim in {64, 72, 128}
- * (LLaDA: 128), ctx_len <= 128.                                                    */
+ * (LLaDA: 128).  Every unit weight, bias, gain and shift pointer is a device pointer,
+ * 16-byte aligned (the kernels read them in 16-byte vectors; SGD_E_ARG otherwise). */
 typedef struct {
     int32_t arch, dtype;
     int32_t B, N, d, H, head_dim, F, L, T;

@@ -1,0 +1,89 @@
+"""Summary of a rocprofv3 kernel trace of bench.py, as markdown.
+
+    rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o <w> -- \\
+        python3 bench.py --config <w> --no-cpu-baseline --no-kernel-table --taus "" \\
+        --lifetimes <lifetimes.json>
+    python -m paper_2609_29505_amd.trace_report --workload <w> --trace <dir>/<w>_kernel_trace.csv \\
+        --lifetimes <lifetimes.json>
+
+Prints the per-kernel statistics of the traced run and the frozen path's HBM rate from the
+trace's own durations: bench.py launches the budgets in increasing order, each as T warm-up
+and 2T timed steps from step 1, so the frozen-run dispatches appear in a known order and
+each one's algorithmic bytes follow from the schedule (maximal runs of frozen units, as the
+launcher fuses them).
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import json
+import os
+import sys
+from collections import defaultdict
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def kernel_stats(rows):
+    agg = defaultdict(lambda: [0, 0.0])
+    for r in rows:
+        a = agg[r["Kernel_Name"]]
+        a[0] += 1
+        a[1] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3  # us
+    tot = sum(v[1] for v in agg.values())
+    return sorted(((k, n, t, t / n, 100.0 * t / tot) for k, (n, t) in agg.items()), key=lambda x: -x[2])
+
+
+def frozen_rates(cfg, rows, lifetimes):
+    import numpy as np
+
+    import bench
+
+    T, L = cfg.T, cfg.L
+    W, K = T, 2 * T
+    fr = sorted((r for r in rows if "frozen_run_kernel" in r["Kernel_Name"]), key=lambda r: int(r["Start_Timestamp"]))
+    i, out = 0, []
+    for pct in sorted(cfg.budgets):
+        life = np.asarray(lifetimes[str(pct)])
+        act = np.arange(1, T + 1)[:, None] <= life[None, :]
+        nbytes, secs, n = 0, 0.0, 0
+        for phase, steps in (("warmup", W), ("timed", K)):
+            for j in range(steps):
+                for b in bench.frozen_launch_bytes(cfg, act[j % T]):
+                    r = fr[i]
+                    i += 1
+                    if phase == "timed":
+                        nbytes += b
+                        secs += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+                        n += 1
+        out.append((pct, n, nbytes, secs))
+    if i != len(fr):
+        raise SystemExit(f"trace has {len(fr)} frozen-run dispatches, the schedules predict {i}")
+    return out
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--workload", required=True)
+    ap.add_argument("--trace", required=True)
+    ap.add_argument("--lifetimes", required=True)
+    args = ap.parse_args()
+
+    import synth
+
+    cfg = synth.get_config(args.workload)
+    rows = list(csv.DictReader(open(args.trace)))
+    print("| kernel | calls | total ms | avg us | % |\n|---|---:|---:|---:|---:|")
+    for name, n, t, avg, pc in kernel_stats(rows)[:12]:
+        print(f"| `{name[:110]}` | {n} | {t / 1e3:.1f} | {avg:.2f} | {pc:.2f} |")
+    print("\n| budget | timed frozen-run launches | GB | ms | GB/s | of 8 TB/s |\n|---:|---:|---:|---:|---:|---:|")
+    for pct, n, nbytes, secs in frozen_rates(cfg, rows, json.load(open(args.lifetimes))):
+        print(f"| {pct}% | {n} | {nbytes / 1e9:.2f} | {secs * 1e3:.2f} | {nbytes / secs / 1e9:.0f} | "
+              f"{nbytes / secs / 8e12:.3f} |")
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
