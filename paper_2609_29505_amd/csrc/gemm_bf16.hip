@@ -18,6 +18,7 @@
 // (i, i + dh/2) of a head) are read from LDS whatever the wave layout.  V^T columns of a
 // head projection are written by a column-major pass (consecutive tokens per thread).
 #include <type_traits>
+#include <utility>
 
 #include "common.h"
 #include "kernels.h"
@@ -28,12 +29,23 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uns
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-template <bool B> struct BoolC { static constexpr bool value = B; };
+template <int I> using IntC = std::integral_constant<int, I>;
 
-template <int BM_, int BN_, int WGM_, int WGN_, int BK_, int STAGES_, int OCC_ = 2>
+// f(IntC<0>{}), ..., f(IntC<N - 1>{})
+template <class Fn, int... I>
+__device__ __forceinline__ void static_for_impl(Fn& f, std::integer_sequence<int, I...>) {
+    (f(IntC<I>{}), ...);
+}
+template <int N, class Fn>
+__device__ __forceinline__ void static_for(Fn&& f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+template <int BM_, int BN_, int WGM_, int WGN_, int BK_, int STAGES_, int OCC_ = 2, int RD_ = 1>
 struct TileCfg {
     static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, BK = BK_, STAGES = STAGES_;
     static constexpr int OCC = OCC_;                     // waves per SIMD the registers allow
+    static constexpr int RD = RD_;                       // k tiles in flight in registers
     static constexpr int NW = WGM * WGN;
     static constexpr int NT = NW * 64;
     static constexpr int WM = BM / WGM, WN = BN / WGN;   // wave tile
@@ -76,7 +88,7 @@ __device__ __forceinline__ float act_fn(float x) {
     return x;
 }
 
-// calls f(BoolC-like tag) with the activation as a compile-time constant
+// calls f(tag) with the activation as a compile-time constant
 template <class Fn>
 __device__ __forceinline__ void with_act(int act, Fn&& f) {
     switch (act) {
@@ -126,21 +138,36 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
     const int c = (tid % RI) * 4, rr0 = tid / RI;        // this thread's columns and first row
     const int cg = (tid % RIG) * 4, rrg0 = tid / RIG;    // gated
     const int n = n0 + c;
-    // q/k columns: projection, head and dims of this thread's columns (fixed), rotary
-    // inverse frequencies of its four dims
+    // q/k columns without rotation: projection, head and dims of this thread's columns
     const int vstart = ep.kind == EP_HEADS ? (2 - ep.which0) * ep.d : 0;
     int proj = 0, hh = 0, j = 0;
-    float inv[4] = {0.f, 0.f, 0.f, 0.f};
     if (ep.kind == EP_HEADS && n < g.N && n < vstart) {
         proj = ep.which0 + n / ep.d;
         const int nn = n - (proj - ep.which0) * ep.d;
         hh = nn / ep.dh;
         j = nn - hh * ep.dh;
-        if (ep.rope) {
-            const int jb = j < ep.dh / 2 ? j : j - ep.dh / 2;
+    }
+    // rotary q/k tiles (whole heads, all q or all k): a thread owns four rotary pairs, dims
+    // pj .. pj+3 and pj+dh/2 .. pj+dh/2+3 of head ph, so one sine/cosine serves both dims of
+    // a pair; invt holds the pairs' inverse frequencies in turns per token
+    constexpr int RIP = C::BN / 8, RPTP = C::NT / RIP, PERP = C::EPR / RPTP;
+    static_assert(C::NT % RIP == 0 && C::EPR % RPTP == 0, "rotary split");
+    const bool rope_tile = ep.kind == EP_HEADS && ep.rope && n0 < vstart;
+    const int rrp0 = tid / RIP;
+    int pc = 0, ph = 0, pj = 0;
+    float invt[4] = {0.f, 0.f, 0.f, 0.f};
+    bf16* pbase = qptr;
+    if (rope_tile) {
+        const int hd = ep.dh / 2, pi = (tid % RIP) * 4;
+        const int hl = pi / hd;
+        pj = pi - hl * hd;
+        pc = hl * ep.dh + pj;
+        const int pproj = ep.which0 + n0 / ep.d;
+        ph = (n0 - (pproj - ep.which0) * ep.d) / ep.dh + hl;
+        pbase = pproj == 0 ? qptr : kptr;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) inv[q] = exp2f(-(2.0f * (float)(jb + q) / (float)ep.dh) * ep.rope_log2_theta);
-        }
+        for (int q = 0; q < 4; ++q)
+            invt[q] = exp2f(-(2.0f * (float)(pj + q) / (float)ep.dh) * ep.rope_log2_theta) * 0.159154943091895336f;
     }
     // V^T columns straight from the accumulators: in the MFMA output layout lane l holds
     // column l % 32 of a 32 x 32 block and, for register group q, rows q * 8 + (l / 32) * 4
@@ -276,39 +303,46 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
                     if (ep.hcopy) store_bf16x4((bf16*)ep.hcopy + idx, hn);
                 }
             }
-        } else if (ep.kind == EP_HEADS) {
-            // q/k columns row-major (a thread stores four dims of one token), with the rotary
-            // pair read from LDS
+        } else if (rope_tile) {
+            // rotation of each pair by the token's angle: hardware sine/cosine (v_sin_f32 /
+            // v_cos_f32 take turns) of the fractional turn; the turn count carries ~1e-4 rad of
+            // fp32 rounding at 1024 tokens, far below the bf16 resolution of the output
             const int hd = ep.dh / 2;
+            const f32x4 b1 = ld4(sbias + pc), b2 = ld4(sbias + pc + hd);
+#pragma unroll 2
+            for (int u = 0; u < PERP; ++u) {
+                const int rr = rrp0 + u * RPTP, row = grow(rr);
+                const f32x4 v1 = ld4(st + rr * C::EPS + pc), v2 = ld4(st + rr * C::EPS + pc + hd);
+                if (row >= g.M) continue;
+                const int bs = sample_of(row), tok = row - bs * ep.ntok;
+                float o1[4], o2[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float x1 = v1[q] + b1[q], x2 = v2[q] + b2[q];
+                    const float t = (float)tok * invt[q];
+                    const float f = t - rintf(t);
+                    const float sn = __builtin_amdgcn_sinf(f), cs = __builtin_amdgcn_cosf(f);
+                    o1[q] = x1 * cs - x2 * sn;
+                    o2[q] = x2 * cs + x1 * sn;
+                }
+                bf16* const dst = pbase + (((long)bs * ep.H + ph) * ep.np + tok) * ep.dh + pj;
+                store_bf16x4(dst, o1);
+                store_bf16x4(dst + hd, o2);
+            }
+        } else if (ep.kind == EP_HEADS) {
+            // q/k columns without rotation, row-major (a thread stores four dims of one token)
             if (n < g.N && n < vstart) {
-                const bool lo = j < hd;
-                const int pc = lo ? c + hd : c - hd;  // partner columns, same tile
                 const f32x4 bb = ld4(sbias + c);
-                const f32x4 pb = ep.rope ? ld4(sbias + pc) : f32x4{0.f, 0.f, 0.f, 0.f};
                 bf16* const base = proj == 0 ? qptr : kptr;
 #pragma unroll 2
                 for (int u = 0; u < PER; ++u) {
                     const int rr = rr0 + u * RPT, row = grow(rr);
                     const f32x4 v = ld4(st + rr * C::EPS + c);
-                    const f32x4 pv = ep.rope ? ld4(st + rr * C::EPS + pc) : f32x4{0.f, 0.f, 0.f, 0.f};
                     if (row >= g.M) continue;
                     const int bs = sample_of(row), tok = row - bs * ep.ntok;
                     float o[4];
 #pragma unroll
                     for (int q = 0; q < 4; ++q) o[q] = v[q] + bb[q];
-                    if (ep.rope) {
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            // hardware sine/cosine (v_sin_f32 / v_cos_f32) of the angle reduced
-                            // to its fractional turn: ~1e-4 rad of fp32 rounding at 1024 tokens,
-                            // far below the bf16 resolution of the output
-                            const float turns = (float)tok * inv[q] * 0.159154943091895336f;
-                            const float ang = (turns - rintf(turns)) * 6.28318530717958648f;
-                            const float sn = __sinf(ang), cs = __cosf(ang);
-                            const float pq = pv[q] + pb[q];
-                            o[q] = lo ? o[q] * cs - pq * sn : o[q] * cs + pq * sn;
-                        }
-                    }
                     store_bf16x4(base + (((long)bs * ep.H + hh) * ep.np + tok) * ep.dh + j, o);
                 }
             }
@@ -319,12 +353,14 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
 
 // --------------------------------------------------------------------------- kernel
 //
-// Three-stage pipeline with two LDS stages: in the period between the barriers before the
-// last k-steps of tiles kt - 1 and kt, the MFMAs consume tile kt (one stage), tile kt + 1
-// moves from registers into the other stage, and tile kt + 2 is loaded into the freed
-// registers.  The register -> LDS writes and the loads are interleaved one part at a time
-// with the period's MFMAs (part p after MFMA slot p * SLOTS / PARTS), so neither the
-// texture unit nor the LDS sees a burst and both SIMD waves keep issuing MFMAs.
+// Pipeline with two LDS stages and a ring of RD register slots: in the period between the
+// barriers before the last k-steps of tiles kt - 1 and kt, the MFMAs consume tile kt (one
+// stage), tile kt + 1 moves from its register slot into the other stage, and tile
+// kt + 1 + RD is loaded into the freed slot, so a load has RD periods to arrive.  Small
+// tiles have short periods and need RD > 1 to cover the latency of weights streamed from
+// HBM.  The register -> LDS writes and the loads are interleaved one part at a time with
+// the period's MFMAs (part p after MFMA slot p * SLOTS / PARTS), so neither the texture
+// unit nor the LDS sees a burst and both SIMD waves keep issuing MFMAs.
 
 template <class C>
 __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, EpiParams ep) {
@@ -348,41 +384,52 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
     const __amdgpu_buffer_rsrc_t rb = buf_rsrc(g.B, (unsigned)((long)g.N * g.ldb * 2));
 
     // thread -> (row, chunk) of a stage: chunk tid % CH of rows tid / CH + p * RPP; parts
-    // 0 .. AP-1 are A rows, AP .. AP+BP-1 are B rows
+    // 0 .. AP-1 are A rows, AP .. AP+BP-1 are B rows.  LDS holds the A stages, then the B
+    // stages.  The swizzle key (r / RPB) % CH of a row does not change when r moves by a
+    // multiple of CH * RPB rows, so a thread's write positions (rows vr + p RPP) and fragment
+    // positions (rows w0 + i 32 + lrow) are one base register plus compile-time offsets.
     constexpr int RPP = C::NT / C::CH;
     constexpr int AP = C::BM / RPP, BP = C::BN / RPP, PARTS = AP + BP;
     static_assert(C::BM % RPP == 0 && C::BN % RPP == 0 && (C::BN / 2) % RPP == 0, "pass split");
+    static_assert(RPP % (C::CH * C::RPB) == 0 && 32 % (C::CH * C::RPB) == 0, "row-invariant swizzle key");
+    constexpr int B_LDS = C::STAGES * C::A_BYTES;  // first B stage
     const int vc = tid % C::CH, vr = tid / C::CH;
-    unsigned goff0[PARTS], goff1[AP];
-    int loff[PARTS];
+    unsigned goff[PARTS];  // A rows of both A sources share the row pitch
 #pragma unroll
-    for (int p = 0; p < AP; ++p) {
-        const int r = vr + p * RPP;
-        goff0[p] = (unsigned)((long)(m0 + r) * g.lda0 * 2 + vc * 16);
-        goff1[p] = (unsigned)((long)(m0 + r) * g.lda1 * 2 + vc * 16);
-        loff[p] = r * C::ROWB + ((vc ^ ((r / C::RPB) % C::CH)) << 4);
-    }
+    for (int p = 0; p < AP; ++p) goff[p] = (unsigned)((long)(m0 + vr + p * RPP) * g.lda0 * 2 + vc * 16);
 #pragma unroll
     for (int p = 0; p < BP; ++p) {
         const int r = vr + p * RPP;
         long gr;
         if (gated) gr = r < C::BN / 2 ? (long)tn * (C::BN / 2) + r : (long)F + tn * (C::BN / 2) + (r - C::BN / 2);
         else gr = (long)tn * C::BN + r;
-        goff0[AP + p] = (unsigned)(gr * g.ldb * 2 + vc * 16);
-        loff[AP + p] = C::A_BYTES + r * C::ROWB + ((vc ^ ((r / C::RPB) % C::CH)) << 4);
+        goff[AP + p] = (unsigned)(gr * g.ldb * 2 + vc * 16);
     }
-    u32x4 vreg[PARTS];
-    auto gload = [&](int kt, int p) {
+    char* const lw = lds + vr * C::ROWB + ((vc ^ ((vr / C::RPB) % C::CH)) << 4);
+    // register slot s holds the k tiles t with t % RD == s (s is a compile-time constant at
+    // every call).  Tiles at or past K load zeros: their offset lies past every operand
+    // buffer (sizes stay below OOB), so the descriptor's range check fails.  The main loop
+    // therefore runs whole trips without a branch, the padding tiles add zero products, and
+    // the compiler sees the same outstanding loads on every trip.
+    const int KT = g.K / C::BK;
+    constexpr unsigned OOB = 0xFFFFFF00u;
+    u32x4 vreg[C::RD][PARTS];
+    auto gload = [&](int kt, int s, int p) {
+        const bool in = kt < KT;
         const int k0 = kt * C::BK;
         if (p < AP) {
             const bool second = g.A1 && k0 >= g.K0;
-            vreg[p] = __builtin_amdgcn_raw_buffer_load_b128(second ? ra1 : ra0, second ? goff1[p] : goff0[p],
-                                                            second ? (k0 - g.K0) * 2 : k0 * 2, 0);
+            vreg[s][p] = __builtin_amdgcn_raw_buffer_load_b128(second ? ra1 : ra0, in ? goff[p] : OOB,
+                                                               in ? (second ? (k0 - g.K0) * 2 : k0 * 2) : 0, 0);
         } else {
-            vreg[p] = __builtin_amdgcn_raw_buffer_load_b128(rb, goff0[p], k0 * 2, 0);
+            vreg[s][p] = __builtin_amdgcn_raw_buffer_load_b128(rb, in ? goff[p] : OOB, in ? k0 * 2 : 0, 0);
         }
     };
-    auto lwrite = [&](int stage, int p) { *(u32x4*)(lds + stage * C::STAGE_BYTES + loff[p]) = vreg[p]; };
+    // stage and part are compile-time constants at every call
+    auto lwrite = [&](int stage, int s, int p) {
+        if (p < AP) *(u32x4*)(lw + stage * C::A_BYTES + p * RPP * C::ROWB) = vreg[s][p];
+        else *(u32x4*)(lw + B_LDS + stage * C::B_BYTES + (p - AP) * RPP * C::ROWB) = vreg[s][p];
+    };
 
     const int wm = wave / C::WGN, wn = wave % C::WGN;
     const int wm0 = wm * C::WM, wn0 = wn * C::WN;
@@ -397,31 +444,26 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
     bf16x8 af[2][C::TM], bfr[2][C::TN];
+    const int fkey = (lrow / C::RPB) % C::CH;
+    const char* const fa = lds + (wm0 + lrow) * C::ROWB;
+    const char* const fb = lds + B_LDS + (wn0 + lrow) * C::ROWB;
     auto frags = [&](int stage, int q, int buf) {
-        const char* sa = lds + stage * C::STAGE_BYTES;
-        const char* sb = sa + C::A_BYTES;
-        const int c = q * 2 + lhalf;
+        const int sw = ((q * 2 + lhalf) ^ fkey) << 4;
 #pragma unroll
-        for (int i = 0; i < C::TM; ++i) {
-            const int r = wm0 + i * 32 + lrow;
-            af[buf][i] = *(const bf16x8*)(sa + r * C::ROWB + ((c ^ ((r / C::RPB) % C::CH)) << 4));
-        }
+        for (int i = 0; i < C::TM; ++i)
+            af[buf][i] = *(const bf16x8*)(fa + sw + stage * C::A_BYTES + i * 32 * C::ROWB);
 #pragma unroll
-        for (int j = 0; j < C::TN; ++j) {
-            const int r = wn0 + j * 32 + lrow;
-            bfr[buf][j] = *(const bf16x8*)(sb + r * C::ROWB + ((c ^ ((r / C::RPB) % C::CH)) << 4));
-        }
+        for (int j = 0; j < C::TN; ++j)
+            bfr[buf][j] = *(const bf16x8*)(fb + sw + stage * C::B_BYTES + j * 32 * C::ROWB);
     };
-    const int KT = g.K / C::BK;
     constexpr int MPK = C::TM * C::TN, SLOTS = C::KSTEPS * MPK;
     static_assert(PARTS <= SLOTS, "part spreading");
     // MFMAs of one k-step; `part` is the k-step's position in its period.  The period moves
-    // tile wt (registers -> stage ws) and loads tile lt into the registers.  The compiler
-    // inserts the vmcnt waits from the register dependences; in the branch-free steady state
-    // (STEADY) that is vmcnt(PARTS - 1) before every write.
-    auto mfmas = [&](int buf, int part, int wt, int ws, int lt, auto steady) {
-        constexpr bool STEADY = decltype(steady)::value;
-        const bool wr = STEADY || wt < KT, ld = STEADY || lt < KT;
+    // a tile from register slot S into stage ws and loads tile lt into slot S.  The compiler
+    // inserts the vmcnt waits from the register dependences: vmcnt(RD * PARTS - 1) before
+    // every write.
+    auto mfmas = [&](int buf, int part, int ws, int lt, auto rs) {
+        constexpr int S = decltype(rs)::value;
 #pragma unroll
         for (int i = 0; i < C::TM; ++i)
 #pragma unroll
@@ -429,72 +471,78 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[buf][i], bfr[buf][j], acc[i][j], 0, 0, 0);
                 const int slot = part * MPK + i * C::TN + j;
                 const int p = (slot * PARTS + SLOTS - 1) / SLOTS;
-                if (p < PARTS && (p * SLOTS) / PARTS == slot && wr) {
+                if (p < PARTS && (p * SLOTS) / PARTS == slot) {
                     __builtin_amdgcn_sched_barrier(0);
-                    lwrite(ws, p);
-                    if (ld) gload(lt, p);
+                    lwrite(ws, S, p);
+                    gload(lt, S, p);
                     __builtin_amdgcn_sched_barrier(0);
                 }
             }
     };
 
-    // prologue: tile 0 into stage 0, tile 1 into the registers.  The first period has no
-    // "last k-step of tile -1", so the parts of its first slot group (write tile 1, load
-    // tile 2) are done here.
+    // prologue: tile 0 into stage 0, tiles 1 .. RD into the register slots (tile RD shares
+    // slot 0 with tile 0).  The first period has no "last k-step of tile -1", so the parts of
+    // its first slot group (write tile 1, load tile 1 + RD) are done here.
 #pragma unroll
-    for (int p = 0; p < PARTS; ++p) gload(0, p);
+    for (int p = 0; p < PARTS; ++p) gload(0, 0, p);
+    static_for<C::RD - 1>([&](auto jc) {
+        constexpr int TT = decltype(jc)::value + 1;
 #pragma unroll
-    for (int p = 0; p < PARTS; ++p) lwrite(0, p);
-    if (KT > 1) {
+        for (int p = 0; p < PARTS; ++p) gload(TT, TT, p);
+    });
 #pragma unroll
-        for (int p = 0; p < PARTS; ++p) gload(1, p);
+    for (int p = 0; p < PARTS; ++p) {
+        lwrite(0, 0, p);
+        gload(C::RD, 0, p);
+    }
 #pragma unroll
-        for (int p = 0; p < PARTS; ++p) {
-            if ((p * SLOTS) / PARTS < MPK) {
-                lwrite(1, p);
-                if (KT > 2) gload(2, p);
-            }
+    for (int p = 0; p < PARTS; ++p) {
+        if ((p * SLOTS) / PARTS < MPK) {
+            lwrite(1, 1 % C::RD, p);
+            gload(1 + C::RD, 1 % C::RD, p);
         }
     }
     __syncthreads();
     frags(0, 0, 0);
-    // one k tile; the period of tile kt (from the barrier before tile kt-1's last k-step)
-    // moves tile kt + 1 into stage st ^ 1 and loads tile kt + 2, and the period of tile
-    // kt + 1 starts with the last k-step
-    auto iter = [&](int kt, auto steady) {
-        constexpr bool STEADY = decltype(steady)::value;
-        const int st = kt & 1;
+    // one k tile; jc is its position in the trip (tile kt sits in register slot J = kt % RD
+    // and LDS stage st = kt % 2).  The period of tile kt (from the barrier before tile kt-1's
+    // last k-step) moves tile kt + 1 into stage st ^ 1 and loads tile kt + 1 + RD, and the
+    // period of tile kt + 1 starts with the last k-step
+    auto iter = [&](int kt, auto jc) {
+        constexpr int J = decltype(jc)::value % C::RD, st = decltype(jc)::value % 2;
 #pragma unroll
         for (int q = 0; q < C::KSTEPS; ++q) {
             const int cur = q & 1, nxt = cur ^ 1;
             __builtin_amdgcn_sched_barrier(0);
             if (q + 1 < C::KSTEPS) {
                 frags(st, q + 1, nxt);
-            } else if (STEADY || kt + 1 < KT) {
+            } else {
                 __syncthreads();  // tile kt + 1 is in stage st ^ 1; stage st is free
                 frags(st ^ 1, 0, nxt);
             }
             __builtin_amdgcn_sched_barrier(0);
-            if (q + 1 < C::KSTEPS) mfmas(cur, q + 1, kt + 1, st ^ 1, kt + 2, steady);
-            else mfmas(cur, 0, kt + 2, st, kt + 3, steady);
+            if (q + 1 < C::KSTEPS) mfmas(cur, q + 1, st ^ 1, kt + 1 + C::RD, IntC<(J + 1) % C::RD>{});
+            else mfmas(cur, 0, st, kt + 2 + C::RD, IntC<(J + 2) % C::RD>{});
         }
     };
     static_assert(C::KSTEPS % 2 == 0, "fragment ring");
-    int kt = 0;
-    for (; kt + 3 < KT; ++kt) iter(kt, BoolC<true>{});
-    for (; kt < KT; ++kt) iter(kt, BoolC<false>{});
+    constexpr int TRIP = C::RD % 2 ? 2 * C::RD : C::RD;  // whole register rings and LDS stage pairs
+    for (int kt = 0; kt < KT; kt += TRIP) static_for<TRIP>([&](auto jc) { iter(kt + decltype(jc)::value, jc); });
     epilogue<C>(acc, lds, g, ep, m0, tn, wm, wn0);
 }
 
 // --------------------------------------------------------------------------- dispatch
 
 namespace {
-// block tiles (BM, BN); eight waves, 64-deep k tiles, two LDS stages plus the register stage.
-// (Four waves of 128 x 128, one per SIMD, measured 10-20 % slower on every branch shape.)
-using T256x256 = TileCfg<256, 256, 4, 2, 64, 2>;  // 64 x 128 wave tiles
-using T256x128 = TileCfg<256, 128, 4, 2, 64, 2>;  // 64 x 64
-using T128x256 = TileCfg<128, 256, 2, 4, 64, 2>;  // 64 x 64
-using T128x128 = TileCfg<128, 128, 2, 4, 64, 2>;  // 64 x 32
+// block tiles (BM, BN); eight waves, 64-deep k tiles, two LDS stages plus RD register slots.
+// Two slots on the smaller tiles: with weights streamed from HBM, one period of a 128 x 128
+// tile is too short for a load to arrive (LLaDA O and W2: -17 % time with two slots); the
+// 256 x 256 tile has a period twice as long and no registers to spare.  (Four waves of
+// 128 x 128, one per SIMD, measured 10-20 % slower on every branch shape.)
+using T256x256 = TileCfg<256, 256, 4, 2, 64, 2, 2, 1>;  // 64 x 128 wave tiles
+using T256x128 = TileCfg<256, 128, 4, 2, 64, 2, 2, 2>;  // 64 x 64
+using T128x256 = TileCfg<128, 256, 2, 4, 64, 2, 2, 2>;  // 64 x 64
+using T128x128 = TileCfg<128, 128, 2, 4, 64, 2, 2, 2>;  // 64 x 32
 
 struct Shape { int bm, bn; double rate; };
 // tile id -> block shape and its per-CU throughput relative to 256 x 256 (measured on the
@@ -540,7 +588,7 @@ bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
     const Shape s = tile_shape(tile);
     if (!s.bm) return false;
     if (g.M >= (1 << 21)) return false;  // the epilogue's fp32 row -> sample split is exact below
-    if (g.K % 64 || (g.A1 && g.K0 % 64)) return false;
+    if (g.K % 64 || (g.A1 && (g.K0 % 64 || g.lda1 != g.lda0))) return false;
     if (g.N % 4 || g.lda0 % 8 || (g.A1 && g.lda1 % 8) || g.ldb % 8) return false;  // 16-byte rows
     if (e.kind == EP_GATED && (g.N % s.bn || e.ldo % 4)) return false;
     if (e.kind == EP_ACT && e.ldo % 4) return false;
@@ -549,9 +597,9 @@ bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
         if (e.d % 32 || e.dh % 4) return false;  // V^T from whole 32-column MFMA blocks
         if (e.rope && (e.dh % 8 || s.bn % e.dh || e.d % s.bn)) return false;  // whole heads per tile
     }
-    if ((long)g.M * g.lda0 * 2 >= (1L << 32) || (g.A1 && (long)g.M * g.lda1 * 2 >= (1L << 32)) ||
-        (long)g.N * g.ldb * 2 >= (1L << 32))
-        return false;  // 32-bit buffer ranges
+    const long lim = 0xFFFFFF00L;  // 32-bit buffer ranges below the loader's out-of-range offset
+    if ((long)g.M * g.lda0 * 2 > lim || (g.A1 && (long)g.M * g.lda1 * 2 > lim) || (long)g.N * g.ldb * 2 > lim)
+        return false;
     return true;
 }
 

@@ -1,11 +1,13 @@
 """Single-kernel microbenchmark of the scheduled step's kernels at a workload's shapes.
 
     python -m paper_2609_29505_amd.kernel_bench --workload llada --kernel gemm_w1 [--reps 20]
-                                                [--copy-mib 256]
+                                                [--cold] [--copy-mib 256]
 
 Runs one kernel class of the step (through the sgd_ops.h entry points, on seeded random
 operands of the workload's shapes) `reps` times and prints its average duration from HIP
-events.  --copy-mib appends a device-to-device copy of that many MiB, a plain copy of known
+events.  --cold cycles through enough distinct weight matrices (>= 1 GiB in all) that every
+launch streams its weights from HBM, as the step does (each unit has its own weights); by
+default one weight matrix is reused and stays in the 256 MB Infinity Cache.  --copy-mib appends a device-to-device copy of that many MiB, a plain copy of known
 size that calibrates the FETCH_SIZE / WRITE_SIZE counters of a rocprofv3 --pmc pass run over
 the same command.  Kernels: gemm_qkv, gemm_o, gemm_w1, gemm_w2, attn, frozen (a run of
 --frozen-r cached updates).
@@ -28,6 +30,7 @@ def main() -> int:
     ap.add_argument("--reps", type=int, default=20)
     ap.add_argument("--frozen-r", type=int, default=4)
     ap.add_argument("--copy-mib", type=int, default=0)
+    ap.add_argument("--cold", action="store_true")
     args = ap.parse_args()
 
     import torch
@@ -47,24 +50,38 @@ def main() -> int:
     def rnd(*shape, scale=1.0, dtype=bf):
         return (torch.randn(*shape, device=dev) * scale).to(dtype)
 
+    def weights(*shape, scale=1.0):
+        # one matrix, or (--cold) a cycle of copies that no cache level holds
+        n = 1
+        if args.cold:
+            nbytes = 2 * shape[0] * shape[1]
+            n = max(2, -(-(1 << 30) // nbytes))
+        ws = [rnd(*shape, scale=scale) for _ in range(n)]
+        state = {"i": -1}
+
+        def nxt():
+            state["i"] = (state["i"] + 1) % n
+            return ws[state["i"]]
+        return nxt
+
     k = args.kernel
     if k == "gemm_w1":
         n1 = 2 * F if cfg.gated else F
-        A, W, out = rnd(M, d), rnd(n1, d, scale=d ** -0.5), torch.empty(M, F, device=dev, dtype=bf)
+        A, W, out = rnd(M, d), weights(n1, d, scale=d ** -0.5), torch.empty(M, F, device=dev, dtype=bf)
         act = {"llada": 3, "dit": 2}.get(cfg.arch, 1)
-        fn = lambda: P.op_linear(A, W, out, act=act, gated=cfg.gated)  # noqa: E731
+        fn = lambda: P.op_linear(A, W(), out, act=act, gated=cfg.gated)  # noqa: E731
         flop = 2.0 * M * n1 * d
     elif k == "gemm_qkv":
-        A, W = rnd(M, d), rnd(3 * d, d, scale=d ** -0.5)
+        A, W = rnd(M, d), weights(3 * d, d, scale=d ** -0.5)
         q = torch.empty(B * H, np_, dh, device=dev, dtype=bf)
         kk = torch.empty_like(q)
         vt = torch.empty(B * H, dh, np_, device=dev, dtype=bf)
-        fn = lambda: P.op_heads(A, W, q, kk, vt, 3, 0, N, H, dh, rope=cfg.arch == "llada")  # noqa: E731
+        fn = lambda: P.op_heads(A, W(), q, kk, vt, 3, 0, N, H, dh, rope=cfg.arch == "llada")  # noqa: E731
         flop = 2.0 * M * 3 * d * d
     elif k in ("gemm_o", "gemm_w2"):
         kd = d if k == "gemm_o" else F
-        A, W, h = rnd(M, kd), rnd(d, kd, scale=kd ** -0.5), torch.randn(M, d, device=dev)
-        fn = lambda: P.op_residual(A, W, h)  # noqa: E731
+        A, W, h = rnd(M, kd), weights(d, kd, scale=kd ** -0.5), torch.randn(M, d, device=dev)
+        fn = lambda: P.op_residual(A, W(), h)  # noqa: E731
         flop = 2.0 * M * d * kd
     elif k == "attn":
         q = rnd(B * H, np_, dh)
@@ -90,7 +107,7 @@ def main() -> int:
     e1.record()
     torch.cuda.synchronize()
     us = e0.elapsed_time(e1) / args.reps * 1e3
-    line = f"{cfg.name} {k}: {us:.1f} us per launch"
+    line = f"{cfg.name} {k}{' (cold weights)' if args.cold else ''}: {us:.1f} us per launch"
     if flop:
         line += f", {flop / us / 1e6:.1f} TFLOP/s"
     else:
