@@ -21,8 +21,8 @@ enum sgd_act { SGD_ACT_NONE = 0, SGD_ACT_GELU_ERF = 1, SGD_ACT_GELU_TANH = 2, SG
 /* out[M x N] = act(A[M x K] W[N x K]^T + bias) in dtype (the branch GEMM of an MLP input
  * projection).  gated != 0: W is [2N x K] = [W_gate; W_up] and out = act(A W_gate^T +
  * b[:N]) * (A W_up^T + b[N:]).  lda/ldw/ldo are row strides in elements.  tile selects a
- * bf16 kernel variant (0 auto; 1..4 fixed block tiles, for tests and sweeps: 1 256x256,
- * 2 256x128, 3 128x256, 4 128x128, rows x columns).  Shape limits (bf16): K % 64 == 0,
+ * bf16 kernel variant (0 auto; 1..5 fixed block tiles, for tests and sweeps: 1 256x256,
+ * 2 256x128, 3 128x256, 4 128x128, 5 256x192, rows x columns).  Shape limits (bf16): K % 64 == 0,
  * N % 4 == 0, gated N a multiple of the tile width, operand rows and bias 16-byte aligned;
  * (fp32): K % 16 == 0, N % 64 == 0. */
 int sgd_op_linear(int32_t dtype, const void* A, int64_t lda, const void* W, int64_t ldw, const float* bias,

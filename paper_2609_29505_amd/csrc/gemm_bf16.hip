@@ -108,12 +108,16 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
                                          const EpiParams& ep, int m0, int tn, int wm, int wn0) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int lrow = lane & 31, lhalf = lane >> 5;
+    // Thread t handles rows r0(t) + u * RPT of its columns.  When the items of a row do not
+    // divide the block (192-column tiles), the threads past the last whole pass have no items
+    // (r0 = EPR) and a thread's last items may fall past the chunk (EX* false: checked).
     constexpr int RI = C::BN / 4;                        // four-column items per row
     constexpr int RPT = C::NT / RI;                      // chunk rows per pass of the block
-    constexpr int PER = C::EPR / RPT;                    // items per thread per chunk
-    constexpr int RIG = RI / 2, RPTG = C::NT / RIG, PERG = C::EPR / RPTG;  // gated: gate half
+    constexpr int PER = (C::EPR + RPT - 1) / RPT;        // items per thread per chunk
+    constexpr bool EXA = C::NT % RI == 0 && C::EPR % RPT == 0;
+    constexpr int RIG = RI / 2, RPTG = C::NT / RIG, PERG = (C::EPR + RPTG - 1) / RPTG;  // gated: gate half
+    constexpr bool EXG = C::NT % RIG == 0 && C::EPR % RPTG == 0;
     constexpr int EB = PER < 4 ? PER : 4;                // residual items per load group
-    static_assert(C::NT % RI == 0 && C::EPR % RPT == 0 && C::EPR % RPTG == 0 && PER % EB == 0, "epilogue split");
     float* st = (float*)lds;
     float* sbias = st + C::EPR * C::EPS;                 // the tile's bias columns
     const int n0 = tn * C::BN;
@@ -135,8 +139,8 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
     // sample of a row: floor((row + 0.5) / ntok) in fp32 is exact while row < 2^21
     const float rntok = 1.0f / (float)ep.ntok;
     auto sample_of = [&](int row) { return (int)(((float)row + 0.5f) * rntok); };
-    const int c = (tid % RI) * 4, rr0 = tid / RI;        // this thread's columns and first row
-    const int cg = (tid % RIG) * 4, rrg0 = tid / RIG;    // gated
+    const int c = (tid % RI) * 4, rr0 = tid < RI * RPT ? tid / RI : C::EPR;  // columns, first row
+    const int cg = (tid % RIG) * 4, rrg0 = tid < RIG * RPTG ? tid / RIG : C::EPR;  // gated
     const int n = n0 + c;
     // q/k columns without rotation: projection, head and dims of this thread's columns
     const int vstart = ep.kind == EP_HEADS ? (2 - ep.which0) * ep.d : 0;
@@ -150,10 +154,10 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
     // rotary q/k tiles (whole heads, all q or all k): a thread owns four rotary pairs, dims
     // pj .. pj+3 and pj+dh/2 .. pj+dh/2+3 of head ph, so one sine/cosine serves both dims of
     // a pair; invt holds the pairs' inverse frequencies in turns per token
-    constexpr int RIP = C::BN / 8, RPTP = C::NT / RIP, PERP = C::EPR / RPTP;
-    static_assert(C::NT % RIP == 0 && C::EPR % RPTP == 0, "rotary split");
+    constexpr int RIP = C::BN / 8, RPTP = C::NT / RIP, PERP = (C::EPR + RPTP - 1) / RPTP;
+    constexpr bool EXP = C::NT % RIP == 0 && C::EPR % RPTP == 0;
     const bool rope_tile = ep.kind == EP_HEADS && ep.rope && n0 < vstart;
-    const int rrp0 = tid / RIP;
+    const int rrp0 = tid < RIP * RPTP ? tid / RIP : C::EPR;
     int pc = 0, ph = 0, pj = 0;
     float invt[4] = {0.f, 0.f, 0.f, 0.f};
     bf16* pbase = qptr;
@@ -230,6 +234,7 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
 #pragma unroll 2
                 for (int u = 0; u < PERG; ++u) {
                     const int rr = rrg0 + u * RPTG, row = grow(rr);
+                    if (!EXG && rr >= C::EPR) continue;
                     const f32x4 gv = ld4(st + rr * C::EPS + cg), uv = ld4(st + rr * C::EPS + C::BN / 2 + cg);
                     if (row >= g.M) continue;
                     float o[4];
@@ -245,6 +250,7 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
 #pragma unroll 2
                 for (int u = 0; u < PER; ++u) {
                     const int rr = rr0 + u * RPT, row = grow(rr);
+                    if (!EXA && rr >= C::EPR) continue;
                     const f32x4 v = ld4(st + rr * C::EPS + c);
                     if (row >= g.M || n >= g.N) continue;
                     float o[4];
@@ -276,6 +282,7 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
 #pragma unroll
                 for (int w = 0; w < EB; ++w) {
                     const int rr = rr0 + (u0 + w) * RPT, row = grow(rr);
+                    if (!EXA && rr >= C::EPR) continue;  // also items u0 + w >= PER
                     const f32x4 v = ld4(st + rr * C::EPS + c);
                     if (row >= g.M || n >= g.N) continue;
                     const long idx = (long)row * ep.d + n;
@@ -312,6 +319,7 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
 #pragma unroll 2
             for (int u = 0; u < PERP; ++u) {
                 const int rr = rrp0 + u * RPTP, row = grow(rr);
+                if (!EXP && rr >= C::EPR) continue;
                 const f32x4 v1 = ld4(st + rr * C::EPS + pc), v2 = ld4(st + rr * C::EPS + pc + hd);
                 if (row >= g.M) continue;
                 const int bs = sample_of(row), tok = row - bs * ep.ntok;
@@ -337,6 +345,7 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
 #pragma unroll 2
                 for (int u = 0; u < PER; ++u) {
                     const int rr = rr0 + u * RPT, row = grow(rr);
+                    if (!EXA && rr >= C::EPR) continue;
                     const f32x4 v = ld4(st + rr * C::EPS + c);
                     if (row >= g.M) continue;
                     const int bs = sample_of(row), tok = row - bs * ep.ntok;
@@ -390,7 +399,7 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
     // positions (rows w0 + i 32 + lrow) are one base register plus compile-time offsets.
     constexpr int RPP = C::NT / C::CH;
     constexpr int AP = C::BM / RPP, BP = C::BN / RPP, PARTS = AP + BP;
-    static_assert(C::BM % RPP == 0 && C::BN % RPP == 0 && (C::BN / 2) % RPP == 0, "pass split");
+    static_assert(C::BM % RPP == 0 && C::BN % RPP == 0, "pass split");
     static_assert(RPP % (C::CH * C::RPB) == 0 && 32 % (C::CH * C::RPB) == 0, "row-invariant swizzle key");
     constexpr int B_LDS = C::STAGES * C::A_BYTES;  // first B stage
     const int vc = tid % C::CH, vr = tid / C::CH;
@@ -543,6 +552,7 @@ using T256x256 = TileCfg<256, 256, 4, 2, 64, 2, 2, 1>;  // 64 x 128 wave tiles
 using T256x128 = TileCfg<256, 128, 4, 2, 64, 2, 2, 2>;  // 64 x 64
 using T128x256 = TileCfg<128, 256, 2, 4, 64, 2, 2, 2>;  // 64 x 64
 using T128x128 = TileCfg<128, 128, 2, 4, 64, 2, 2, 2>;  // 64 x 32
+using T256x192 = TileCfg<256, 192, 4, 2, 64, 2, 2, 2>;  // 64 x 96
 
 struct Shape { int bm, bn; double rate; };
 // tile id -> block shape and its per-CU throughput relative to 256 x 256 (measured on the
@@ -553,6 +563,7 @@ Shape tile_shape(int tile) {
         case 2: return {256, 128, 0.78};
         case 3: return {128, 256, 0.80};
         case 4: return {128, 128, 0.51};
+        case 5: return {256, 192, 0.82};
         default: return {0, 0, 0.0};
     }
 }
@@ -617,6 +628,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& g, const EpiParams& e, hipStream_t s
         case 2: return run_tile<T256x128>(g, e, st);
         case 3: return run_tile<T128x256>(g, e, st);
         case 4: return run_tile<T128x128>(g, e, st);
+        case 5: return run_tile<T256x192>(g, e, st);
         default: return hipErrorInvalidValue;
     }
 }

@@ -39,8 +39,8 @@ struct EpiParams {
 };
 
 // dtype: 0 fp32, 1 bf16.  tile: 0 = pick automatically; 1..kGemmTiles a fixed bf16 block
-// tile (1: 256x256, 2: 256x128, 3: 128x256, 4: 128x128).
-constexpr int kGemmTiles = 4;
+// tile (1: 256x256, 2: 256x128, 3: 128x256, 4: 128x128, 5: 256x192).
+constexpr int kGemmTiles = 5;
 hipError_t launch_gemm(int dtype, const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile = 0);
 bool gemm_shape_ok(int dtype, const GemmArgs& g, const EpiParams& e, int tile = 0);
 hipError_t launch_gemm_bf16(const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile);

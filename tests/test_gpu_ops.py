@@ -43,7 +43,8 @@ def relmax(x, ref):
     return float(np.max(np.abs(x - ref)) / np.max(np.abs(ref)))
 
 
-TILES = [0, 1, 2, 3, 4]
+TILES = [0, 1, 2, 3, 4, 5]
+TILE_WIDTH = {1: 256, 2: 128, 3: 256, 4: 128, 5: 192}
 
 
 @pytest.mark.parametrize("tile", TILES)
@@ -79,7 +80,8 @@ def test_linear_act_bf16(P, act):
 @pytest.mark.parametrize("tile", TILES)
 def test_linear_gated_bf16(P, tile):
     rng = np.random.default_rng(11 + tile)
-    M, F, K = 260, 256, 128
+    # gate and up halves split evenly over the tiles: 2F a multiple of the tile width
+    M, F, K = 260, (288 if tile == 5 else 256), 128
     A = synth.store(rng.standard_normal((M, K)), "bf16")
     W = synth.store(rng.standard_normal((2 * F, K)) / np.sqrt(K), "bf16")
     b = synth.representable(0.1 * rng.standard_normal(2 * F), "bf16")
@@ -189,12 +191,15 @@ def _tile_cases():
 @pytest.mark.parametrize("dtype,tile", _tile_cases())
 @pytest.mark.parametrize("B,N,H,dh,rope,bias", [(1, 200, 2, 128, True, False), (2, 80, 16, 72, False, True),
                                                 (2, 66, 4, 64, False, False), (1, 130, 2, 128, False, True),
-                                                (3, 77, 4, 128, True, True)])
+                                                (3, 77, 4, 128, True, True),
+                                                # rotary heads that fit 192-wide tiles
+                                                (2, 90, 6, 64, True, True), (1, 150, 4, 96, True, False)])
 def test_heads(P, dtype, tile, B, N, H, dh, rope, bias):
     if dtype == "f32" and rope:
         pytest.skip("rotary epilogue is bf16 only")
-    if rope and tile in (1, 3) and (H * dh) % 256:
-        pytest.skip("rotary pairs need whole heads in every 256-wide tile")
+    bn = TILE_WIDTH.get(tile)
+    if rope and bn and (bn % dh or (H * dh) % bn):
+        pytest.skip("rotary pairs need whole heads in every tile of this width")
     rng = np.random.default_rng(N + dh)
     d = H * dh
     M = B * N
