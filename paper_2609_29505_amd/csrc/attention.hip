@@ -30,8 +30,9 @@ __device__ __forceinline__ float pair_sum(float v) {
 // exp2(s - m) <= 256, exact in fp32 and in bf16's 8-bit exponent range.
 constexpr float kRescaleSlack = 8.0f;
 
-template <int DHP, int NW>
+template <int DH, int NW>
 __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float scale_log2) {
+    constexpr int DHP = (DH + 31) / 32 * 32;  // head dims padded to whole 32-row MFMA blocks
     constexpr int BQ = 32 * NW, BKV = 64, NT = NW * 64;
     constexpr int KS = DHP / 16, DT = DHP / 32;
     constexpr int KLDS = DHP + 8, VLDS = BKV + 8;        // padded rows: conflict-free fragment reads
@@ -43,7 +44,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int bh = blockIdx.y;
     const int b = bh / a.H, hh = bh - b * a.H;
-    const int dh = a.dh;
+    constexpr int dh = DH;
     const int q = blockIdx.x * BQ + wave * 32 + (lane & 31);
     const int half = lane >> 5;
 
@@ -73,7 +74,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
     }
 
     // register prefetch of one key/value block
-    const int kchunks = dh / 8;  // 16-byte chunks per key row
+    constexpr int kchunks = dh / 8;  // 16-byte chunks per key row
     u32x4 rk[K_CH], rv[V_CH];
     auto gload = [&](int k0) {
 #pragma unroll
@@ -155,26 +156,20 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
         }
         // scale into the log2 domain (masking keys beyond nk in the tail block only), block max
         float bm = -INFINITY;
-        if (k0 + BKV <= a.nk) {
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    s[t][r] *= scale_log2;
-                    bm = fmaxf(bm, s[t][r]);
-                }
-        } else {
+        if (k0 + BKV > a.nk) {
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int key = k0 + t * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-                    const float v = key < a.nk ? s[t][r] * scale_log2 : -INFINITY;
-                    s[t][r] = v;
-                    bm = fmaxf(bm, v);
+                    if (key >= a.nk) s[t][r] = -INFINITY;
                 }
         }
-        bm = pair_max(bm);
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) bm = fmaxf(bm, s[t][r]);
+        bm = pair_max(bm) * scale_log2;  // the scale is positive: max and scaling commute
         if (__builtin_amdgcn_ballot_w64(bm > m + kRescaleSlack)) {
             const float mn = fmaxf(m, bm);
             const float alpha = __builtin_amdgcn_exp2f(m - mn);
@@ -190,7 +185,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
         for (int t = 0; t < 2; ++t)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const float p = __builtin_amdgcn_exp2f(s[t][r] - m);
+                const float p = __builtin_amdgcn_exp2f(fmaf(s[t][r], scale_log2, -m));
                 s[t][r] = p;
                 ps += p;
             }
@@ -242,8 +237,9 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
 // so two waves share each SIMD and one half's softmax overlaps the other's MFMAs.  At the
 // end half 1 leaves (m, partial sums, O^T) in LDS and half 0 merges them:
 // O = O_0 2^(m_0 - m) + O_1 2^(m_1 - m) with m = max(m_0, m_1).
-template <int DHP, int NQG>
+template <int DH, int NQG>
 __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnArgs a, float scale_log2) {
+    constexpr int DHP = (DH + 31) / 32 * 32;
     constexpr int BQ = 32 * NQG, BKV = 64, HT = NQG * 64, NT = 2 * HT;
     constexpr int KS = DHP / 16, DT = DHP / 32;
     constexpr int KLDS = DHP + 8, VLDS = BKV + 8;        // padded rows: conflict-free fragment reads
@@ -260,7 +256,7 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
     bf16* sv = sk + BKV * KLDS;
     const int bh = blockIdx.y;
     const int b = bh / a.H, hh = bh - b * a.H;
-    const int dh = a.dh;
+    constexpr int dh = DH;
     const int q = blockIdx.x * BQ + qg * 32 + (lane & 31);
     const int half = lane >> 5;
 
@@ -284,7 +280,7 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
     }
 
     // register prefetch of one key/value block of this half
-    const int kchunks = dh / 8;  // 16-byte chunks per key row
+    constexpr int kchunks = dh / 8;  // 16-byte chunks per key row
     u32x4 rk[K_CH], rv[V_CH];
     auto gload = [&](int k0) {
 #pragma unroll
@@ -368,26 +364,20 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
             }
             // scale into the log2 domain (masking keys beyond nk in the tail block only), block max
             float bm = -INFINITY;
-            if (k0 + BKV <= a.nk) {
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        s[t][r] *= scale_log2;
-                        bm = fmaxf(bm, s[t][r]);
-                    }
-            } else {
+            if (k0 + BKV > a.nk) {
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
                         const int key = k0 + t * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-                        const float v = key < a.nk ? s[t][r] * scale_log2 : -INFINITY;
-                        s[t][r] = v;
-                        bm = fmaxf(bm, v);
+                        if (key >= a.nk) s[t][r] = -INFINITY;
                     }
             }
-            bm = pair_max(bm);
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) bm = fmaxf(bm, s[t][r]);
+            bm = pair_max(bm) * scale_log2;  // the scale is positive: max and scaling commute
             if (__builtin_amdgcn_ballot_w64(bm > m + kRescaleSlack)) {
                 const float mn = fmaxf(m, bm);
                 const float alpha = __builtin_amdgcn_exp2f(m - mn);
@@ -403,7 +393,7 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
             for (int t = 0; t < 2; ++t)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const float p = __builtin_amdgcn_exp2f(s[t][r] - m);
+                    const float p = __builtin_amdgcn_exp2f(fmaf(s[t][r], scale_log2, -m));
                     s[t][r] = p;
                     ps += p;
                 }
@@ -540,36 +530,39 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, float scale) {
     }
 }
 
+// bf16 launch for one head dim (every loader index and padding bound a compile-time constant)
+template <int DH>
+static void launch_attention_bf16(const AttnArgs& a, hipStream_t st) {
+    const int BH = a.B * a.H;
+    const float sl2 = (float)(1.4426950408889634 / sqrt((double)DH));
+    const long qg128 = (long)((a.nq + 127) / 128) * BH;  // 128-query workgroups
+    const int nkb = (a.nk + 63) / 64;
+    if (nkb >= 8 && qg128 < 1024) {
+        // long key range, few query groups: split the keys between two wave halves
+        if (qg128 >= 256)
+            hipLaunchKernelGGL((attn_split_bf16_kernel<DH, 4>), dim3((a.nq + 127) / 128, BH), dim3(512), 0, st, a, sl2);
+        else
+            hipLaunchKernelGGL((attn_split_bf16_kernel<DH, 2>), dim3((a.nq + 63) / 64, BH), dim3(256), 0, st, a, sl2);
+    } else if (qg128 < 1024) {
+        // two-wave workgroups when four-wave ones would leave CUs without a second workgroup
+        hipLaunchKernelGGL((attn_bf16_kernel<DH, 2>), dim3((a.nq + 63) / 64, BH), dim3(128), 0, st, a, sl2);
+    } else {
+        hipLaunchKernelGGL((attn_bf16_kernel<DH, 4>), dim3((a.nq + 127) / 128, BH), dim3(256), 0, st, a, sl2);
+    }
+}
+
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st) {
     const int BH = a.B * a.H;
     if (dtype == 1) {
-        const float sl2 = (float)(1.4426950408889634 / sqrt((double)a.dh));
-        const long qg128 = (long)((a.nq + 127) / 128) * BH;  // 128-query workgroups
-        const int nkb = (a.nk + 63) / 64;
-        if (nkb >= 8 && qg128 < 1024) {
-            // long key range, few query groups: split the keys between two wave halves
-            if (qg128 >= 256) {
-                dim3 grid((a.nq + 127) / 128, BH), block(512);
-                if (a.dh <= 64) hipLaunchKernelGGL((attn_split_bf16_kernel<64, 4>), grid, block, 0, st, a, sl2);
-                else if (a.dh <= 96) hipLaunchKernelGGL((attn_split_bf16_kernel<96, 4>), grid, block, 0, st, a, sl2);
-                else hipLaunchKernelGGL((attn_split_bf16_kernel<128, 4>), grid, block, 0, st, a, sl2);
-            } else {
-                dim3 grid((a.nq + 63) / 64, BH), block(256);
-                if (a.dh <= 64) hipLaunchKernelGGL((attn_split_bf16_kernel<64, 2>), grid, block, 0, st, a, sl2);
-                else if (a.dh <= 96) hipLaunchKernelGGL((attn_split_bf16_kernel<96, 2>), grid, block, 0, st, a, sl2);
-                else hipLaunchKernelGGL((attn_split_bf16_kernel<128, 2>), grid, block, 0, st, a, sl2);
-            }
-        } else if ((long)((a.nq + 127) / 128) * BH < 1024) {
-            // two-wave workgroups when four-wave ones would leave CUs without a second workgroup
-            dim3 grid((a.nq + 63) / 64, BH), block(128);
-            if (a.dh <= 64) hipLaunchKernelGGL((attn_bf16_kernel<64, 2>), grid, block, 0, st, a, sl2);
-            else if (a.dh <= 96) hipLaunchKernelGGL((attn_bf16_kernel<96, 2>), grid, block, 0, st, a, sl2);
-            else hipLaunchKernelGGL((attn_bf16_kernel<128, 2>), grid, block, 0, st, a, sl2);
-        } else {
-            dim3 grid((a.nq + 127) / 128, BH), block(256);
-            if (a.dh <= 64) hipLaunchKernelGGL((attn_bf16_kernel<64, 4>), grid, block, 0, st, a, sl2);
-            else if (a.dh <= 96) hipLaunchKernelGGL((attn_bf16_kernel<96, 4>), grid, block, 0, st, a, sl2);
-            else hipLaunchKernelGGL((attn_bf16_kernel<128, 4>), grid, block, 0, st, a, sl2);
+        switch (a.dh) {
+#define SGD_ATTN_DH(D) \
+    case D: launch_attention_bf16<D>(a, st); break;
+            SGD_ATTN_DH(8) SGD_ATTN_DH(16) SGD_ATTN_DH(24) SGD_ATTN_DH(32)
+            SGD_ATTN_DH(40) SGD_ATTN_DH(48) SGD_ATTN_DH(56) SGD_ATTN_DH(64)
+            SGD_ATTN_DH(72) SGD_ATTN_DH(80) SGD_ATTN_DH(88) SGD_ATTN_DH(96)
+            SGD_ATTN_DH(104) SGD_ATTN_DH(112) SGD_ATTN_DH(120) SGD_ATTN_DH(128)
+#undef SGD_ATTN_DH
+            default: return hipErrorInvalidValue;
         }
     } else {
         const float sc = (float)(1.0 / sqrt((double)a.dh));
