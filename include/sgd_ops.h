@@ -31,7 +31,8 @@ int sgd_op_linear(int32_t dtype, const void* A, int64_t lda, const void* W, int6
 
 /* Attention (Sec. 3 units; the softmax(q k^T / sqrt(dh)) v of every head).  q [B*H, npq, dh],
  * k [B*H, npk, dh], vt [B*H, dh, npk] (dtype), o [B, nq, H*dh].  Keys >= nk are masked;
- * npk must be a multiple of 64 and >= nk; npq >= nq. */
+ * npk must be a multiple of 64 and >= nk; npq >= nq; 8 <= dh <= 128, dh % 8 == 0.  q, k, vt
+ * 16-byte aligned, o 16-byte (fp32) or 8-byte (bf16) aligned. */
 int sgd_op_attention(int32_t dtype, const void* q, const void* k, const void* vt, void* o, int32_t B, int32_t H,
                      int32_t dh, int32_t nq, int32_t npq, int32_t nk, int32_t npk, void* hip_stream);
 
@@ -65,6 +66,14 @@ int sgd_op_residual(int32_t dtype, const void* A, int64_t lda, const void* W, co
 /* h <- h + delta[0] + ... + delta[r-1] elementwise over n fp32 values (n % 4 == 0), in
  * that order (the frozen-unit update of Sec. 3.1 for a run of r frozen units). */
 int sgd_op_frozen_run(float* h, const float* const* deltas, int32_t r, int64_t n, void* hip_stream);
+
+/* DiT AdaLN modulation (Sec. 4.2: conditioning keeps propagating; the per-block shift,
+ * scale and gate vectors): mod[b, j] = sum_k x[b, k] W[j, k] + bias[j] for B rows of
+ * x = SiLU(c) (fp32 [B x d]), W[n_out x d] of dtype (F32 or BF16), bias fp32 [n_out] or NULL,
+ * mod fp32 [B x n_out].  d % 64 == 0; x, W 16-byte aligned.  fp32 accumulation of the exact
+ * fp32 products x[b, k] W[j, k]. */
+int sgd_op_adaln_mod(int32_t dtype, const float* x, const void* W, const float* bias, float* mod, int32_t B,
+                     int32_t d, int32_t n_out, void* hip_stream);
 
 #ifdef __cplusplus
 }

@@ -116,6 +116,7 @@ def lib() -> C.CDLL:
             "sgd_op_frozen_run": [vp, C.POINTER(vp), i32, i64, vp],
             "sgd_op_heads": [i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, vp],
             "sgd_op_residual": [i32, vp, i64, vp, vp, vp, vp, i32, vp, i64, i32, i32, i32, i32, i32, vp],
+            "sgd_op_adaln_mod": [i32, vp, vp, vp, vp, i32, i32, i32, vp],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -286,6 +287,12 @@ def op_residual(A, W, h, bias=None, delta=None, delta_mode=0, gate=None, ntok=1,
     gate_ld = gate.stride(0) if gate is not None else 0
     _check(lib().sgd_op_residual(_dtype_code(A), _p(A), A.stride(0), _p(W), _p(bias), _p(h), _p(delta), delta_mode,
                                  _p(gate), gate_ld, ntok, M, N, K, tile, C.c_void_p(_stream_ptr(stream))))
+
+
+def op_adaln_mod(x, W, mod, bias=None, stream=None) -> None:
+    B, d = x.shape
+    _check(lib().sgd_op_adaln_mod(_dtype_code(W), _p(x), _p(W), _p(bias), _p(mod), B, d, W.shape[0],
+                                  C.c_void_p(_stream_ptr(stream))))
 
 
 def op_frozen_run(h, deltas, stream=None) -> None:

@@ -550,6 +550,8 @@ extern "C" int sgd_op_attention(int32_t dtype, const void* q, const void* k, con
     if (dtype != SGD_F32 && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
     if (B < 1 || H < 1 || nq < 1 || nk < 1 || npq < nq || npk < nk || npk % 64 || dh < 8 || dh > 128 || dh % 8)
         return fail(SGD_E_SHAPE, "attention shape not supported");
+    if ((uintptr_t)q % 16 || (uintptr_t)k % 16 || (uintptr_t)vt % 16 || (uintptr_t)o % (dtype == SGD_F32 ? 16 : 8))
+        return fail(SGD_E_ARG, "attention operands must be 16-byte aligned (bf16 output: 8)");
     AttnArgs a{q, k, vt, o, B, H, dh, nq, npq, nk, npk};
     SGD_HIP_TRY(launch_attention(dtype == SGD_BF16 ? 1 : 0, a, (hipStream_t)hip_stream));
     return SGD_OK;
@@ -581,5 +583,15 @@ extern "C" int sgd_op_frozen_run(float* h, const float* const* deltas, int32_t r
         f.snap[i] = nullptr;
     }
     SGD_HIP_TRY(launch_frozen_run(f, (hipStream_t)hip_stream));
+    return SGD_OK;
+}
+
+extern "C" int sgd_op_adaln_mod(int32_t dtype, const float* x, const void* W, const float* bias, float* mod,
+                                int32_t B, int32_t d, int32_t n_out, void* hip_stream) {
+    if (!x || !W || !mod) return fail(SGD_E_ARG, "NULL argument");
+    if (dtype != SGD_F32 && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
+    if (B < 1 || n_out < 1 || d < 64 || d % 64) return fail(SGD_E_SHAPE, "modulation shape not supported");
+    if ((uintptr_t)x % 16 || (uintptr_t)W % 16) return fail(SGD_E_ARG, "x and W must be 16-byte aligned");
+    SGD_HIP_TRY(launch_adaln_mod(dtype == SGD_BF16 ? 1 : 0, x, W, bias, mod, B, d, n_out, (hipStream_t)hip_stream));
     return SGD_OK;
 }

@@ -9,7 +9,9 @@
 // both operands), and V^T is read from the head-major transposed value layout written by
 // the QKV GEMM epilogue.  Keys beyond nk are masked; head dims are zero-padded to a
 // multiple of 32.
-// fp32 path: one thread per query, scores for a 64-key block, online softmax.
+// fp32 path (MFMA 32x32x2 fp32): the same transposed formulation with one fp32 k-slot pair
+// per MFMA; a workgroup's waves share 32 queries and take alternate 32-key blocks, and their
+// partial softmax states are merged through LDS in wave order.
 #include "common.h"
 #include "kernels.h"
 
@@ -466,68 +468,139 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
     }
 }
 
-template <int DHP>
-__global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a, float scale) {
-    constexpr int BKV = 64;
-    __shared__ float sk[BKV][DHP + 1];
-    __shared__ float sv[DHP][BKV + 1];
-    const int tid = threadIdx.x;
-    const int bh = blockIdx.y;
-    const int b = bh / a.H, hh = bh - b * a.H;
+// fp32 attention.  Wave w of a workgroup takes key blocks w, w + NW, ... of its 32 queries.
+// Scores: S^T (32 keys x 32 queries) = K Q^T over head dims, MFMA step t contracting dims t
+// (lanes 0-31) and HD + t (lanes 32-63), so each lane reads one contiguous half row of K and
+// of Q.  In the accumulator lane l holds query l % 32 and keys (r / 4) * 8 + (l / 32) * 4 +
+// r % 4 (register r).  Output: O^T += V^T P^T, MFMA r contracting keys (r / 4) * 8 + r % 4
+// (lanes 0-31) and the same + 4 (lanes 32-63): the B operand is the lane's own score register
+// r, the A operand four consecutive keys of a V^T row, one float4 per (32-dim block, r / 4).
+template <int DHP, int NW>
+__global__ __launch_bounds__(NW * 64) void attn_f32_kernel(AttnArgs a, float scale_log2) {
+    constexpr int HD = DHP / 2, DB = DHP / 32, MS = DB * 16 + 2;  // merge record per lane
+    __shared__ float mg[(NW > 1 ? NW - 1 : 1) * MS * 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = lane & 31, half = lane >> 5;
+    const int bh = blockIdx.y, b = bh / a.H, hh = bh - b * a.H;
     const int dh = a.dh;
-    const int q = blockIdx.x * 64 + tid;
+    const int q0 = blockIdx.x * 32;
     const float* Q = (const float*)a.q + (long)bh * a.npq * dh;
     const float* K = (const float*)a.k + (long)bh * a.npk * dh;
     const float* VT = (const float*)a.vt + (long)bh * dh * a.npk;
-    float qv[DHP], ov[DHP];
-    const int qrow = min(q, a.npq - 1);
+    // dims half * HD + t of the lane's query row (rows past nq read the last query; dims past
+    // dh are zero: dh % 8 == 0, so a float4 group is wholly inside or outside)
+    float qv[HD];
+    {
+        const float* qr = Q + (long)min(q0 + col, a.nq - 1) * dh + half * HD;
 #pragma unroll
-    for (int j = 0; j < DHP; ++j) {
-        qv[j] = j < dh ? Q[(long)qrow * dh + j] : 0.f;
-        ov[j] = 0.f;
+        for (int t = 0; t < HD; t += 4) {
+            const f32x4 v = half * HD + t < dh ? *(const f32x4*)(qr + t) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) qv[t + e] = v[e];
+        }
     }
+    f32x16 o[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
     float m = -INFINITY, l = 0.f;
-    for (int k0 = 0; k0 < a.nk; k0 += BKV) {
-        __syncthreads();
-        for (int i = tid; i < BKV * DHP; i += 64) {
-            int r = i / DHP, c = i % DHP;
-            sk[r][c] = c < dh ? K[(long)(k0 + r) * dh + c] : 0.f;
+    const int nkb = (a.nk + 31) / 32;
+    for (int kb = wave; kb < nkb; kb += NW) {
+        const int k0 = kb * 32;
+        f32x16 sc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sc[r] = 0.f;
+        {
+            // key rows k0 + col < npk (npk is a multiple of 64 and >= nk); rows past nk are masked
+            const float* kr = K + (long)(k0 + col) * dh + half * HD;
+#pragma unroll
+            for (int t = 0; t < HD; t += 4) {
+                const f32x4 v = half * HD + t < dh ? *(const f32x4*)(kr + t) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) sc = __builtin_amdgcn_mfma_f32_32x32x2f32(v[e], qv[t + e], sc, 0, 0, 0);
+            }
         }
-        for (int i = tid; i < DHP * BKV; i += 64) {
-            int r = i / BKV, c = i % BKV;
-            sv[r][c] = (r < dh && k0 + c < a.nk) ? VT[(long)r * a.npk + k0 + c] : 0.f;
+        f32x4 vv[DB][4];
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            const int dim = db * 32 + col;
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                vv[db][g] = dim < dh ? *(const f32x4*)(VT + (long)dim * a.npk + k0 + g * 8 + half * 4)
+                                     : f32x4{0.f, 0.f, 0.f, 0.f};
         }
-        __syncthreads();
-        float s[BKV];
         float bm = -INFINITY;
 #pragma unroll
-        for (int j = 0; j < BKV; ++j) {
-            float acc = 0.f;
-#pragma unroll
-            for (int c = 0; c < DHP; ++c) acc = fmaf(qv[c], sk[j][c], acc);
-            acc *= scale;
-            s[j] = (k0 + j < a.nk) ? acc : -INFINITY;
-            bm = fmaxf(bm, s[j]);
+        for (int r = 0; r < 16; ++r) {
+            const int key = k0 + (r >> 2) * 8 + half * 4 + (r & 3);
+            sc[r] = key < a.nk ? sc[r] * scale_log2 : -INFINITY;
+            bm = fmaxf(bm, sc[r]);
         }
+        bm = fmaxf(bm, __shfl_xor(bm, 32, 64));  // key 0 of the block is valid: bm is finite
         const float mn = fmaxf(m, bm);
-        const float alpha = expf(m - mn);
+        const float alpha = __builtin_amdgcn_exp2f(m - mn);
         m = mn;
         l *= alpha;
 #pragma unroll
-        for (int c = 0; c < DHP; ++c) ov[c] *= alpha;
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-        for (int j = 0; j < BKV; ++j) {
-            const float p = expf(s[j] - mn);
-            l += p;
+            for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
 #pragma unroll
-            for (int c = 0; c < DHP; ++c) ov[c] = fmaf(p, sv[c][j], ov[c]);
+        for (int r = 0; r < 16; ++r) {
+            sc[r] = __builtin_amdgcn_exp2f(sc[r] - mn);
+            l += sc[r];
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int key = k0 + (r >> 2) * 8 + half * 4 + (r & 3);
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                // masked keys have p = 0, but their V^T entries may be any value (NaN included)
+                const float v = key < a.nk ? vv[db][r >> 2][r & 3] : 0.f;
+                o[db] = __builtin_amdgcn_mfma_f32_32x32x2f32(v, sc[r], o[db], 0, 0, 0);
+            }
         }
     }
-    if (q < a.nq) {
-        float* O = (float*)a.o + ((long)b * a.nq + q) * ((long)a.H * dh) + (long)hh * dh;
-        const float inv = 1.0f / l;
-        for (int c = 0; c < dh; ++c) O[c] = ov[c] * inv;
+    if (NW > 1) {
+        // waves 1 .. NW-1 hand (O^T, m, l) to wave 0, which merges them in wave order
+        if (wave > 0) {
+            float* rec = mg + (wave - 1) * MS * 64 + lane;
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) rec[(db * 16 + r) * 64] = o[db][r];
+            rec[DB * 16 * 64] = m;
+            rec[(DB * 16 + 1) * 64] = l;
+        }
+        __syncthreads();
+        if (wave > 0) return;
+        for (int w = 1; w < NW; ++w) {
+            const float* rec = mg + (w - 1) * MS * 64 + lane;
+            const float mw = rec[DB * 16 * 64], lw = rec[(DB * 16 + 1) * 64];
+            const float mn = fmaxf(m, mw);  // wave 0 holds key block 0: m and mn are finite
+            const float a0 = __builtin_amdgcn_exp2f(m - mn), a1 = __builtin_amdgcn_exp2f(mw - mn);
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) o[db][r] = o[db][r] * a0 + rec[(db * 16 + r) * 64] * a1;
+            l = l * a0 + lw * a1;
+            m = mn;
+        }
     }
+    const int q = q0 + col;
+    if (q >= a.nq) return;
+    const float inv = 1.0f / (l + __shfl_xor(l, 32, 64));
+    float* O = (float*)a.o + ((long)b * a.nq + q) * ((long)a.H * dh) + (long)hh * dh;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int d0 = db * 32 + g * 8 + half * 4;
+            if (d0 < dh)
+                *(f32x4*)(O + d0) = f32x4{o[db][g * 4] * inv, o[db][g * 4 + 1] * inv, o[db][g * 4 + 2] * inv,
+                                          o[db][g * 4 + 3] * inv};
+        }
 }
 
 // bf16 launch for one head dim (every loader index and padding bound a compile-time constant)
@@ -565,11 +638,12 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st) {
             default: return hipErrorInvalidValue;
         }
     } else {
-        const float sc = (float)(1.0 / sqrt((double)a.dh));
-        dim3 grid((a.nq + 63) / 64, BH), block(64);
-        if (a.dh <= 64) hipLaunchKernelGGL(attn_f32_kernel<64>, grid, block, 0, st, a, sc);
-        else if (a.dh <= 96) hipLaunchKernelGGL(attn_f32_kernel<96>, grid, block, 0, st, a, sc);
-        else hipLaunchKernelGGL(attn_f32_kernel<128>, grid, block, 0, st, a, sc);
+        const float sl2 = (float)(1.4426950408889634 / sqrt((double)a.dh));
+        dim3 grid((a.nq + 31) / 32, BH), block(4 * 64);
+        if (a.dh <= 32) hipLaunchKernelGGL((attn_f32_kernel<32, 4>), grid, block, 0, st, a, sl2);
+        else if (a.dh <= 64) hipLaunchKernelGGL((attn_f32_kernel<64, 4>), grid, block, 0, st, a, sl2);
+        else if (a.dh <= 96) hipLaunchKernelGGL((attn_f32_kernel<96, 4>), grid, block, 0, st, a, sl2);
+        else hipLaunchKernelGGL((attn_f32_kernel<128, 4>), grid, block, 0, st, a, sl2);
     }
     return hipGetLastError();
 }

@@ -252,15 +252,83 @@ __global__ __launch_bounds__(256) void adaln_mod_kernel(const float* x, const WT
     }
 }
 
+// bf16 weights: the same product on the matrix cores.  SiLU(c) is fp32; it is split into
+// three bf16 parts, x = hi + mid + lo (each part the round-to-nearest-even bf16 of what the
+// previous parts leave: x - hi has at most 16 significant bits and x - hi - mid at most 8, so
+// hi + mid + lo == x exactly), and bf16 x bf16 products are exact in fp32: the MFMAs sum the
+// fp32 products of the FMA kernel above, in another order.  A workgroup owns 32 features x 32 samples
+// (v_mfma_f32_32x32x16_bf16: A = the x parts, one sample per lane row; B = the weight rows,
+// one feature per lane column); its sixteen waves take consecutive 16-deep k steps, every
+// lane loads its operands straight from global memory (16 bytes of weights, 32 bytes of x
+// per step, all steps of a wave issued together), and the partial tiles are summed in LDS
+// in wave order (deterministic).
+constexpr int kModWaves = 16, kModChunk = 5;
+__global__ __launch_bounds__(kModWaves * 64) void adaln_mod_mfma_kernel(const float* x, const bf16* W,
+                                                                        const float* bias, float* mod, int B,
+                                                                        int d, int n_out) {
+    __shared__ float red[kModWaves][32 * 32];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int j0 = blockIdx.x * 32, b0 = blockIdx.y * 32;
+    const int col = lane & 31, kh = (lane >> 5) * 8;
+    const int steps = d / 16;
+    const int s0 = wave * steps / kModWaves, s1 = (wave + 1) * steps / kModWaves;
+    const bool jin = j0 + col < n_out, bin = b0 + col < B;
+    const bf16* wrow = W + (long)(jin ? j0 + col : 0) * d + kh;
+    const float* xrow = x + (long)(bin ? b0 + col : 0) * d + kh;
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    for (int s = s0; s < s1; s += kModChunk) {
+        u32x4 wv[kModChunk];
+        f32x4 xa[kModChunk], xb[kModChunk];
+#pragma unroll
+        for (int c = 0; c < kModChunk; ++c) {
+            const bool ok = s + c < s1;
+            const int k = (s + c) * 16;
+            wv[c] = ok && jin ? *(const u32x4*)(wrow + k) : u32x4{0u, 0u, 0u, 0u};
+            xa[c] = ok && bin ? *(const f32x4*)(xrow + k) : f32x4{0.f, 0.f, 0.f, 0.f};
+            xb[c] = ok && bin ? *(const f32x4*)(xrow + k + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int c = 0; c < kModChunk; ++c) {
+            bf16x8 hi, mid, lo;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float v = e < 4 ? xa[c][e] : xb[c][e - 4];
+                hi[e] = f2bf(v);
+                const float r1 = v - bf2f(hi[e]);
+                mid[e] = f2bf(r1);
+                lo[e] = f2bf(r1 - bf2f(mid[e]));
+            }
+            const bf16x8 wf = __builtin_bit_cast(bf16x8, wv[c]);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lo, wf, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(mid, wf, acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(hi, wf, acc, 0, 0, 0);
+        }
+    }
+    // lane l holds feature column l % 32 and, for register r, sample row
+    // (r / 4) * 8 + (l / 32) * 4 + r % 4 of the tile
+#pragma unroll
+    for (int r = 0; r < 16; ++r) red[wave][((r >> 2) * 8 + (lane >> 5) * 4 + (r & 3)) * 32 + col] = acc[r];
+    __syncthreads();
+    const int i = tid >> 5, j = tid & 31;  // one output per thread: sample i, feature j
+    float v = red[0][tid];
+#pragma unroll
+    for (int w = 1; w < kModWaves; ++w) v += red[w][tid];
+    if (b0 + i < B && j0 + j < n_out) mod[(long)(b0 + i) * n_out + j0 + j] = v + (bias ? bias[j0 + j] : 0.f);
+}
+
 hipError_t launch_adaln_mod(int dtype, const float* x, const void* W, const float* bias, float* mod, int B,
                             int d, int n_out, hipStream_t st) {
     if (d % 64) return hipErrorInvalidValue;  // whole 64-deep k chunks (the model requires d % 128 == 0)
-    dim3 grid((n_out + 63) / 64, (B + 31) / 32), block(256);
-    if (dtype == 1)
-        hipLaunchKernelGGL(adaln_mod_kernel<bf16>, grid, block, 0, st, x, (const bf16*)W, bias, mod, B, d, n_out);
-    else
+    if (dtype == 1) {
+        dim3 grid((n_out + 31) / 32, (B + 31) / 32), block(kModWaves * 64);
+        hipLaunchKernelGGL(adaln_mod_mfma_kernel, grid, block, 0, st, x, (const bf16*)W, bias, mod, B, d, n_out);
+    } else {
+        dim3 grid((n_out + 63) / 64, (B + 31) / 32), block(256);
         hipLaunchKernelGGL(adaln_mod_kernel<float>, grid, block, 0, st, x, (const float*)W, bias, mod, B, d,
                            n_out);
+    }
     return hipGetLastError();
 }
 

@@ -1,9 +1,9 @@
 // Branch GEMMs of the active units in fp32: C = A . B^T with fused epilogues, and the
 // dtype dispatch (the bf16 path is in gemm_bf16.hip).
 //
-// fp32 path: LDS-tiled FMA kernel (the fp32 workload is small and latency-bound).  Each
-// thread holds columns c and c + 32 of its rows, so paired epilogues (gated MLPs: gate and
-// up projections of one output column) read both halves from registers.
+// fp32 path: matrix-core kernel (v_mfma_f32_32x32x2_f32) with small tiles and K split across
+// the waves of a workgroup (the fp32 workload is small and latency-bound); paired epilogues
+// (gated MLPs: gate and up projections of one output column) read both halves from LDS.
 #include "common.h"
 #include "kernels.h"
 
@@ -111,78 +111,84 @@ __device__ __forceinline__ bool kind_paired(const EpiParams& p) {
     return p.kind == EP_GATED || (p.kind == EP_HEADS && p.rope);
 }
 
-// ---------------------------------------------------------------------------- fp32 FMA
+// ---------------------------------------------------------------------------- fp32 MFMA
 
-// 64 x 64 tile, BK = 16, 256 threads, 4 x 4 outputs per thread.  Thread (ty, tx) owns rows
-// ty + 16 i and columns tx + 16 j (j = 0..3): columns tx and tx + 32 form pairs.
-__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, EpiParams ep) {
-    constexpr int BM = 64, BN = 64, BK = 16;
-    __shared__ float sa[BK][BM + 4];
-    __shared__ float sb[BK][BN + 4];
-    const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
-    const int nt_m = (g.M + BM - 1) / BM;
+// 32 x 32 output tile per workgroup on v_mfma_f32_32x32x2_f32 (fp32 products, fp32
+// accumulation).  The four waves split K: k unit u (8 values) goes to wave u % 4, and in a unit
+// lanes 0-31 contract k = 8u .. 8u+3 and lanes 32-63 k = 8u+4 .. 8u+7 (four MFMA steps), so each
+// lane reads one float4 of its A row and one of its B row per unit, straight from global
+// memory.  The partial tiles meet in LDS and are summed in wave order (deterministic); every
+// thread then applies the epilogue to its elements.  Gated tiles hold 16 gate and the matching
+// 16 up columns (pairs c, c + 16).
+constexpr int kF32Waves = 4, kF32Chunk = 4;  // k units per wave per pass (loads issued together)
+__global__ __launch_bounds__(kF32Waves * 64) void gemm_f32_kernel(GemmArgs g, EpiParams ep) {
+    __shared__ float red[kF32Waves][32 * 33];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int col = lane & 31, half = lane >> 5;
+    const int nt_m = (g.M + 31) / 32;
+    const int tm = blockIdx.x % nt_m, tn = blockIdx.x / nt_m;
+    const int m0 = tm * 32;
     const bool gated = ep.kind == EP_GATED;
-    const int t = blockIdx.x;
-    const int tm = t % nt_m, tn = t / nt_m;
-    const int m0 = tm * BM;
     const int F = g.N / 2;
-    float acc[4][4] = {};
-    // loader: 64 rows x 16 k = 1024 elements, 4 per thread (one float4 along k)
-    const int lr = tid >> 2, lk = (tid & 3) * 4;
-    const int ar = min(m0 + lr, g.M - 1);
-    long br;
-    if (gated) br = lr < 32 ? (long)tn * 32 + lr : (long)F + tn * 32 + (lr - 32);
-    else br = (long)tn * BN + lr;
-    for (int k0 = 0; k0 < g.K; k0 += BK) {
-        const bool second = g.A1 && k0 >= g.K0;
-        const float* ap = second ? (const float*)g.A1 + (long)ar * g.lda1 + (k0 - g.K0) + lk
-                                 : (const float*)g.A0 + (long)ar * g.lda0 + k0 + lk;
-        float4 av = *(const float4*)ap;
-        float4 bv = *(const float4*)((const float*)g.B + br * g.ldb + k0 + lk);
-        sa[lk + 0][lr] = av.x; sa[lk + 1][lr] = av.y; sa[lk + 2][lr] = av.z; sa[lk + 3][lr] = av.w;
-        sb[lk + 0][lr] = bv.x; sb[lk + 1][lr] = bv.y; sb[lk + 2][lr] = bv.z; sb[lk + 3][lr] = bv.w;
-        __syncthreads();
+    // operand rows of this lane: A row m0 + col (clamped; rows past M are never stored), B row
+    // of product column col of the tile
+    const int ar = min(m0 + col, g.M - 1);
+    const long br = gated ? (col < 16 ? (long)tn * 16 + col : (long)F + tn * 16 + (col - 16)) : (long)tn * 32 + col;
+    const float* bp = (const float*)g.B + br * g.ldb + half * 4;
+    f32x16 acc;
 #pragma unroll
-        for (int kk = 0; kk < BK; ++kk) {
-            float a[4], b[4];
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    const int units = g.K / 8;
+    for (int u0 = wave; u0 < units; u0 += kF32Waves * kF32Chunk) {
+        f32x4 av[kF32Chunk], bv[kF32Chunk];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) a[i] = sa[kk][ty + 16 * i];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) b[j] = sb[kk][tx + 16 * j];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+        for (int c = 0; c < kF32Chunk; ++c) {
+            const int u = u0 + c * kF32Waves;
+            const int k = u * 8 + half * 4;
+            if (u < units) {
+                const bool second = g.A1 && k >= g.K0;
+                const float* ap = second ? (const float*)g.A1 + (long)ar * g.lda1 + (k - g.K0)
+                                         : (const float*)g.A0 + (long)ar * g.lda0 + k;
+                av[c] = *(const f32x4*)ap;
+                bv[c] = *(const f32x4*)(bp + u * 8);
+            } else {
+                av[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+                bv[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
         }
-        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < kF32Chunk; ++c)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[c][e], bv[c][e], acc, 0, 0, 0);
     }
+    // lane l holds tile column l % 32 and, for register r, row (r / 4) * 8 + (l / 32) * 4 + r % 4
+#pragma unroll
+    for (int r = 0; r < 16; ++r) red[wave][((r >> 2) * 8 + half * 4 + (r & 3)) * 33 + col] = acc[r];
+    __syncthreads();
+    auto tile_at = [&](int row, int c) {
+        float v = red[0][row * 33 + c];
+#pragma unroll
+        for (int w = 1; w < kF32Waves; ++w) v += red[w][row * 33 + c];
+        return v;
+    };
     Epi<float> e{ep};
-    const bool paired = kind_paired(ep);
-    if (ep.kind == EP_HEADS) e.tw = ep.which0 + (tn * BN) / ep.d;
-    if (ep.kind == EP_HEADS && e.tw == 2 && !paired) {
+    if (ep.kind == EP_HEADS) e.tw = ep.which0 + (tn * 32) / ep.d;
+    if (gated) {
+        // 32 rows x 16 (gate, up) pairs, two per thread
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int row = m0 + ty + 16 * i;
-            if (row >= g.M) continue;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) e.single_vt(row, tn * BN + tx + 16 * j, acc[i][j]);
+        for (int i = 0; i < 2; ++i) {
+            const int pidx = tid + i * kF32Waves * 64, row = pidx >> 4, c = pidx & 15;
+            if (m0 + row < g.M) e.pair(m0 + row, tn * 32 + c, 16, tn * 16 + c, tile_at(row, c), tile_at(row, c + 16));
         }
         return;
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int row = m0 + ty + 16 * i;
-        if (row >= g.M) continue;
-        if (paired) {
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int lc = tx + 16 * j;
-                e.pair(row, tn * BN + lc, 32, tn * 32 + lc, acc[i][j], acc[i][j + 2]);
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) e.single(row, tn * BN + tx + 16 * j, acc[i][j]);
-        }
+        const int idx = tid + i * kF32Waves * 64, row = idx >> 5, c = idx & 31;
+        if (m0 + row >= g.M) continue;
+        const float v = tile_at(row, c);
+        if (ep.kind == EP_HEADS && e.tw == 2) e.single_vt(m0 + row, tn * 32 + c, v);
+        else e.single(m0 + row, tn * 32 + c, v);
     }
 }
 
@@ -199,8 +205,8 @@ bool gemm_shape_ok(int dtype, const GemmArgs& g, const EpiParams& e, int tile) {
 
 hipError_t launch_gemm(int dtype, const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile) {
     if (dtype == 1) return launch_gemm_bf16(g, e, st, tile);
-    const int nt_m = (g.M + 63) / 64, nt_n = g.N / 64;
-    hipLaunchKernelGGL(gemm_f32_kernel, dim3(nt_m * nt_n), dim3(256), 0, st, g, e);
+    const int nt_m = (g.M + 31) / 32, nt_n = g.N / 32;
+    hipLaunchKernelGGL(gemm_f32_kernel, dim3(nt_m * nt_n), dim3(kF32Waves * 64), 0, st, g, e);
     return hipGetLastError();
 }
 

@@ -167,6 +167,21 @@ def test_norm(P, dtype, kind, d, M):
         assert relmax(got, ref) <= 1e-5
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("B,d,n_out", [(32, 1152, 6912), (2, 1152, 6912), (5, 256, 200), (40, 128, 96), (3, 64, 32)])
+def test_adaln_mod(P, dtype, B, d, n_out):
+    """DiT modulation vectors SiLU(c) W_ada^T + b: fp32 accumulation of the exact products
+    (bf16 weights run on the matrix cores with x split into three bf16 parts)."""
+    rng = np.random.default_rng(B * 7 + d + n_out)
+    x = om.silu(rng.standard_normal((B, d))).astype(np.float32)
+    W = synth.store(rng.standard_normal((n_out, d)) / np.sqrt(d), dtype)
+    b = synth.representable(0.02 * rng.standard_normal(n_out), "f32")
+    mod = empty((B, n_out), "f32")
+    P.op_adaln_mod(dev(x), dev(W), mod, bias=dev(b))
+    ref = x.astype(np.float64) @ decode(W, dtype).T + b
+    assert relmax(host(mod), ref) < 2e-6
+
+
 def test_frozen_run_bitwise(P):
     rng = np.random.default_rng(0)
     n = 4096 * 33
