@@ -46,12 +46,14 @@ __device__ __forceinline__ float erf_as(float x) {
     const float y = 1.0f - poly * __expf(-ax * ax);
     return copysignf(y, x);
 }
-// tanh(x) = 1 - 2 / (exp(2x) + 1): exact limits +-1 when exp overflows or underflows
-__device__ __forceinline__ float tanh_exp(float x) { return 1.0f - 2.0f * fast_rcp(__expf(2.0f * x) + 1.0f); }
 __device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erf_as(x * 0.70710678118654752f)); }
+// 0.5 x (1 + tanh(u)) = x / (1 + exp(-2u)), u = sqrt(2/pi) (x + 0.044715 x^3); the exponent
+// -2u log2(e) = x (c0 + c1 x^2) goes straight to v_exp_f32 (exp2): five VALU operations plus
+// the exponential and the reciprocal.  Limits: exp2 -> inf gives x * 0, exp2 -> 0 gives x.
 __device__ __forceinline__ float gelu_tanh(float x) {
-    const float k0 = 0.79788456080286536f;  // sqrt(2/pi)
-    return 0.5f * x * (1.0f + tanh_exp(k0 * (x + 0.044715f * x * x * x)));
+    const float c0 = -2.302208198144325f;    // -2 sqrt(2/pi) log2(e)
+    const float c1 = -0.1029432395800235f;   // -2 sqrt(2/pi) 0.044715 log2(e)
+    return x * fast_rcp(1.0f + __builtin_amdgcn_exp2f(x * fmaf(c1, x * x, c0)));
 }
 __device__ __forceinline__ float silu(float x) { return x * fast_rcp(1.0f + __expf(-x)); }
 

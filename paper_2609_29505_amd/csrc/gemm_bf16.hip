@@ -379,13 +379,13 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bool gated = ep.kind == EP_GATED;
-    const int nt_m = (g.M + C::BM - 1) / C::BM;
+    const int nt_m = (g.M - g.m_begin + C::BM - 1) / C::BM;
     const int nt_n = (g.N + C::BN - 1) / C::BN;
     const int total = nt_m * nt_n;
     const int bid = blockIdx.x;
     const int t = total % 8 == 0 ? (bid % 8) * (total / 8) + bid / 8 : bid;
     const int tm = t % nt_m, tn = t / nt_m;
-    const int m0 = tm * C::BM;
+    const int m0 = g.m_begin + tm * C::BM;
     const int F = g.N / 2;
 
     const __amdgpu_buffer_rsrc_t ra0 = buf_rsrc(g.A0, (unsigned)((long)g.M * g.lda0 * 2));
@@ -569,27 +569,57 @@ Shape tile_shape(int tile) {
 }
 }  // namespace
 
-// Automatic choice: one workgroup per CU, so a launch of n tiles takes ceil(n / 256) rounds;
-// pick the tile with the least rounds x tile area / per-CU rate (e.g. at 1024 rows the
-// 4096-column GEMMs run 128 x 128 tiles, one full round, rather than 64 large tiles).
-int gemm_bf16_auto_tile(const GemmArgs& g, const EpiParams& e) {
-    int best = 1;
+// Cost of one launch of `tile` over `rows` rows in units of a 256 x 256 tile at full rate: one
+// workgroup per CU, so n tiles take ceil(n / 256) rounds of tile area / per-CU rate.
+// Infinite when the epilogue cannot use the tile.
+static double tile_cost(int tile, long rows, const GemmArgs& g, const EpiParams& e) {
+    const Shape s = tile_shape(tile);
+    if (!s.bm) return 1e300;
+    if (e.kind == EP_GATED && g.N % s.bn) return 1e300;
+    if (e.kind == EP_HEADS && e.rope && (s.bn % e.dh || e.d % s.bn)) return 1e300;
+    const long tiles = ((rows + s.bm - 1) / s.bm) * ((g.N + s.bn - 1) / s.bn);
+    return (double)((tiles + 255) / 256) * s.bm * s.bn / s.rate / (256.0 * 256.0);
+}
+
+// Automatic choice: the tile with the least cost (e.g. at 1024 rows the 4096-column GEMMs run
+// 128 x 128 tiles, one full round, rather than 64 large tiles).  When the rows leave a short
+// tail past the last whole 256-row tile (U-ViT: 32 x 258 = 8256 = 32 x 256 + 64 rows), the
+// tail can go to a second launch of 128-row tiles, so the main launch fills whole rounds
+// instead of starting a third round for 64 rows; the split is taken when it is cheaper with
+// the second launch charged a tenth of a round for its start-up.
+GemmPlan gemm_bf16_plan(const GemmArgs& g, const EpiParams& e) {
+    GemmPlan best{1, g.M, 0};
     double best_t = 1e300;
     for (int tile = 1; tile <= kGemmTiles; ++tile) {
-        const Shape s = tile_shape(tile);
-        if (e.kind == EP_GATED && g.N % s.bn) continue;
-        if (e.kind == EP_HEADS && e.rope && (s.bn % e.dh || e.d % s.bn)) continue;
-        const long tiles = (long)((g.M + s.bm - 1) / s.bm) * ((g.N + s.bn - 1) / s.bn);
-        const double t = (double)((tiles + 255) / 256) * s.bm * s.bn / s.rate;
-        if (t < best_t * 0.999) { best_t = t; best = tile; }
+        const double t = tile_cost(tile, g.M, g, e);
+        if (t < best_t * 0.999) { best_t = t; best = GemmPlan{tile, g.M, 0}; }
+    }
+    const int tail = g.M % 256;
+    if (g.M > 2048 && tail > 0 && tail <= 128) {
+        for (int tile = 1; tile <= kGemmTiles; ++tile) {
+            if (tile_shape(tile).bm != 256) continue;
+            const double tm = tile_cost(tile, g.M - tail, g, e);
+            for (int tt = 1; tt <= kGemmTiles; ++tt) {
+                if (tile_shape(tt).bm != 128) continue;
+                const double t = tm + tile_cost(tt, tail, g, e) + 0.1;
+                if (t < best_t * 0.97) { best_t = t; best = GemmPlan{tile, g.M - tail, tt}; }
+            }
+        }
     }
     return best;
 }
 
+int gemm_bf16_auto_tile(const GemmArgs& g, const EpiParams& e) { return gemm_bf16_plan(g, e).tile; }
+
 static bool aligned(const void* p, unsigned a) { return ((uintptr_t)p % a) == 0; }
 
 bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
-    if (tile == 0) tile = gemm_bf16_auto_tile(g, e);
+    if (tile == 0) {
+        const GemmPlan p = gemm_bf16_plan(g, e);
+        if (p.tail_tile && !gemm_bf16_shape_ok(g, e, p.tail_tile)) return false;
+        tile = p.tile;
+    }
+    if (g.m_begin != 0) return false;  // set by the dispatcher only
     // vector accesses of the loader and the epilogue: 16-byte operand rows and fp32 vectors,
     // 8-byte bf16 output groups
     if (!aligned(g.A0, 16) || !aligned(g.A1, 16) || !aligned(g.B, 16) || !aligned(e.bias, 16) ||
@@ -616,13 +646,12 @@ bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
 
 template <class C>
 static hipError_t run_tile(const GemmArgs& g, const EpiParams& e, hipStream_t st) {
-    const int nt_m = (g.M + C::BM - 1) / C::BM, nt_n = (g.N + C::BN - 1) / C::BN;
+    const int nt_m = (g.M - g.m_begin + C::BM - 1) / C::BM, nt_n = (g.N + C::BN - 1) / C::BN;
     hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3(nt_m * nt_n), dim3(C::NT), 0, st, g, e);
     return hipGetLastError();
 }
 
-hipError_t launch_gemm_bf16(const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile) {
-    if (tile == 0) tile = gemm_bf16_auto_tile(g, e);
+static hipError_t launch_tile(const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile) {
     switch (tile) {
         case 1: return run_tile<T256x256>(g, e, st);
         case 2: return run_tile<T256x128>(g, e, st);
@@ -631,6 +660,21 @@ hipError_t launch_gemm_bf16(const GemmArgs& g, const EpiParams& e, hipStream_t s
         case 5: return run_tile<T256x192>(g, e, st);
         default: return hipErrorInvalidValue;
     }
+}
+
+// rows [0, m_split) with the plan's tile, then the tail rows [m_split, M) with the tail tile;
+// both launches index rows globally (the epilogue's sample / token split needs it)
+hipError_t launch_gemm_bf16(const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile) {
+    if (tile != 0) return launch_tile(g, e, st, tile);
+    const GemmPlan p = gemm_bf16_plan(g, e);
+    if (!p.tail_tile) return launch_tile(g, e, st, p.tile);
+    GemmArgs gm = g;
+    gm.M = p.m_split;
+    const hipError_t err = launch_tile(gm, e, st, p.tile);
+    if (err != hipSuccess) return err;
+    GemmArgs gt = g;
+    gt.m_begin = p.m_split;
+    return launch_tile(gt, e, st, p.tail_tile);
 }
 
 }  // namespace sgd

@@ -19,6 +19,7 @@ struct GemmArgs {
     const void* A1 = nullptr; long lda1 = 0; int K0 = 0;
     const void* B = nullptr; long ldb = 0;
     int M = 0, N = 0, K = 0;  // N: product columns (gated: 2F)
+    int m_begin = 0;          // first row of the launch's row tiles (rows below belong to another launch)
 };
 
 enum EpKind { EP_HEADS = 0, EP_ACT = 1, EP_GATED = 2, EP_RESID = 3, EP_SKIP = 4 };
@@ -46,6 +47,9 @@ bool gemm_shape_ok(int dtype, const GemmArgs& g, const EpiParams& e, int tile = 
 hipError_t launch_gemm_bf16(const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile);
 bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile);
 int gemm_bf16_auto_tile(const GemmArgs& g, const EpiParams& e);
+// automatic tiling: rows [0, m_split) with `tile`, rows [m_split, M) (if any) with tail_tile
+struct GemmPlan { int tile, m_split, tail_tile; };
+GemmPlan gemm_bf16_plan(const GemmArgs& g, const EpiParams& e);
 
 // ---------------------------------------------------------------- attention
 // O[b, i, h*dh + j] = softmax_j'(q_i . k_j' / sqrt(dh)) v_j'  over keys j' < nk.

@@ -92,6 +92,41 @@ def test_linear_gated_bf16(P, tile):
     assert relmax(host(out), ref) <= 1e-2
 
 
+def test_linear_row_tail_split_bf16(P):
+    """8256 = 32 x 258 rows (U-ViT batch): the automatic tiling runs rows [0, 8192) and the
+    64-row tail as two launches; both must index rows globally."""
+    rng = np.random.default_rng(8256)
+    M, N, K = 8256, 4096, 128
+    A = synth.store(rng.standard_normal((M, K)), "bf16")
+    W = synth.store(rng.standard_normal((N, K)) / np.sqrt(K), "bf16")
+    b = synth.representable(0.1 * rng.standard_normal(N), "bf16")
+    out = empty((M, N), "bf16")
+    P.op_linear(dev(A), dev(W), out, bias=dev(b), act=1)
+    ref = om.gelu_erf(decode(A, "bf16") @ decode(W, "bf16").T + b)
+    got = host(out)
+    assert np.isfinite(got).all()
+    assert relmax(got, ref) <= 1e-2
+    assert relmax(got[8192:], ref[8192:]) <= 1e-2
+
+
+def test_residual_row_tail_split_bf16(P):
+    """Residual epilogue with per-sample gates (258 rows per sample) across the row-tail split."""
+    rng = np.random.default_rng(258)
+    B, ntok, N, K = 32, 258, 4096, 128
+    M = B * ntok
+    A = synth.store(rng.standard_normal((M, K)), "bf16")
+    W = synth.store(rng.standard_normal((N, K)) / np.sqrt(K), "bf16")
+    b = synth.representable(0.1 * rng.standard_normal(N), "bf16")
+    h0 = rng.standard_normal((M, N)).astype(np.float32)
+    d0 = rng.standard_normal((M, N)).astype(np.float32)
+    gate = rng.standard_normal((B, N)).astype(np.float32)
+    th, td = dev(h0), dev(d0)
+    P.op_residual(dev(A), dev(W), th, bias=dev(b), delta=td, delta_mode=2, gate=dev(gate), ntok=ntok)
+    v = (decode(A, "bf16") @ decode(W, "bf16").T + b) * np.repeat(gate, ntok, axis=0)
+    assert relmax(host(th), h0 + v) <= 1e-3
+    assert relmax(host(td), d0 + v) <= 1e-3
+
+
 @pytest.mark.parametrize("M,N,K", [(72, 128, 64), (256, 768, 256), (144, 1024, 256)])
 def test_linear_f32(P, M, N, K):
     rng = np.random.default_rng(M * N)
