@@ -38,8 +38,8 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
     constexpr int BQ = 32 * NW, BKV = 64, NT = NW * 64;
     constexpr int KS = DHP / 16, DT = DHP / 32;
     constexpr int KLDS = DHP + 8, VLDS = BKV + 8;        // padded rows: conflict-free fragment reads
-    constexpr int K_CH = BKV * (DHP / 8) / NT;            // 16-byte chunks per thread per block (upper bound)
-    constexpr int V_CH = DHP * (BKV / 8) / NT;
+    constexpr int K_CH = (BKV * (DHP / 8) + NT - 1) / NT;  // 16-byte chunks per thread per block (upper bound)
+    constexpr int V_CH = (DHP * (BKV / 8) + NT - 1) / NT;
     __shared__ __attribute__((aligned(16))) bf16 sk[2][BKV * KLDS];
     __shared__ __attribute__((aligned(16))) bf16 sv[2][DHP * VLDS];
 
@@ -245,8 +245,8 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
     constexpr int BQ = 32 * NQG, BKV = 64, HT = NQG * 64, NT = 2 * HT;
     constexpr int KS = DHP / 16, DT = DHP / 32;
     constexpr int KLDS = DHP + 8, VLDS = BKV + 8;        // padded rows: conflict-free fragment reads
-    constexpr int K_CH = BKV * (DHP / 8) / HT;            // 16-byte chunks per thread per block (upper bound)
-    constexpr int V_CH = DHP * (BKV / 8) / HT;
+    constexpr int K_CH = (BKV * (DHP / 8) + HT - 1) / HT;  // 16-byte chunks per thread per block (upper bound)
+    constexpr int V_CH = (DHP * (BKV / 8) + HT - 1) / HT;
     constexpr int HALF_BYTES = (BKV * KLDS + DHP * VLDS) * 2;
     constexpr int MERGE_BYTES = NQG * (DT * 16 + 2) * 64 * 4;  // half 1's state, lane-major
     static_assert(MERGE_BYTES <= 2 * HALF_BYTES, "merge area");
@@ -619,6 +619,14 @@ static void launch_attention_bf16(const AttnArgs& a, hipStream_t st) {
     } else if (qg128 < 1024) {
         // two-wave workgroups when four-wave ones would leave CUs without a second workgroup
         hipLaunchKernelGGL((attn_bf16_kernel<DH, 2>), dim3((a.nq + 63) / 64, BH), dim3(128), 0, st, a, sl2);
+    } else if (nkb < 8 && a.nq <= 256) {
+        // short sequences (DiT: 256 queries and keys per head): one workgroup holds every query
+        // of a head, so each key/value block is loaded once per head and the launch is a
+        // single round of workgroups
+        hipLaunchKernelGGL((attn_bf16_kernel<DH, 8>), dim3(1, BH), dim3(512), 0, st, a, sl2);
+    } else if (nkb < 8 && a.nq <= 288) {
+        // U-ViT: 258 queries per head (256 patches + time and class tokens)
+        hipLaunchKernelGGL((attn_bf16_kernel<DH, 9>), dim3(1, BH), dim3(576), 0, st, a, sl2);
     } else {
         hipLaunchKernelGGL((attn_bf16_kernel<DH, 4>), dim3((a.nq + 127) / 128, BH), dim3(256), 0, st, a, sl2);
     }

@@ -153,7 +153,12 @@ def _heads_inputs(rng, B, H, nq, nk, dh, dtype, npq, npk):
                                           # >= 8 key blocks: keys split between two wave halves
                                           # (odd block count, ragged tail, padded head dim)
                                           (1, 2, 300, 600, 128), (1, 3, 150, 1000, 64), (2, 2, 130, 700, 72),
-                                          (1, 2, 64, 513, 128)])
+                                          (1, 2, 64, 513, 128),
+                                          # many heads of short sequences: one workgroup per head
+                                          # (DiT 256 and U-ViT 258 queries, a ragged case), and
+                                          # the SDXL cross-attention shape (77 keys)
+                                          (32, 16, 256, 256, 72), (32, 16, 258, 258, 64), (16, 64, 250, 240, 64),
+                                          (8, 20, 1024, 77, 64)])
 def test_attention(P, dtype, B, H, nq, nk, dh):
     rng = np.random.default_rng(nq * 7 + nk + dh)
     npq, npk = -(-nq // 64) * 64, -(-nk // 64) * 64
