@@ -154,11 +154,12 @@ def _heads_inputs(rng, B, H, nq, nk, dh, dtype, npq, npk):
                                           # (odd block count, ragged tail, padded head dim)
                                           (1, 2, 300, 600, 128), (1, 3, 150, 1000, 64), (2, 2, 130, 700, 72),
                                           (1, 2, 64, 513, 128),
-                                          # many heads of short sequences: one workgroup per head
-                                          # (DiT 256 and U-ViT 258 queries, a ragged case), and
-                                          # the SDXL cross-attention shape (77 keys)
-                                          (32, 16, 256, 256, 72), (32, 16, 258, 258, 64), (16, 64, 250, 240, 64),
-                                          (8, 20, 1024, 77, 64)])
+                                          # many heads: 256-query workgroups (DiT, one per head; a
+                                          # ragged case; the SDXL cross-attention shape, 77 keys),
+                                          # U-ViT's 258 queries in one workgroup, and 128-query
+                                          # workgroups where 256 would add padded queries
+                                          (32, 16, 256, 256, 72), (16, 64, 250, 240, 64), (8, 20, 1024, 77, 64),
+                                          (32, 16, 258, 258, 64), (16, 64, 300, 300, 64)])
 def test_attention(P, dtype, B, H, nq, nk, dh):
     rng = np.random.default_rng(nq * 7 + nk + dh)
     npq, npk = -(-nq // 64) * 64, -(-nk // 64) * 64
