@@ -118,8 +118,11 @@ static hipError_t launch_norm_wpr(int dtype, const NormArgs& a, hipStream_t st) 
 }
 
 hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t st) {
-    // one wave per row while the rows alone give ~16 waves per CU, else four
-    return a.M >= 4096 ? launch_norm_wpr<1>(dtype, a, st) : launch_norm_wpr<4>(dtype, a, st);
+    // few rows (LLaDA: 1024): four waves per row.  Many rows: two waves per row when the row's
+    // float4 groups split evenly over 128 lanes (U-ViT, d = 1024: 13.9 -> 12.5 us), else one
+    // (DiT d = 1152 and SDXL d = 1280 measured slower with two: uneven lanes)
+    if (a.M < 4096) return launch_norm_wpr<4>(dtype, a, st);
+    return (a.d / 4) % 128 == 0 ? launch_norm_wpr<2>(dtype, a, st) : launch_norm_wpr<1>(dtype, a, st);
 }
 
 }  // namespace sgd
