@@ -95,7 +95,8 @@ def main() -> int:
                     help="tau-mode schedules (Eq. schedule at a fixed tau) timed beside the budgets; '' for none")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md, 'Sharding').",
+        print("bench.py measures one GPU: the library has no multi-GPU path (batches would shard by "
+              "sample with no exchange; LLaDA would need tensor parallelism).",
               file=sys.stderr)
         return 2
 

@@ -13,8 +13,9 @@ Paper passages followed:
 
 The architectures themselves (pre-norm attention + MLP blocks shaped like
 LLaDA-8B, DiT-XL/2, U-ViT-L and an SDXL spatial transformer) are standard
-and not specified by the paper; their constants are readings listed in
-the design doc (norm epsilons, RoPE base, GELU forms, sinusoidal embeddings).
+and not specified by the paper; their constants are readings of this
+implementation (norm epsilons, RoPE base, GELU forms, sinusoidal embeddings),
+fixed below.
 
 Precision: float64 everywhere.  For bf16 configs the values the GPU stores
 in bf16 are rounded with ``Precision.q``: norm outputs, Q/K/V after bias

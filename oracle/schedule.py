@@ -3,7 +3,7 @@
 Sec. 4.1, Eq. schedule:  S_l = max{S_min, ceil(T min(1, Lambda_hat_l / tau))}
 and Alg. 1 (score every matrix, combine, normalise, apply Eq. schedule).
 
-Readings (listed in DESIGN.md):
+Readings where the paper is silent:
 * S_min defaults to ceil(T / 10), the smallest integer >= 0.1 T.
 * A percentage budget is the integer ceiling N* = floor(pct L T / 100)
   layer-steps.

@@ -7,7 +7,7 @@ app-conv-score, app-block-score, app-score-normalization).
 
 All arithmetic is float64 on the stored weights upcast exactly.
 
-Readings where the paper is silent (also listed in the design doc):
+Readings where the paper is silent:
 * the default regulariser is eta = 1e-6 (the paper uses the regularised
   form in implementation but never prints eta);
 * a gated MLP's input projection W1 is the stacked [W_gate; W_up] matrix;
