@@ -29,6 +29,16 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uns
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
+// Rotary head projections: the q and k product columns of each head are taken in the order
+// (0, dh/2, 1, dh/2 + 1, ...), so the two dims of every rotary pair are adjacent columns and a
+// block tile of any even width holds whole pairs.  Column n of the product is weight row (and
+// bias entry) rope_row(n); v columns (n >= vstart) keep their order.
+__device__ __forceinline__ long rope_row(long n, int dh, long vstart) {
+    if (n >= vstart) return n;
+    const int hl = (int)(n % dh);
+    return n - hl + ((hl & 1) ? dh / 2 + hl / 2 : hl / 2);
+}
+
 template <int I> using IntC = std::integral_constant<int, I>;
 
 // f(IntC<0>{}), ..., f(IntC<N - 1>{})
@@ -122,12 +132,14 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
     float* sbias = st + C::EPR * C::EPS;                 // the tile's bias columns
     const int n0 = tn * C::BN;
     const bool gated = ep.kind == EP_GATED;
+    const bool rope = ep.kind == EP_HEADS && ep.rope;
+    const int vstart = ep.kind == EP_HEADS ? (2 - ep.which0) * ep.d : 0;  // first v^T product column
     __syncthreads();  // every wave is done with the stage buffers
     for (int c = tid; c < C::BN; c += C::NT) {
         float b = 0.f;
         if (ep.bias) {
             if (gated) b = ep.bias[c < C::BN / 2 ? tn * (C::BN / 2) + c : ep.F + tn * (C::BN / 2) + c - C::BN / 2];
-            else if (n0 + c < g.N) b = ep.bias[n0 + c];
+            else if (n0 + c < g.N) b = ep.bias[rope ? rope_row(n0 + c, ep.dh, vstart) : n0 + c];
         }
         sbias[c] = b;
     }
@@ -143,7 +155,6 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
     const int cg = (tid % RIG) * 4, rrg0 = tid < RIG * RPTG ? tid / RIG : C::EPR;  // gated
     const int n = n0 + c;
     // q/k columns without rotation: projection, head and dims of this thread's columns
-    const int vstart = ep.kind == EP_HEADS ? (2 - ep.which0) * ep.d : 0;
     int proj = 0, hh = 0, j = 0;
     if (ep.kind == EP_HEADS && n < g.N && n < vstart) {
         proj = ep.which0 + n / ep.d;
@@ -151,23 +162,26 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
         hh = nn / ep.dh;
         j = nn - hh * ep.dh;
     }
-    // rotary q/k tiles (whole heads, all q or all k): a thread owns four rotary pairs, dims
-    // pj .. pj+3 and pj+dh/2 .. pj+dh/2+3 of head ph, so one sine/cosine serves both dims of
-    // a pair; invt holds the pairs' inverse frequencies in turns per token
+    // rotary q/k columns (pairs adjacent, see rope_row): a thread owns eight consecutive
+    // columns, i.e. the four rotary pairs of dims pj .. pj+3 and pj+dh/2 .. pj+dh/2+3 of head
+    // ph (one head: dh % 8 == 0), so one sine/cosine serves both dims of a pair; invt holds
+    // the pairs' inverse frequencies in turns per token.  Tiles may hold columns of q and k,
+    // or of k and v (v columns go through the V^T path below).
     constexpr int RIP = C::BN / 8, RPTP = C::NT / RIP, PERP = (C::EPR + RPTP - 1) / RPTP;
     constexpr bool EXP = C::NT % RIP == 0 && C::EPR % RPTP == 0;
-    const bool rope_tile = ep.kind == EP_HEADS && ep.rope && n0 < vstart;
+    const int pc = (tid % RIP) * 8;  // first tile column of the thread's pairs
+    const bool rope_thread = rope && n0 + pc < vstart && n0 + pc < g.N;
+    const bool rope_tile = rope && n0 < vstart;
     const int rrp0 = tid < RIP * RPTP ? tid / RIP : C::EPR;
-    int pc = 0, ph = 0, pj = 0;
+    int ph = 0, pj = 0;
     float invt[4] = {0.f, 0.f, 0.f, 0.f};
     bf16* pbase = qptr;
-    if (rope_tile) {
-        const int hd = ep.dh / 2, pi = (tid % RIP) * 4;
-        const int hl = pi / hd;
-        pj = pi - hl * hd;
-        pc = hl * ep.dh + pj;
-        const int pproj = ep.which0 + n0 / ep.d;
-        ph = (n0 - (pproj - ep.which0) * ep.d) / ep.dh + hl;
+    if (rope_thread) {
+        const int pn = n0 + pc;
+        const int pproj = ep.which0 + pn / ep.d;
+        const int nn = pn - (pproj - ep.which0) * ep.d;
+        ph = nn / ep.dh;
+        pj = (nn - ph * ep.dh) / 2;
         pbase = pproj == 0 ? qptr : kptr;
 #pragma unroll
         for (int q = 0; q < 4; ++q)
@@ -315,23 +329,25 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
             // v_cos_f32 take turns) of the fractional turn; the turn count carries ~1e-4 rad of
             // fp32 rounding at 1024 tokens, far below the bf16 resolution of the output
             const int hd = ep.dh / 2;
-            const f32x4 b1 = ld4(sbias + pc), b2 = ld4(sbias + pc + hd);
+            const f32x4 ba = ld4(sbias + pc), bb = ld4(sbias + pc + 4);
 #pragma unroll 2
             for (int u = 0; u < PERP; ++u) {
                 const int rr = rrp0 + u * RPTP, row = grow(rr);
                 if (!EXP && rr >= C::EPR) continue;
-                const f32x4 v1 = ld4(st + rr * C::EPS + pc), v2 = ld4(st + rr * C::EPS + pc + hd);
-                if (row >= g.M) continue;
+                const f32x4 va = ld4(st + rr * C::EPS + pc), vb = ld4(st + rr * C::EPS + pc + 4);
+                if (row >= g.M || !rope_thread) continue;
                 const int bs = sample_of(row), tok = row - bs * ep.ntok;
+                // columns pc + 2q and pc + 2q + 1 hold dims pj + q and pj + q + dh/2
+                const float x1[4] = {va[0] + ba[0], va[2] + ba[2], vb[0] + bb[0], vb[2] + bb[2]};
+                const float x2[4] = {va[1] + ba[1], va[3] + ba[3], vb[1] + bb[1], vb[3] + bb[3]};
                 float o1[4], o2[4];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const float x1 = v1[q] + b1[q], x2 = v2[q] + b2[q];
                     const float t = (float)tok * invt[q];
                     const float f = t - rintf(t);
                     const float sn = __builtin_amdgcn_sinf(f), cs = __builtin_amdgcn_cosf(f);
-                    o1[q] = x1 * cs - x2 * sn;
-                    o2[q] = x2 * cs + x1 * sn;
+                    o1[q] = x1[q] * cs - x2[q] * sn;
+                    o2[q] = x2[q] * cs + x1[q] * sn;
                 }
                 bf16* const dst = pbase + (((long)bs * ep.H + ph) * ep.np + tok) * ep.dh + pj;
                 store_bf16x4(dst, o1);
@@ -411,6 +427,7 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
         const int r = vr + p * RPP;
         long gr;
         if (gated) gr = r < C::BN / 2 ? (long)tn * (C::BN / 2) + r : (long)F + tn * (C::BN / 2) + (r - C::BN / 2);
+        else if (ep.kind == EP_HEADS && ep.rope) gr = rope_row((long)tn * C::BN + r, ep.dh, (long)(2 - ep.which0) * ep.d);
         else gr = (long)tn * C::BN + r;
         goff[AP + p] = (unsigned)(gr * g.ldb * 2 + vc * 16);
     }
@@ -576,7 +593,6 @@ static double tile_cost(int tile, long rows, const GemmArgs& g, const EpiParams&
     const Shape s = tile_shape(tile);
     if (!s.bm) return 1e300;
     if (e.kind == EP_GATED && g.N % s.bn) return 1e300;
-    if (e.kind == EP_HEADS && e.rope && (s.bn % e.dh || e.d % s.bn)) return 1e300;
     const long tiles = ((rows + s.bm - 1) / s.bm) * ((g.N + s.bn - 1) / s.bn);
     return (double)((tiles + 255) / 256) * s.bm * s.bn / s.rate / (256.0 * 256.0);
 }
@@ -636,7 +652,7 @@ bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
     if ((e.kind == EP_RESID || e.kind == EP_SKIP) && (g.N != e.d)) return false;
     if (e.kind == EP_HEADS) {
         if (e.d % 32 || e.dh % 4) return false;  // V^T from whole 32-column MFMA blocks
-        if (e.rope && (e.dh % 8 || s.bn % e.dh || e.d % s.bn)) return false;  // whole heads per tile
+        if (e.rope && e.dh % 8) return false;  // eight-column pair groups within one head
     }
     const long lim = 0xFFFFFF00L;  // 32-bit buffer ranges below the loader's out-of-range offset
     if ((long)g.M * g.lda0 * 2 > lim || (g.A1 && (long)g.M * g.lda1 * 2 > lim) || (long)g.N * g.ldb * 2 > lim)
