@@ -27,14 +27,24 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 
+def _grid(r) -> int:
+    """Work-items of a dispatch (rocprofv3 names the column Grid_Size or Grid_Size_X)."""
+    for k in ("Grid_Size", "Grid_Size_X"):
+        if r.get(k):
+            return int(r[k])
+    return 0
+
+
 def kernel_stats(rows):
+    """Per (kernel, grid size): one template instance serves GEMMs of different shapes (e.g. the
+    LLaDA QKV and MLP input GEMMs both run 256 x 192 tiles), which the grid tells apart."""
     agg = defaultdict(lambda: [0, 0.0])
     for r in rows:
-        a = agg[r["Kernel_Name"]]
+        a = agg[(r["Kernel_Name"], _grid(r))]
         a[0] += 1
         a[1] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3  # us
     tot = sum(v[1] for v in agg.values())
-    return sorted(((k, n, t, t / n, 100.0 * t / tot) for k, (n, t) in agg.items()), key=lambda x: -x[2])
+    return sorted(((k, g, n, t, t / n, 100.0 * t / tot) for (k, g), (n, t) in agg.items()), key=lambda x: -x[3])
 
 
 def frozen_rates(cfg, rows, lifetimes):
@@ -80,9 +90,9 @@ def main() -> int:
 
     cfg = synth.get_config(args.workload)
     rows = list(csv.DictReader(open(args.trace)))
-    print("| kernel | calls | total ms | avg us | % |\n|---|---:|---:|---:|---:|")
-    for name, n, t, avg, pc in kernel_stats(rows)[:12]:
-        print(f"| `{name[:110]}` | {n} | {t / 1e3:.1f} | {avg:.2f} | {pc:.2f} |")
+    print("| kernel | grid (work-items) | calls | total ms | avg us | % |\n|---|---:|---:|---:|---:|---:|")
+    for name, grid, n, t, avg, pc in kernel_stats(rows)[:14]:
+        print(f"| `{name[:110]}` | {grid} | {n} | {t / 1e3:.1f} | {avg:.2f} | {pc:.2f} |")
     print("\n| budget | timed frozen-run launches | GB | ms | GB/s | of 8 TB/s |\n|---:|---:|---:|---:|---:|---:|")
     for pct, n, nbytes, secs in frozen_rates(cfg, rows, json.load(open(args.lifetimes))):
         print(f"| {pct}% | {n} | {nbytes / 1e9:.2f} | {secs * 1e3:.2f} | {nbytes / secs / 1e9:.0f} | "

@@ -103,3 +103,14 @@ def test_bench_refuses_more_than_one_gpu():
                        text=True, timeout=300, cwd=ROOT)
     assert r.returncode != 0
     assert "one GPU" in r.stderr
+
+
+def test_trace_report_separates_grids():
+    from paper_2609_29505_amd import trace_report
+
+    rows = [{"Kernel_Name": "gemm<256, 192>", "Grid_Size": "131072", "Start_Timestamp": "0", "End_Timestamp": "96000"},
+            {"Kernel_Name": "gemm<256, 192>", "Grid_Size": "262144", "Start_Timestamp": "0", "End_Timestamp": "178000"},
+            {"Kernel_Name": "gemm<256, 192>", "Grid_Size": "262144", "Start_Timestamp": "0", "End_Timestamp": "180000"}]
+    st = trace_report.kernel_stats(rows)
+    assert [(g, n) for _, g, n, _, _, _ in st] == [(262144, 2), (131072, 1)]
+    assert st[0][4] == pytest.approx(179.0) and st[1][4] == pytest.approx(96.0)
