@@ -249,13 +249,14 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
     constexpr int V_CH = (DHP * (BKV / 8) + HT - 1) / HT;
     constexpr int HALF_BYTES = (BKV * KLDS + DHP * VLDS) * 2;
     constexpr int MERGE_BYTES = NQG * (DT * 16 + 2) * 64 * 4;  // half 1's state, lane-major
-    static_assert(MERGE_BYTES <= 2 * HALF_BYTES, "merge area");
-    __shared__ __attribute__((aligned(16))) char smem[2 * HALF_BYTES];
+    static_assert(MERGE_BYTES <= 4 * HALF_BYTES, "merge area");
+    __shared__ __attribute__((aligned(16))) char smem[4 * HALF_BYTES];  // two buffers per half
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int kh = wave / NQG, qg = wave % NQG, htid = tid - kh * HT;
-    bf16* sk = (bf16*)(smem + kh * HALF_BYTES);
-    bf16* sv = sk + BKV * KLDS;
+    bf16* const sk0 = (bf16*)(smem + kh * 2 * HALF_BYTES);  // buffer b: sk0 + b * HALF_BYTES / 2
+    constexpr int BUF = HALF_BYTES / 2;                     // bf16 elements per buffer
+    constexpr int VOFF = BKV * KLDS;                        // V^T part of a buffer
     const int bh = blockIdx.y;
     const int b = bh / a.H, hh = bh - b * a.H;
     constexpr int dh = DH;
@@ -267,8 +268,12 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
     const bf16* VT = (const bf16*)a.vt + (long)bh * dh * a.npk;
 
     // zero the padded head dims of this half's buffers once (the loads never write them)
-    for (int i = htid; i < BKV * (DHP - dh); i += HT) sk[(i / (DHP - dh)) * KLDS + dh + i % (DHP - dh)] = f2bf(0.f);
-    for (int i = htid; i < (DHP - dh) * BKV; i += HT) sv[(dh + i / BKV) * VLDS + i % BKV] = f2bf(0.f);
+#pragma unroll
+    for (int bb = 0; bb < 2; ++bb) {
+        bf16* const zk = sk0 + bb * BUF;
+        for (int i = htid; i < BKV * (DHP - dh); i += HT) zk[(i / (DHP - dh)) * KLDS + dh + i % (DHP - dh)] = f2bf(0.f);
+        for (int i = htid; i < (DHP - dh) * BKV; i += HT) zk[VOFF + (dh + i / BKV) * VLDS + i % BKV] = f2bf(0.f);
+    }
 
     // this lane's query fragments (B operand of S^T = K Q^T)
     bf16x8 qf[KS];
@@ -302,7 +307,9 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
             }
         }
     };
-    auto lstore = [&](int k0) {
+    auto lstore = [&](int k0, int bb) {
+        bf16* const sk = sk0 + bb * BUF;
+        bf16* const sv = sk + VOFF;
 #pragma unroll
         for (int t = 0; t < K_CH; ++t) {
             const int i = htid + t * HT;
@@ -343,15 +350,25 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
 
     const int nkb = (a.nk + BKV - 1) / BKV;
     const int nit = (nkb + 1) / 2;  // block pairs: half h takes block 2 it + h
+    // Two LDS buffers per half: iteration it computes block 2 it + kh from buffer it & 1 while
+    // block 2 (it + 1) + kh moves from registers into the other buffer (read last in iteration
+    // it - 1, before its closing barrier) and block 2 (it + 2) + kh is loaded into registers:
+    // one barrier per iteration.
     if (kh < nkb) gload(kh * BKV);
     __syncthreads();  // padding zeroed
-    if (kh < nkb) lstore(kh * BKV);
+    if (kh < nkb) lstore(kh * BKV, 0);
+    if (kh + 2 < nkb) gload((kh + 2) * BKV);
     __syncthreads();
     for (int it = 0; it < nit; ++it) {
         const int kb = 2 * it + kh;
         const int k0 = kb * BKV;
         const bool mine = kb < nkb;
-        if (kb + 2 < nkb) gload(k0 + 2 * BKV);  // in flight while this block computes
+        const bf16* const sk = sk0 + (it & 1) * BUF;
+        const bf16* const sv = sk + VOFF;
+        if (kb + 2 < nkb) {
+            lstore(k0 + 2 * BKV, (it & 1) ^ 1);
+            if (kb + 4 < nkb) gload(k0 + 4 * BKV);  // in flight while this block computes
+        }
         if (mine) {
             f32x16 s[2];
 #pragma unroll
@@ -418,11 +435,7 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
                 }
             }
         }
-        if (it + 1 < nit) {
-            __syncthreads();  // both halves are done with their buffers
-            if (kb + 2 < nkb) lstore(k0 + 2 * BKV);
-            __syncthreads();
-        }
+        __syncthreads();  // block it + 1 is in place; buffer it & 1 is free
     }
 
     // merge the two key halves through LDS (lane-major: conflict-free)
