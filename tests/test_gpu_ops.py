@@ -307,9 +307,11 @@ def test_residual(P, dtype, tile, M, N, K, gated_rows, mode):
         assert np.array_equal(host(td), d0.astype(np.float64))
 
 
+@pytest.mark.parametrize("rope", [False, True])
 @pytest.mark.parametrize("tile", TILES)
-def test_heads_kv_only(P, tile):
-    """Key/value projection of a context (which0 = 1): columns [0, d) are k, [d, 2d) are v^T."""
+def test_heads_kv_only(P, tile, rope):
+    """Key/value projection of a context (which0 = 1): columns [0, d) are k, [d, 2d) are v^T;
+    with rope, the k columns are read in rotary-pair order."""
     rng = np.random.default_rng(77 + tile)
     B, N, H, dh, K = 3, 77, 5, 64, 192
     d = H * dh
@@ -318,9 +320,11 @@ def test_heads_kv_only(P, tile):
     A = synth.store(rng.standard_normal((M, K)), "bf16")
     W = synth.store(rng.standard_normal((2 * d, K)) / np.sqrt(K), "bf16")
     k, vt = empty((B * H, np_, dh), "bf16"), empty((B * H, dh, np_), "bf16")
-    P.op_heads(dev(A), dev(W), None, k, vt, 2, 1, N, H, dh, tile=tile)
+    P.op_heads(dev(A), dev(W), None, k, vt, 2, 1, N, H, dh, rope=rope, tile=tile)
     z = decode(A, "bf16") @ decode(W, "bf16").T
     Kr, Vr = (om.heads(z[:, i * d:(i + 1) * d].reshape(B, N, d), H) for i in range(2))
+    if rope:
+        Kr = om.rope(Kr)
     got_k = host(k).reshape(B, H, np_, dh)[:, :, :N]
     got_v = host(vt).reshape(B, H, dh, np_)[:, :, :, :N].transpose(0, 1, 3, 2)
     for g, r in ((got_k, Kr), (got_v, Vr)):
