@@ -48,9 +48,9 @@ int sgd_op_norm(int32_t dtype, int32_t kind, const float* x, void* y, int32_t M,
  * (+ bias), column n of P belongs to projection which0 + n / d (0: q, 1: k, 2: v^T), head
  * (n % d) / dh, dim n % dh; row r is token r % ntok of sample r / ntok.  q, k are
  * [B*H, np, dh], vt is [B*H, dh, np].  rope != 0 rotates the q and k pairs (i, i + dh/2) of
- * token t by t * 10000^(-2i/dh) (bf16 only; every block tile must hold whole heads: H*dh a
- * multiple of the tile width, dh a multiple of 8 dividing it).  Padded tokens (>= ntok) are not
- * written.  tile as for sgd_op_linear. */
+ * token t by t * 10000^(-2i/dh) (rotary position embedding, the LLaDA attention; bf16 only,
+ * dh a multiple of 8; any tile width).  Padded tokens (>= ntok) are not written.  tile as for
+ * sgd_op_linear. */
 int sgd_op_heads(int32_t dtype, const void* A, const void* W, const float* bias, void* q, void* k, void* vt,
                  int32_t M, int32_t K, int32_t n_proj, int32_t which0, int32_t ntok, int32_t np, int32_t H,
                  int32_t dh, int32_t rope, int32_t tile, void* hip_stream);
