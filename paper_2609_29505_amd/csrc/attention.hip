@@ -632,9 +632,11 @@ static void launch_attention_bf16(const AttnArgs& a, hipStream_t st) {
     } else if (qg128 < 1024) {
         // two-wave workgroups when four-wave ones would leave CUs without a second workgroup
         hipLaunchKernelGGL((attn_bf16_kernel<DH, 2>), dim3((a.nq + 63) / 64, BH), dim3(128), 0, st, a, sl2);
-    } else if (nkb < 8 && a.nq > 256 && a.nq <= 288) {
+    } else if (DH <= 96 && nkb < 8 && a.nq > 256 && a.nq <= 288) {
         // U-ViT: 258 queries per head (256 patches + time and class tokens) in one workgroup
-        hipLaunchKernelGGL((attn_bf16_kernel<DH, 9>), dim3(1, BH), dim3(576), 0, st, a, sl2);
+        // (nine waves leave 170 VGPRs a wave: head dims above 96 would spill)
+        if constexpr (DH <= 96)
+            hipLaunchKernelGGL((attn_bf16_kernel<DH, 9>), dim3(1, BH), dim3(576), 0, st, a, sl2);
     } else if ((a.nq + 255) / 256 * 256 == (a.nq + 127) / 128 * 128) {
         // 256-query workgroups where they add no padded queries (DiT: one workgroup per head;
         // SDXL: four): each key/value block is loaded once per 256 queries

@@ -159,7 +159,7 @@ def _heads_inputs(rng, B, H, nq, nk, dh, dtype, npq, npk):
                                           # U-ViT's 258 queries in one workgroup, and 128-query
                                           # workgroups where 256 would add padded queries
                                           (32, 16, 256, 256, 72), (16, 64, 250, 240, 64), (8, 20, 1024, 77, 64),
-                                          (32, 16, 258, 258, 64), (16, 64, 300, 300, 64)])
+                                          (32, 16, 258, 258, 64), (16, 64, 300, 300, 64), (16, 32, 260, 200, 128)])
 def test_attention(P, dtype, B, H, nq, nk, dh):
     rng = np.random.default_rng(nq * 7 + nk + dh)
     npq, npk = -(-nq // 64) * 64, -(-nk // 64) * 64
