@@ -2,7 +2,8 @@
 bench.py times.
 
 * Step parity, teacher-forced: step 1 (every unit active) and step 2 with every other unit
-  frozen (lifetimes 1 / T) match the oracle at the per-step bar (2e-2 bf16, 1e-4 fp32).
+  frozen (lifetimes 1 / T) match the oracle at the per-step bar (2e-2 bf16, 1e-4 fp32); step 1
+  run twice gives bitwise the same state.
 * Schedule: budget, bounds and nesting properties at any size; the schedule equals the
   host budget reading of its own scores; sampled matrices' statistics and one unit's raw
   score match the oracle computed one by one.
@@ -71,6 +72,14 @@ def test_fullsize_step_parity(P, name):
     z = torch.from_numpy(x["z"].copy()).cuda()
     dm.step(z, 1, sched, cache)
     g1 = z.cpu().numpy().astype(np.float64)
+    # the same step again on a fresh cache: bitwise the same state (no order-dependent sums,
+    # e.g. in the split-K exchange of the long-K MLP output GEMM)
+    cache_b = P.Cache(dm)
+    cache_b.reset()
+    zb = torch.from_numpy(x["z"].copy()).cuda()
+    dm.step(zb, 1, sched, cache_b)
+    assert np.array_equal(zb.cpu().numpy(), z.cpu().numpy())
+    del cache_b, zb
     progress(f"{name}: oracle step 1")
     oc = {}
     eps1 = om.denoise_step(m, x["z"], 1, mask[0], oc, cross)
