@@ -22,6 +22,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "tile_order.h"
 
 namespace sgd {
 
@@ -397,10 +398,8 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
     const bool gated = ep.kind == EP_GATED;
     const int nt_m = (g.M - g.m_begin + C::BM - 1) / C::BM;
     const int nt_n = (g.N + C::BN - 1) / C::BN;
-    const int total = nt_m * nt_n;
-    const int bid = blockIdx.x;
-    const int t = total % 8 == 0 ? (bid % 8) * (total / 8) + bid / 8 : bid;
-    const int tm = t % nt_m, tn = t / nt_m;
+    int tm, tn;
+    tile_at(tile_position(blockIdx.x, nt_m * nt_n), nt_m, nt_n, g.band, tm, tn);
     const int m0 = g.m_begin + tm * C::BM;
     const int F = g.N / 2;
 
@@ -663,7 +662,9 @@ bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
 template <class C>
 static hipError_t run_tile(const GemmArgs& g, const EpiParams& e, hipStream_t st) {
     const int nt_m = (g.M - g.m_begin + C::BM - 1) / C::BM, nt_n = (g.N + C::BN - 1) / C::BN;
-    hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3(nt_m * nt_n), dim3(C::NT), 0, st, g, e);
+    GemmArgs ga = g;
+    ga.band = tile_band(nt_m, nt_n, C::BM, C::BN);
+    hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3(nt_m * nt_n), dim3(C::NT), 0, st, ga, e);
     return hipGetLastError();
 }
 

@@ -20,6 +20,7 @@ struct GemmArgs {
     const void* B = nullptr; long ldb = 0;
     int M = 0, N = 0, K = 0;  // N: product columns (gated: 2F)
     int m_begin = 0;          // first row of the launch's row tiles (rows below belong to another launch)
+    int band = 0;             // bf16 GEMM tile order: row tiles per band (set by the dispatcher)
 };
 
 enum EpKind { EP_HEADS = 0, EP_ACT = 1, EP_GATED = 2, EP_RESID = 3, EP_SKIP = 4 };

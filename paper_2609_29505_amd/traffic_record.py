@@ -7,7 +7,9 @@
         --write <dir>/write/p_counter_collection.csv --kernel gemm_bf16_kernel --copy-mib 256 \\
         --source paper_2609_29505_amd/csrc/gemm_bf16.hip --algorithmic-bytes <B> --out profiles/<k>_<w>_traffic.json
 
-FETCH_SIZE and WRITE_SIZE (KiB per dispatch) count traffic below the L2.  The same passes
+FETCH_SIZE and WRITE_SIZE (KiB per dispatch) count traffic below the L2.  --group N sums
+every N consecutive dispatches of the kernel into one call (a GEMM whose rows are split into a
+main launch and a row-tail launch).  The same passes
 measure a device-to-device copy of --copy-mib MiB (read and written once), and each counter is
 scaled by (copy bytes) / (copy counter): the factor that turns the counter into bytes on this
 GPU.  The record keeps the SHA-256 of the kernel's source file, so that a reader (bench.py)
@@ -36,6 +38,14 @@ def per_dispatch(path: str, counter: str, match: str):
     return [vals[k] for k in sorted(vals)]
 
 
+def grouped(vals, n: int):
+    """Sums of n consecutive values (one call of a kernel dispatched as n launches); a
+    trailing incomplete group is dropped."""
+    if n < 1:
+        raise ValueError("group size must be positive")
+    return [sum(vals[i:i + n]) for i in range(0, len(vals) - n + 1, n)]
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--fetch", required=True, help="counter_collection.csv of the FETCH_SIZE pass")
@@ -49,11 +59,12 @@ def main() -> int:
     ap.add_argument("--describe-workload", default="")
     ap.add_argument("--command", action="append", default=[], help="command lines that produced the passes")
     ap.add_argument("--note", default="")
+    ap.add_argument("--group", type=int, default=1, help="consecutive dispatches that form one call")
     ap.add_argument("--out", required=True)
     a = ap.parse_args()
 
-    fk = per_dispatch(a.fetch, "FETCH_SIZE", a.kernel)
-    wk = per_dispatch(a.write, "WRITE_SIZE", a.kernel)
+    fk = grouped(per_dispatch(a.fetch, "FETCH_SIZE", a.kernel), a.group)
+    wk = grouped(per_dispatch(a.write, "WRITE_SIZE", a.kernel), a.group)
     fc = per_dispatch(a.fetch, "FETCH_SIZE", a.copy_match)
     wc = per_dispatch(a.write, "WRITE_SIZE", a.copy_match)
     if not fk or not wk or not fc or not wc:
@@ -71,6 +82,7 @@ def main() -> int:
         "source": a.source,
         "sha256": hashlib.sha256(open(src, "rb").read()).hexdigest(),
         "commands": a.command,
+        "dispatches_per_call": a.group,
         "fetch_size_kib_per_dispatch": fk,
         "write_size_kib_per_dispatch": wk,
         f"copy_{a.copy_mib}mib_fetch_size_kib": fc,

@@ -54,6 +54,39 @@ def test_traffic_record_scales_by_the_copy(tmp_path):
     assert len(rec["sha256"]) == 64
 
 
+def test_traffic_record_groups_split_launches(tmp_path):
+    from paper_2609_29505_amd import traffic_record as tr
+
+    # one call = a main launch and a row-tail launch; the pass ends with the copy
+    kib = 256 * 1024
+    _counter_csv(tmp_path / "f.csv", "FETCH_SIZE",
+                 [(1, "void k<1>(A)", 1000.0), (2, "void k<2>(A)", 100.0), (3, "void k<1>(A)", 800.0),
+                  (4, "void k<2>(A)", 60.0), (5, "void k<1>(A)", 820.0), (6, "void k<2>(A)", 40.0),
+                  (7, "__amd_rocclr_copyBuffer", kib / 2)])
+    _counter_csv(tmp_path / "w.csv", "WRITE_SIZE",
+                 [(1, "void k<1>(A)", 10.0), (2, "void k<2>(A)", 1.0), (3, "void k<1>(A)", 10.0),
+                  (4, "void k<2>(A)", 1.0), (5, "void k<1>(A)", 10.0), (6, "void k<2>(A)", 1.0),
+                  (7, "__amd_rocclr_copyBuffer", float(kib))])
+    out = tmp_path / "rec.json"
+    argv = ["traffic_record", "--fetch", str(tmp_path / "f.csv"), "--write", str(tmp_path / "w.csv"),
+            "--kernel", "void k<", "--group", "2", "--source", "bench.py", "--algorithmic-bytes", "1000",
+            "--out", str(out)]
+    old = sys.argv
+    try:
+        sys.argv = argv
+        assert tr.main() == 0
+    finally:
+        sys.argv = old
+    rec = json.load(open(out))
+    assert rec["dispatches_per_call"] == 2
+    assert rec["fetch_size_kib_per_dispatch"] == [1100.0, 860.0, 860.0]
+    assert rec["fetch_bytes"] == round(860.0 * 2.0 * 1024)
+    assert rec["write_bytes"] == round(11.0 * 1024)
+    assert tr.grouped([1, 2, 3, 4, 5], 2) == [3, 7]
+    with pytest.raises(ValueError):
+        tr.grouped([1.0], 0)
+
+
 def _trace_rows(cfg, lifetimes, extra=0):
     """Frozen-run dispatches in bench.py's order: every budget (T warm-up + 2T timed steps), then
     the headline budget once more; launch i lasts 1 + i ns."""
