@@ -14,8 +14,21 @@
 // partial softmax states are merged through LDS in wave order.
 #include "common.h"
 #include "kernels.h"
+#include "tile_order.h"
 
 namespace sgd {
+
+// Query block and head (batch x head index) of a bf16 workgroup, from a grid of query blocks x
+// heads.  The workgroups go round-robin to the XCDs in dispatch order (x fastest); they are
+// renumbered so that the query blocks of one head are neighbours in the order that the XCDs
+// split between them (tile_position), i.e. run on one XCD and read the head's keys and values
+// through one L2 instead of one per XCD.
+__device__ __forceinline__ void attn_block(int& qb, int& bh) {
+    const int nqb = gridDim.x;
+    const int pos = tile_position(blockIdx.y * nqb + blockIdx.x, nqb * gridDim.y);
+    bh = pos / nqb;
+    qb = pos - bh * nqb;
+}
 
 // {v[l], v[l ^ 32]} combined across the two 32-lane halves of the wave (one lane swap)
 __device__ __forceinline__ float pair_max(float v) {
@@ -44,10 +57,11 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
     __shared__ __attribute__((aligned(16))) bf16 sv[2][DHP * VLDS];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int bh = blockIdx.y;
+    int qb, bh;
+    attn_block(qb, bh);
     const int b = bh / a.H, hh = bh - b * a.H;
     constexpr int dh = DH;
-    const int q = blockIdx.x * BQ + wave * 32 + (lane & 31);
+    const int q = qb * BQ + wave * 32 + (lane & 31);
     const int half = lane >> 5;
 
     const bf16* Q = (const bf16*)a.q + (long)bh * a.npq * dh;
@@ -257,10 +271,11 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
     bf16* const sk0 = (bf16*)(smem + kh * 2 * HALF_BYTES);  // buffer b: sk0 + b * HALF_BYTES / 2
     constexpr int BUF = HALF_BYTES / 2;                     // bf16 elements per buffer
     constexpr int VOFF = BKV * KLDS;                        // V^T part of a buffer
-    const int bh = blockIdx.y;
+    int qb, bh;
+    attn_block(qb, bh);
     const int b = bh / a.H, hh = bh - b * a.H;
     constexpr int dh = DH;
-    const int q = blockIdx.x * BQ + qg * 32 + (lane & 31);
+    const int q = qb * BQ + qg * 32 + (lane & 31);
     const int half = lane >> 5;
 
     const bf16* Q = (const bf16*)a.q + (long)bh * a.npq * dh;
