@@ -3,14 +3,16 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config llada] [--budget 35]
 
 A "step" is one network evaluation of the whole unit stack plus the sampler update,
-for the full batch of the workload (Alg. 2 + the update of Sec. 3.1).  Steps run in
-trajectory order 1..T and wrap to a fresh trajectory (cache reset) after step T, so K = T
-times one complete scheduled trajectory.  Inputs and weights are seeded synthetic data
-with the workload's shapes (planted power-law spectra), resident in HBM before timing.
+for the full batch of the workload (Alg. 2 + the update of Sec. 3.1).  Timing is done in
+whole T-step trajectories (a fresh cache and z_1 each): ceil(K / T) of them, at least one,
+so every timed step is part of a complete trajectory and the timed mask rows are the whole
+schedule.  `value` = T / median trajectory time.  Inputs and weights are seeded synthetic
+data with the workload's shapes (planted power-law spectra), resident in HBM before timing.
 
 Prints one JSON line.  `value` is scheduled denoising steps/s at the headline budget; the
-all-active rate (every unit computing at every step, same launcher) and the other budgets
-are reported beside it.  `roofline` times the dominant kernel (the gated MLP input GEMM)
+all-active rate (every unit computing at every step, same launcher), the other budgets, the
+tau-mode schedules and the static ranking rules (with each one's output deviation from the
+all-active trajectory) are reported beside it.  `roofline` times the dominant kernel (the gated MLP input GEMM)
 with HIP events on the launch stream inside the timed region.  `cpu_baseline` times the
 CPU oracle on a bounded sample (a few units of an all-active step).
 """
@@ -78,8 +80,9 @@ def frozen_launch_bytes(cfg, active_row) -> list:
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=0, help="timed steps (default 2 T)")
-    ap.add_argument("--warmup", type=int, default=0, help="warm-up steps (default T)")
+    ap.add_argument("--steps", type=int, default=0,
+                    help="steps to time, rounded up to whole trajectories (default 3 T)")
+    ap.add_argument("--warmup", type=int, default=0, help="warm-up steps per schedule (default T)")
     ap.add_argument("--config", default="llada")
     ap.add_argument("--budget", type=int, default=0, help="headline budget in percent (default: smallest)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -93,6 +96,8 @@ def main() -> int:
                     "instead of rebuilding the spectra (e.g. under a kernel tracer)")
     ap.add_argument("--taus", default="0.5,1,2",
                     help="tau-mode schedules (Eq. schedule at a fixed tau) timed beside the budgets; '' for none")
+    ap.add_argument("--rules", default="random,depth,frob,spectral,stable_rank,frob_srank,raw_scr",
+                    help="static ranking rules timed at the headline budget; '' for none")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the library has no multi-GPU path (batches would shard by "
@@ -108,7 +113,8 @@ def main() -> int:
 
     cfg = synth.get_config(args.config)
     T, L = cfg.T, cfg.L
-    K = args.steps or 2 * T
+    K = args.steps or 3 * T
+    n_traj = max(1, -(-K // T))  # whole trajectories
     W = args.warmup or T
     budgets = sorted(cfg.budgets)
     head = args.budget or budgets[0]
@@ -130,31 +136,43 @@ def main() -> int:
 
     t0 = time.time()
     scheds = {}
-    n_head = P.budget_layer_steps(head, L, T)
+    units = dm.scored_units()
+    roles = [[r for r, _ in u] for u in units]
+    rule_names = [r for r in args.rules.split(",") if r]
     if args.lifetimes:
         saved = json.load(open(args.lifetimes))
         for pct in budgets:
             scheds[pct] = P.schedule_from_lifetimes(saved[str(pct)], T)
         scores = saved.get("scores")
+        mat_stats = np.array(saved["mat_stats"]) if "mat_stats" in saved else None
     else:
-        scheds[head] = P.schedule_build(dm.scored_units(), [cfg.dh] * L, T, budget=n_head)
+        scheds[head] = P.schedule_build(units, [cfg.dh] * L, T, budget_pct=head)
         scores = scheds[head].unit_score.tolist()
+        mat_stats = scheds[head].mat_stats.copy()
     t_build = time.time() - t0
     for pct in budgets:
         if args.lifetimes:
             continue
         if pct != head:  # same spectra, lifetimes at another budget
-            scheds[pct] = P.schedule_from_scores(scheds[head].unit_score, T, budget=P.budget_layer_steps(pct, L, T))
+            scheds[pct] = P.schedule_from_scores(scheds[head].unit_score, T, budget_pct=pct)
         log(f"budget {pct}%: N*={scheds[pct].layer_steps} lifetimes={scheds[pct].lifetimes.tolist()} "
             f"margin={scheds[pct].cut_margin:.3g}")
-    log(f"schedule ready in {t_build:.1f}s (spectra of {sum(len(u) for u in dm.scored_units())} matrices; "
+    log(f"schedule ready in {t_build:.1f}s (spectra of {sum(len(u) for u in units)} matrices; "
         f"offline, not timed)")
     if args.save_lifetimes:
         rec = {str(p): scheds[p].lifetimes.tolist() for p in budgets}
         rec["scores"] = scores
+        rec["mat_stats"] = mat_stats.tolist() if mat_stats is not None else None
         json.dump(rec, open(args.save_lifetimes, "w"))
     taus = [float(t) for t in args.taus.split(",") if t] if scores is not None else []
     tau_scheds = {t: P.schedule_from_scores(scores, T, tau=t) for t in taus}
+    # the static ranking baselines at the headline budget, re-ranked from the same spectra
+    rule_scheds = {}
+    for r in rule_names:
+        if r in ("depth", "random"):
+            rule_scheds[r] = P.schedule_build(None, None, T, budget_pct=head, rule=r, seed=2024, L=L)
+        elif mat_stats is not None:
+            rule_scheds[r] = P.schedule_from_stats(roles, [cfg.dh] * L, mat_stats, T, budget_pct=head, rule=r)
     all_active = P.schedule_from_lifetimes([T] * L, T)
 
     z0 = torch.from_numpy(inputs["z"]).cuda()
@@ -162,57 +180,85 @@ def main() -> int:
     cache = P.Cache(dm)
     stream = torch.cuda.current_stream()
 
-    def run(sched, nsteps, start):
-        """Enqueue nsteps steps continuing a trajectory at step `start` (1-based)."""
-        s = start
-        for _ in range(nsteps):
-            if s == 1:
-                cache.reset()
-                z.copy_(z0)
+    def trajectory(sched, steps=T):
+        """Enqueue steps 1..steps of a fresh trajectory (cache reset, z = z_1)."""
+        cache.reset()
+        z.copy_(z0)
+        for s in range(1, steps + 1):
             dm.step(z, s, sched, cache)
-            s = s + 1 if s < T else 1
-        return s
 
     def timed(sched, profile=None):
-        run(sched, W, 1)
+        """W warm-up steps, then n_traj whole trajectories, each bracketed by HIP events on
+        the step stream.  Returns the per-trajectory times (ms) and the profile record."""
+        w = W
+        while w > 0:
+            trajectory(sched, min(w, T))
+            w -= T
         torch.cuda.synchronize()
         if profile:
             dm.profile_begin(profile, 16384)
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        evs = []
+        for _ in range(n_traj):
+            cache.reset()
+            z.copy_(z0)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for s in range(1, T + 1):
+                dm.step(z, s, sched, cache)
+            e1.record(stream)
+            evs.append((e0, e1))
         torch.cuda.synchronize()
-        ev0.record(stream)
-        run(sched, K, 1)
-        ev1.record(stream)
-        torch.cuda.synchronize()
-        ms = ev0.elapsed_time(ev1)
+        times = [a.elapsed_time(b) for a, b in evs]
         prof = dm.profile_end() if profile else None
-        return ms, prof
+        return times, prof
+
+    def rate(times):
+        return T * 1000.0 / float(np.median(times))
 
     results = {}
     for pct in budgets:
-        ms, _ = timed(scheds[pct])
-        results[pct] = (ms, None)
-        log(f"budget {pct}%: {K} steps in {ms:.2f} ms -> {K * 1000.0 / ms:.2f} steps/s")
-    ms_all, _ = timed(all_active)
-    log(f"all-active: {K} steps in {ms_all:.2f} ms -> {K * 1000.0 / ms_all:.2f} steps/s")
+        times, _ = timed(scheds[pct])
+        results[pct] = times
+        log(f"budget {pct}%: {n_traj} trajectories of {T} steps, median {np.median(times):.2f} ms "
+            f"-> {rate(times):.2f} steps/s")
+    t_all, _ = timed(all_active)
+    z_full = z.clone()  # the all-active trajectory's final state
+    log(f"all-active: median {np.median(t_all):.2f} ms per trajectory -> {rate(t_all):.2f} steps/s")
+    all_rate = rate(t_all)
     # kernel timings in runs of their own, so that the steps/s figures above carry no
     # per-launch events: the frozen-run kernel in the headline schedule (the all-active
     # schedule has none), the profiled kernel class in the all-active schedule
     ms_fz, prof_fz = timed(scheds[head], "frozen")
-    results[head] = (results[head][0], prof_fz)
     ms_pk, prof_all = timed(all_active, args.profile_kernel)
-    log(f"profiled runs: headline with frozen-run events {ms_fz:.2f} ms, all-active with "
-        f"{args.profile_kernel} events {ms_pk:.2f} ms")
-    kernels = {} if args.no_kernel_table else kernel_table(cfg, K, T, lambda c: timed(all_active, c)[1])
+    log(f"profiled runs: headline with frozen-run events {np.median(ms_fz):.2f} ms, all-active with "
+        f"{args.profile_kernel} events {np.median(ms_pk):.2f} ms per trajectory")
+    kernels = {} if args.no_kernel_table else kernel_table(cfg, n_traj, T, lambda c: timed(all_active, c)[1])
+
+    def deviation():
+        """Output deviation of the trajectory just run from the all-active one: the synthetic
+        stand-in for the quality metrics (relative L2 and max-abs errors of the final state)."""
+        d = (z - z_full).double()
+        return {"rel_l2": float(d.norm() / z_full.double().norm()),
+                "rel_max": float(d.abs().max() / z_full.double().abs().max())}
+
     tau_res = {}
     for t, sch in tau_scheds.items():
-        ms, _ = timed(sch)
-        tau_res[t] = ms
-        log(f"tau {t:g}: {sch.layer_steps} layer-steps, {K} steps in {ms:.2f} ms -> {K * 1000.0 / ms:.2f} steps/s")
+        times, _ = timed(sch)
+        tau_res[t] = (times, deviation())
+        log(f"tau {t:g}: {sch.layer_steps} layer-steps -> {rate(times):.2f} steps/s")
+    rule_res = {}
+    dev_head = None
+    if rule_scheds:
+        timed(scheds[head])
+        dev_head = deviation()
+    for r, sch in rule_scheds.items():
+        times, _ = timed(sch)
+        rule_res[r] = (times, deviation())
+        log(f"rule {r}: lifetimes {sch.lifetimes.tolist()} -> {rate(times):.2f} steps/s, "
+            f"deviation {rule_res[r][1]['rel_l2']:.3e} (method {dev_head['rel_l2']:.3e})")
 
-    ms_head, prof_head = results[head]
-    value = K * 1000.0 / ms_head
-    all_rate = K * 1000.0 / ms_all
+    value = rate(results[head])
+    head_ms = float(np.median(results[head]))
 
     # roofline of the dominant kernel, from the all-active run (largest launch count)
     fl = unit_flops(cfg)
@@ -226,10 +272,14 @@ def main() -> int:
                 "avg_launch_us": kavg * 1e6, "launches": kn,
                 "flop_per_launch": fl.get(kern, 0.0)}
 
-    # frozen path: algorithmic bytes of every frozen-run launch of the timed steps / their time
+    # the mask rows actually timed: n_traj whole trajectories of the headline schedule
     act = np.asarray(scheds[head].active, bool)
-    fbytes = sum(sum(frozen_launch_bytes(cfg, act[(i % T)])) for i in range(K))
-    fms, fn = prof_head if prof_head else (0.0, 0)
+    timed_rows = np.concatenate([act] * n_traj)
+    active_frac = float(timed_rows.mean())
+    mean_active = float(timed_rows.sum(axis=1).mean())
+    # frozen path: algorithmic bytes of every frozen-run launch of the timed steps / their time
+    fbytes = sum(sum(frozen_launch_bytes(cfg, row)) for row in timed_rows)
+    fms, fn = prof_fz if prof_fz else (0.0, 0)
     frozen = None
     if fn:
         frozen = {"bound": "hbm", "kernel": "frozen_run", "achieved": fbytes / (fms / 1000.0) / 1e9,
@@ -249,7 +299,7 @@ def main() -> int:
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, weights, inputs, scheds[head], args.cpu_seconds)
+        cpu = cpu_baseline(cfg, weights, inputs, mean_active, args.cpu_seconds)
 
     lay = {pct: scheds[pct].layer_steps for pct in budgets}
     line = {
@@ -257,9 +307,11 @@ def main() -> int:
         "value": round(value, 3),
         "unit": "steps/s",
         "n_gpus": 1,
-        "steps": K,
+        "steps": n_traj * T,
+        "steps_requested": K,
+        "trajectories": n_traj,
         "warmup": W,
-        "ms_per_step": round(ms_head / K, 4),
+        "ms_per_step": round(head_ms / T, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -270,12 +322,20 @@ def main() -> int:
                    "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "single GPU"},
         "all_active_steps_per_s": round(all_rate, 3),
         "speedup_vs_all_active": round(value / all_rate, 4),
-        "skipped_layer_step_fraction": round(1 - lay[head] / (L * T), 4),
-        "budgets": {str(p): {"steps_per_s": round(K * 1000.0 / results[p][0], 3), "layer_steps": lay[p],
-                             "speedup": round((K * 1000.0 / results[p][0]) / all_rate, 4)} for p in budgets},
-        "tau": {f"{t:g}": {"steps_per_s": round(K * 1000.0 / ms, 3), "layer_steps": tau_scheds[t].layer_steps,
+        "skipped_layer_step_fraction": round(1 - active_frac, 4),
+        "ideal_speedup": round(1 / active_frac, 4),
+        "budgets": {str(p): {"steps_per_s": round(rate(results[p]), 3), "layer_steps": lay[p],
+                             "speedup": round(rate(results[p]) / all_rate, 4),
+                             "traj_ms": [round(t, 3) for t in results[p]]} for p in budgets},
+        "all_active_traj_ms": [round(t, 3) for t in t_all],
+        "tau": {f"{t:g}": {"steps_per_s": round(rate(tm), 3), "layer_steps": tau_scheds[t].layer_steps,
                            "frac_layer_steps": round(tau_scheds[t].layer_steps / (L * T), 4),
-                           "speedup": round((K * 1000.0 / ms) / all_rate, 4)} for t, ms in tau_res.items()},
+                           "speedup": round(rate(tm) / all_rate, 4), "deviation": dv}
+                for t, (tm, dv) in tau_res.items()},
+        "rules": {"budget_pct": head, "scr_frob": {"steps_per_s": round(value, 3), "deviation": dev_head},
+                  **{r: {"steps_per_s": round(rate(tm), 3), "speedup": round(rate(tm) / all_rate, 4),
+                         "layer_steps": rule_scheds[r].layer_steps, "deviation": dv}
+                     for r, (tm, dv) in rule_res.items()}},
         "roofline": roofline,
         "kernels": kernels,
         "frozen_path": frozen,
@@ -286,7 +346,7 @@ def main() -> int:
     return 0
 
 
-def kernel_table(cfg, K, T, profile) -> dict:
+def kernel_table(cfg, n_traj, T, profile) -> dict:
     """Average launch duration of every kernel class of the all-active step (HIP events around
     each launch on the step's stream, one timed pass per class) with its algorithmic work:
     FLOP against the MFMA peak of the workload's dtype, bytes against HBM for the norms."""
@@ -314,7 +374,7 @@ def kernel_table(cfg, K, T, profile) -> dict:
                         "frac_hbm": round(nbytes * n / (ms / 1000.0) / PEAK_HBM, 4)})
         elif c == "gemm_x":
             # cross q / o projections every step, context k / v once per trajectory and unit
-            n_ctx = cfg.L * ((K + T - 1) // T)
+            n_ctx = cfg.L * n_traj
             total = (n - n_ctx) * 2.0 * M * d * d + n_ctx * 2.0 * B * cfg.ctx_len * 2 * d * cfg.ctx_dim
             rec.update({"TFLOP/s": round(total / (ms / 1000.0) / 1e12, 1),
                         "frac_peak": round(total / (ms / 1000.0) / peak, 4)})
@@ -325,12 +385,13 @@ def kernel_table(cfg, K, T, profile) -> dict:
     return out
 
 
-def cpu_baseline(cfg, weights, inputs, sched, seconds):
+def cpu_baseline(cfg, weights, inputs, mean_active, seconds):
     """Oracle (numpy float64) on a bounded sample: units of one all-active step, in stack order,
     until `seconds` have passed (at least two units, at most the whole stack).
 
-    Scaled to steps/s of the scheduled trajectory: the oracle's time per step is its time per
-    active unit times the mean active units per step (frozen units cost an addition each).
+    Scaled to steps/s of the timed scheduled trajectories: the oracle's time per step is its
+    time per active unit times the mean active units per timed step (frozen units cost an
+    addition each).
     """
     import dataclasses
 
@@ -351,7 +412,6 @@ def cpu_baseline(cfg, weights, inputs, sched, seconds):
         n += 1
     dt = time.time() - t0
     per_unit = dt / n
-    mean_active = float(np.asarray(sched.active, np.float64).sum(axis=1).mean())
     per_step = per_unit * mean_active
     log(f"cpu baseline: {n} units in {dt:.1f}s, {per_unit:.2f}s per active unit -> {per_step:.1f}s per scheduled step")
     return {"value": round(1.0 / per_step, 6), "unit": "steps/s", "cores": threads, "kind": "oracle",

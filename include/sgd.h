@@ -23,9 +23,7 @@
  *     returns a thread-local description of the last failure.
  *   - "Device pointer" means memory of the current HIP device.  The caller
  *     owns every buffer (weights, state, cache, workspace); handles only
- *     borrow pointers and never allocate or free device memory, with one
- *     exception: sgd_schedule_build and sgd_matrix_stats allocate and free a
- *     temporary fp64 Gram matrix (offline work).
+ *     borrow pointers and never allocate or free device memory.
  *   - Weight matrices are row-major [out, in] (y = x W^T), dtype SGD_F32 or
  *     SGD_BF16.  Norm gains/shifts, biases, class embeddings: fp32.
  *   - Calls that take a hip_stream enqueue on it and return without a host
@@ -94,31 +92,65 @@ typedef struct {
     int32_t head_dim;
 } sgd_unit;
 
-/* Schedule parameters.
+/* Ranking rule of a schedule: the unit score that Eq. schedule maps to lifetimes.
+ * SGD_RULE_SCR_FROB is the method (Alg. 1: g(W) = ||W||_F sqrt(rho(SCR_eta)), Eq.
+ * app-matrix-score).  The others are the static baselines of Sec. "Static ranking
+ * comparisons" (Table "Static rankings at matched layer-step budgets"), built at the same
+ * budget reading.  A matrix rule replaces g(W) by its own statistic gamma(W) inside Eqs.
+ * app-attn-score, app-xattn-score, app-mlp-score and app-conv-score, so a unit keeps the
+ * same component structure:
+ *   SGD_RULE_FROB         gamma = ||W||_F
+ *   SGD_RULE_SPECTRAL     gamma = ||W||_2 (largest singular value)
+ *   SGD_RULE_STABLE_RANK  gamma = ||W||_2^2 / ||W||_F^2, the stable rank oriented like SCR
+ *                         (a concentrated spectrum ranks high; the raw stable rank ranks the
+ *                         other way round)
+ *   SGD_RULE_FROB_SRANK   gamma = ||W||_F ||W||_2^2 / ||W||_F^2
+ *   SGD_RULE_RAW_SCR      gamma = sqrt(rho(SCR_eta)), i.e. g(W) without ||W||_F
+ * Unit rules need no spectra (units may be NULL):
+ *   SGD_RULE_DEPTH        raw score l + 1 (deeper units live longer)
+ *   SGD_RULE_RANDOM       raw score of unit l = the (l+1)-th output of SplitMix64 (Steele,
+ *                         Lea and Flood, 2014) seeded with `seed`, as (x >> 11) * 2^-53
+ * Every rule's raw scores are normalised by Eq. app-score-normalization. */
+enum sgd_rule {
+    SGD_RULE_SCR_FROB = 0, SGD_RULE_RANDOM = 1, SGD_RULE_DEPTH = 2, SGD_RULE_FROB = 3,
+    SGD_RULE_SPECTRAL = 4, SGD_RULE_STABLE_RANK = 5, SGD_RULE_FROB_SRANK = 6, SGD_RULE_RAW_SCR = 7,
+    SGD_RULE_COUNT = 8
+};
+
+/* Schedule parameters (Alg. 1 inputs: T, tau, S_min; plus the budget reading).
  *   T                  horizon (denoising steps), >= 1
- *   budget_layer_steps N* >= 0 selects budget mode (Eq. schedule swept over tau, filled to
- *                      exactly N*; increments granted in increasing key j / Lambda_hat_l,
- *                      ties to the lower unit index, then the lower j); -1 selects tau mode
- *   tau                scale of Eq. schedule (tau mode only), > 0
- *   s_min              minimum lifetime, 1..T
- *   eta                regulariser of Eq. scr-reg, >= 0                                     */
+ *   budget_layer_steps N* >= 0 selects budget mode: Eq. schedule swept over tau, filled to
+ *                      exactly N* (increments granted in increasing key j / Lambda_hat_l,
+ *                      ties to the lower unit index, then the lower j)
+ *   budget_pct         used when budget_layer_steps < 0 and budget_pct > 0: budget mode with
+ *                      N* = floor(budget_pct * L * T / 100) (sgd_budget_layer_steps)
+ *   tau                scale of Eq. schedule, > 0; tau mode when neither budget is given
+ *   s_min              minimum lifetime S_min, 1..T; <= 0 selects ceil(T / 10), the smallest
+ *                      integer lifetime of at least a tenth of the horizon (sgd_s_min_default)
+ *   eta                regulariser of Eq. scr-reg, >= 0
+ *   rule               an sgd_rule value; SGD_RULE_SCR_FROB is the method
+ *   seed               SGD_RULE_RANDOM only                                                   */
 typedef struct {
     int32_t T;
     int32_t budget_layer_steps;
     double tau;
     int32_t s_min;
     double eta;
+    int32_t budget_pct;
+    int32_t rule;
+    uint64_t seed;
 } sgd_sched_params;
 
 /* Output of the schedule calls.  The caller allocates every array on the host; optional
  * arrays may be NULL.  L and T are filled in by the library.
  *   lifetimes  [L]      S_l
  *   active     [T*L]    active[(s-1)*L + l] = (s <= S_l)
- *   unit_raw   [L]      raw unit score q~_l                    (optional)
+ *   unit_raw   [L]      raw unit score q~_l of the rule        (optional)
  *   unit_score [L]      Lambda_hat_l                           (optional)
- *   mat_stats  [5*n]    per matrix, in input order: E_k, tail energy, ||W||_F^2,
- *                       SCR_eta, g(W)                          (optional)
+ *   mat_stats  [6*n]    per matrix, in input order: E_k, tail energy, ||W||_F^2,
+ *                       SCR_eta, g(W), ||W||_2^2               (optional)
  *   layer_steps         sum_l S_l
+ *   s_min               the S_min used
  *   cut_margin          budget mode: (kappa_next - kappa_last) / kappa_last between the
  *                       first refused and the last granted increment (+inf if none)     */
 typedef struct {
@@ -130,23 +162,49 @@ typedef struct {
     double* mat_stats;
     int64_t layer_steps;
     double cut_margin;
+    int32_t s_min;
 } sgd_schedule;
+
+/* Integer arithmetic of the schedule's readings, exported so that callers hold none:
+ * the default minimum lifetime ceil(T / 10) for T >= 1 (0 otherwise), and the layer-step
+ * ceiling N* = floor(pct * L * T / 100) of a percentage budget (SGD_E_ARG unless
+ * 0 <= pct <= 100, L >= 1, T >= 1). */
+int32_t sgd_s_min_default(int32_t T);
+int sgd_budget_layer_steps(int32_t pct, int32_t L, int32_t T, int64_t* n_star);
+
+/* Device scratch that sgd_schedule_build / sgd_matrix_stats need for `workers` concurrent
+ * matrices (fp64 Gram of the short side plus tridiagonal work arrays per worker), for the
+ * largest scored matrix of `units`.  The caller allocates it (256-byte aligned) and passes
+ * it in; the library allocates no device memory. */
+int sgd_schedule_workspace_bytes(const sgd_unit* units, int32_t L, int32_t workers, size_t* bytes);
 
 /* Alg. 1: score every matrix of every unit on the GPU (fp64 Gram of the short side,
  * Householder tridiagonalisation, host implicit-QL eigenvalues), then set lifetimes.
- * Offline, once per model: up to 16 host worker threads, each with its own stream and a
- * temporary fp64 device workspace (allocated here and freed before returning; the step
- * path allocates nothing).  Synchronises hip_stream before returning.  Errors: SGD_E_ARG,
- * SGD_E_DTYPE, SGD_E_BUDGET, SGD_E_NUMERIC, SGD_E_HIP. */
-int sgd_schedule_build(const sgd_unit* units, int32_t L, const sgd_sched_params* params,
-                       void* hip_stream, sgd_schedule* out);
+ * Offline, once per model.  As many matrices are scored at once as the workspace holds
+ * worker slots (at most 16, each with its own host thread and stream); the workspace must
+ * hold at least one.  units may be NULL for SGD_RULE_DEPTH and SGD_RULE_RANDOM (then L
+ * alone sizes the schedule and nothing runs on the GPU).  Synchronises hip_stream before
+ * returning.  Errors: SGD_E_ARG, SGD_E_DTYPE, SGD_E_BUDGET, SGD_E_NUMERIC, SGD_E_HIP. */
+int sgd_schedule_build(const sgd_unit* units, int32_t L, const sgd_sched_params* params, void* workspace,
+                       size_t workspace_bytes, void* hip_stream, sgd_schedule* out);
 
-/* Statistics of one matrix (Eq. scr-reg, Eq. app-matrix-score): out[5] =
- * {E_k, tail energy, ||W||_F^2, SCR_eta, g}.  Synchronises hip_stream. */
-int sgd_matrix_stats(const sgd_matrix* m, double eta, void* hip_stream, double out[5]);
+/* Statistics of one matrix (Eq. scr-reg, Eq. app-matrix-score): out[6] =
+ * {E_k, tail energy, ||W||_F^2, SCR_eta, g, ||W||_2^2}.  workspace as for
+ * sgd_schedule_build with one worker.  Synchronises hip_stream. */
+int sgd_matrix_stats(const sgd_matrix* m, double eta, void* workspace, size_t workspace_bytes, void* hip_stream,
+                     double out[6]);
+
+/* Host only: the rule's schedule from matrix statistics already computed, e.g. the mat_stats
+ * of an earlier sgd_schedule_build (to rank the same model by several rules, or at other
+ * budgets, without recomputing spectra).  units gives each matrix's role and the head
+ * dimension (matrix pointers are not read); mat_stats holds 6 doubles per matrix in the
+ * order of units, as sgd_schedule_build writes them.  out->mat_stats is left untouched. */
+int sgd_schedule_from_stats(const sgd_unit* units, int32_t L, const double* mat_stats,
+                            const sgd_sched_params* params, sgd_schedule* out);
 
 /* Host only: lifetimes from given normalised scores Lambda_hat_l in [0, 1] (Eq. schedule
- * and the budget reading above).  unit_raw / mat_stats of out are left untouched. */
+ * and the budget reading above; params->rule and seed are ignored).  unit_raw / mat_stats
+ * of out are left untouched. */
 int sgd_schedule_from_scores(const double* unit_score, int32_t L, const sgd_sched_params* params,
                              sgd_schedule* out);
 

@@ -21,6 +21,8 @@ Modules
               the deterministic sampler update (Sec. 3.1).
 ``numerics``  bfloat16 decode/rounding used to emulate the GPU's storage
               points.
+``rules``     The static ranking baselines at a matched budget (Sec. "Static
+              ranking comparisons").
 
 Parity status
 -------------

@@ -291,19 +291,25 @@ def initial_stream(model: Model, z: np.ndarray, s: int) -> np.ndarray:
 
 
 def denoise_step(model: Model, z: np.ndarray, s: int, active: Optional[Sequence[int]],
-                 cache: Dict[int, np.ndarray], cross=None) -> np.ndarray:
+                 cache: Dict[int, np.ndarray], cross=None,
+                 unit_inputs: Optional[Dict[int, np.ndarray]] = None) -> np.ndarray:
     """One network evaluation at step s (Alg. 2).  Returns eps = h_L.
 
     ``active=None`` is the unscheduled forward (every unit computes, cache untouched).
     ``cross`` (SDXL) holds each unit's step-invariant context keys and values.
     An active unit refreshes ``cache[l]`` with its update (Alg. 2 refreshes at every
-    active step; the entry read later is the one from the last active step S_l).
+    active step; the entry read later is the one from the last active step, S_l for a
+    static schedule).  The active set need not be nested in s (the input-aware baselines).
+    ``unit_inputs``, if given, receives each unit's input h_{l-1,s}: the residual stream
+    arriving at unit l (for a U-ViT out-block, before its skip linear).
     """
     cfg = model.cfg
     t = timestep_value(s, cfg.T)
     h = initial_stream(model, z, s)
     skips: Dict[int, np.ndarray] = {}
     for l in range(cfg.L):
+        if unit_inputs is not None:
+            unit_inputs[l] = h.copy()
         src = model.skip_source(l)
         if src >= 0:
             h = model.skip_linear(model.units[l], h, skips[src])

@@ -60,6 +60,8 @@ class MatrixStats:
     frob_sq: float      # ||W||_F^2 = sum_ij W_ij^2
     scr: float          # SCR_eta (Eq. scr-reg)
     g: float            # ||W||_F sqrt(rho(SCR_eta))  (Eq. app-matrix-score)
+    sigma1_sq: float = 0.0  # largest squared singular value ||W||_2^2 (spectral-norm and
+                            # stable-rank rankings of Sec. "Static ranking comparisons")
 
 
 def matrix_stats(w64: np.ndarray, eta: float = DEFAULT_ETA) -> MatrixStats:
@@ -81,7 +83,7 @@ def matrix_stats(w64: np.ndarray, eta: float = DEFAULT_ETA) -> MatrixStats:
     scr = math.log(a / b) if b > 0 else math.inf
     rho = a / (a + b) if (a + b) > 0 else 0.0
     g = math.sqrt(frob_sq) * math.sqrt(rho)
-    return MatrixStats(m, n, k, e_top, e_tail, frob_sq, scr, g)
+    return MatrixStats(m, n, k, e_top, e_tail, frob_sq, scr, g, float(lam[0]))
 
 
 def rho_of(u: float) -> float:

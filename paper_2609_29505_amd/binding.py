@@ -6,7 +6,6 @@ Every computation runs in ``libsgd.so``.  Torch tensors supply device buffers
 from __future__ import annotations
 
 import ctypes as C
-import math
 import os
 from typing import Dict, List, Optional, Sequence
 
@@ -17,6 +16,8 @@ lib_path = os.path.join(_PKG, "lib", "libsgd.so")
 
 SGD_F32, SGD_BF16 = 0, 1
 SGD_ARCH = {"tiny": 0, "llada": 1, "dit": 2, "uvit": 3, "sdxl": 4}
+SGD_RULE = {"scr_frob": 0, "random": 1, "depth": 2, "frob": 3, "spectral": 4, "stable_rank": 5,
+            "frob_srank": 6, "raw_scr": 7}
 SGD_ROLE = {"q": 0, "k": 1, "v": 2, "o": 3, "xq": 4, "xk": 5, "xv": 6, "xo": 7, "w1": 8, "w2": 9, "conv": 10}
 SGD_K = {"norm": 0, "gemm_qkv": 1, "attn": 2, "gemm_o": 3, "gemm_w1": 4, "gemm_w2": 5, "frozen": 6,
          "state": 7, "cond": 8, "gemm_skip": 9, "gemm_x": 10, "attn_x": 11}
@@ -43,14 +44,15 @@ class sgd_unit(C.Structure):
 
 class sgd_sched_params(C.Structure):
     _fields_ = [("T", C.c_int32), ("budget_layer_steps", C.c_int32), ("tau", C.c_double),
-                ("s_min", C.c_int32), ("eta", C.c_double)]
+                ("s_min", C.c_int32), ("eta", C.c_double), ("budget_pct", C.c_int32), ("rule", C.c_int32),
+                ("seed", C.c_uint64)]
 
 
 class sgd_schedule(C.Structure):
     _fields_ = [("L", C.c_int32), ("T", C.c_int32), ("lifetimes", C.POINTER(C.c_int32)),
                 ("active", C.POINTER(C.c_uint8)), ("unit_raw", C.POINTER(C.c_double)),
                 ("unit_score", C.POINTER(C.c_double)), ("mat_stats", C.POINTER(C.c_double)),
-                ("layer_steps", C.c_int64), ("cut_margin", C.c_double)]
+                ("layer_steps", C.c_int64), ("cut_margin", C.c_double), ("s_min", C.c_int32)]
 
 
 _W_FIELDS = ["norm1_w", "norm1_b", "w_qkv", "b_qkv", "w_o", "b_o", "norm2_w", "norm2_b", "w1", "b1", "w2", "b2",
@@ -78,11 +80,13 @@ class sgd_step_args(C.Structure):
 
 _lib = None
 
-EXPORTS = ["sgd_last_error", "sgd_version", "sgd_schedule_build", "sgd_matrix_stats", "sgd_schedule_from_scores",
+EXPORTS = ["sgd_last_error", "sgd_version", "sgd_s_min_default", "sgd_budget_layer_steps",
+           "sgd_schedule_workspace_bytes", "sgd_schedule_build", "sgd_matrix_stats", "sgd_schedule_from_scores",
+           "sgd_schedule_from_stats",
            "sgd_schedule_from_lifetimes", "sgd_model_create", "sgd_model_destroy", "sgd_workspace_bytes",
            "sgd_cache_bytes", "sgd_cache_bind", "sgd_cache_reset", "sgd_cache_destroy", "sgd_denoise_step",
            "sgd_profile_begin", "sgd_profile_end", "sgd_op_linear", "sgd_op_attention", "sgd_op_norm",
-           "sgd_op_frozen_run", "sgd_op_heads", "sgd_op_residual"]
+           "sgd_op_frozen_run", "sgd_op_heads", "sgd_op_residual", "sgd_op_adaln_mod"]
 
 
 def lib() -> C.CDLL:
@@ -96,9 +100,14 @@ def lib() -> C.CDLL:
         vp, i32, i64 = C.c_void_p, C.c_int32, C.c_int64
         sig = {
             "sgd_version": [],
-            "sgd_schedule_build": [C.POINTER(sgd_unit), i32, C.POINTER(sgd_sched_params), vp, C.POINTER(sgd_schedule)],
-            "sgd_matrix_stats": [C.POINTER(sgd_matrix), C.c_double, vp, C.POINTER(C.c_double)],
+            "sgd_budget_layer_steps": [i32, i32, i32, C.POINTER(i64)],
+            "sgd_schedule_workspace_bytes": [C.POINTER(sgd_unit), i32, i32, C.POINTER(C.c_size_t)],
+            "sgd_schedule_build": [C.POINTER(sgd_unit), i32, C.POINTER(sgd_sched_params), vp, C.c_size_t, vp,
+                                   C.POINTER(sgd_schedule)],
+            "sgd_matrix_stats": [C.POINTER(sgd_matrix), C.c_double, vp, C.c_size_t, vp, C.POINTER(C.c_double)],
             "sgd_schedule_from_scores": [C.POINTER(C.c_double), i32, C.POINTER(sgd_sched_params), C.POINTER(sgd_schedule)],
+            "sgd_schedule_from_stats": [C.POINTER(sgd_unit), i32, C.POINTER(C.c_double), C.POINTER(sgd_sched_params),
+                                        C.POINTER(sgd_schedule)],
             "sgd_schedule_from_lifetimes": [i32, i32, C.POINTER(C.c_int32), C.POINTER(sgd_schedule)],
             "sgd_model_create": [C.POINTER(sgd_model_desc), C.POINTER(vp)],
             "sgd_model_destroy": [vp],
@@ -122,6 +131,8 @@ def lib() -> C.CDLL:
             f = getattr(L, name)
             f.argtypes = args
             f.restype = C.c_int
+        L.sgd_s_min_default.argtypes = [i32]
+        L.sgd_s_min_default.restype = C.c_int32
         _lib = L
     return _lib
 
@@ -132,13 +143,15 @@ def _check(rc: int) -> None:
 
 
 def s_min_default(T: int) -> int:
-    """ceil(T / 10): smallest integer lifetime covering a tenth of the horizon."""
-    return (T + 9) // 10
+    """The library's default minimum lifetime (sgd_s_min_default)."""
+    return int(lib().sgd_s_min_default(T))
 
 
 def budget_layer_steps(pct: int, L: int, T: int) -> int:
-    """Integer layer-step ceiling floor(pct * L * T / 100)."""
-    return (pct * L * T) // 100
+    """The library's layer-step ceiling of a percentage budget (sgd_budget_layer_steps)."""
+    n = C.c_int64()
+    _check(lib().sgd_budget_layer_steps(pct, L, T, C.byref(n)))
+    return int(n.value)
 
 
 # ------------------------------------------------------------------ schedule
@@ -151,7 +164,7 @@ class Schedule:
         self.active = np.zeros((T, L), np.uint8)
         self.unit_raw = np.zeros(L, np.float64)
         self.unit_score = np.zeros(L, np.float64)
-        self.mat_stats = np.zeros((max(n_mats, 1), 5), np.float64)
+        self.mat_stats = np.zeros((max(n_mats, 1), 6), np.float64)
         self.c = sgd_schedule()
         self.c.L, self.c.T = L, T
         self.c.lifetimes = self.lifetimes.ctypes.data_as(C.POINTER(C.c_int32))
@@ -168,14 +181,23 @@ class Schedule:
     def cut_margin(self) -> float:
         return float(self.c.cut_margin)
 
+    @property
+    def s_min(self) -> int:
+        return int(self.c.s_min)
 
-def _params(T, budget=None, tau=1.0, s_min=None, eta=1e-6):
+
+def _params(T, budget=None, tau=1.0, s_min=None, eta=1e-6, budget_pct=None, rule="scr_frob", seed=0):
+    """budget: N* layer-steps; budget_pct: a percentage the library turns into N*; neither:
+    tau mode.  s_min None: the library's default."""
     p = sgd_sched_params()
     p.T = T
     p.budget_layer_steps = -1 if budget is None else int(budget)
+    p.budget_pct = 0 if budget_pct is None else int(budget_pct)
     p.tau = tau
-    p.s_min = s_min_default(T) if s_min is None else s_min
+    p.s_min = 0 if s_min is None else s_min
     p.eta = eta
+    p.rule = SGD_RULE[rule]
+    p.seed = seed
     return p
 
 
@@ -194,9 +216,21 @@ def _dtype_code(t) -> int:
     raise ValueError(f"unsupported dtype {t.dtype}")
 
 
-def schedule_build(units: Sequence[Sequence[tuple]], head_dims: Sequence[int], T: int, budget=None, tau=1.0,
-                   s_min=None, eta=1e-6, stream=None) -> Schedule:
-    """``units[l]`` is a list of ``(role, tensor)`` pairs (2-D device tensors, bf16 or fp32)."""
+def _workspace(nbytes: int):
+    import torch
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device="cuda")
+
+
+def schedule_build(units: Optional[Sequence[Sequence[tuple]]], head_dims: Optional[Sequence[int]], T: int,
+                   budget=None, tau=1.0, s_min=None, eta=1e-6, budget_pct=None, rule="scr_frob", seed=0,
+                   workers=16, L=None, stream=None) -> Schedule:
+    """``units[l]`` is a list of ``(role, tensor)`` pairs (2-D device tensors, bf16 or fp32).
+    ``units`` may be None for the depth and random rules (then ``L`` gives the unit count)."""
+    if units is None:
+        sch = Schedule(L, T)
+        p = _params(T, budget, tau, s_min, eta, budget_pct, rule, seed)
+        _check(lib().sgd_schedule_build(None, L, C.byref(p), None, 0, None, C.byref(sch.c)))
+        return sch
     L = len(units)
     mats_keep = []
     cunits = (sgd_unit * L)()
@@ -215,28 +249,67 @@ def schedule_build(units: Sequence[Sequence[tuple]], head_dims: Sequence[int], T
         cunits[l].head_dim = int(head_dims[l])
         n_total += len(mats)
     sch = Schedule(L, T, n_total)
-    p = _params(T, budget, tau, s_min, eta)
-    _check(lib().sgd_schedule_build(cunits, L, C.byref(p), C.c_void_p(_stream_ptr(stream)), C.byref(sch.c)))
+    p = _params(T, budget, tau, s_min, eta, budget_pct, rule, seed)
+    nb = C.c_size_t()
+    _check(lib().sgd_schedule_workspace_bytes(cunits, L, workers, C.byref(nb)))
+    ws = _workspace(nb.value)
+    _check(lib().sgd_schedule_build(cunits, L, C.byref(p), C.c_void_p(ws.data_ptr()), ws.numel(),
+                                    C.c_void_p(_stream_ptr(stream)), C.byref(sch.c)))
+    del ws
     return sch
 
 
 def matrix_stats(t, eta=1e-6, role="w1", stream=None) -> np.ndarray:
+    """{E_k, tail energy, ||W||_F^2, SCR_eta, g, ||W||_2^2} of one device matrix."""
     m = sgd_matrix()
     m.ptr = t.data_ptr()
     m.rows, m.cols = t.shape
     m.dtype = _dtype_code(t)
     m.role = SGD_ROLE[role]
-    out = (C.c_double * 5)()
-    _check(lib().sgd_matrix_stats(C.byref(m), eta, C.c_void_p(_stream_ptr(stream)), out))
+    u = sgd_unit()
+    u.mats = C.pointer(m)
+    u.n_mats = 1
+    u.head_dim = 1
+    nb = C.c_size_t()
+    _check(lib().sgd_schedule_workspace_bytes(C.byref(u), 1, 1, C.byref(nb)))
+    ws = _workspace(nb.value)
+    out = (C.c_double * 6)()
+    _check(lib().sgd_matrix_stats(C.byref(m), eta, C.c_void_p(ws.data_ptr()), ws.numel(),
+                                  C.c_void_p(_stream_ptr(stream)), out))
     return np.array(list(out))
 
 
-def schedule_from_scores(scores: Sequence[float], T: int, budget=None, tau=1.0, s_min=None) -> Schedule:
+def schedule_from_scores(scores: Sequence[float], T: int, budget=None, tau=1.0, s_min=None,
+                         budget_pct=None) -> Schedule:
     sc = np.ascontiguousarray(scores, dtype=np.float64)
     sch = Schedule(len(sc), T)
-    p = _params(T, budget, tau, s_min)
+    p = _params(T, budget, tau, s_min, budget_pct=budget_pct)
     _check(lib().sgd_schedule_from_scores(sc.ctypes.data_as(C.POINTER(C.c_double)), len(sc), C.byref(p),
                                           C.byref(sch.c)))
+    return sch
+
+
+def schedule_from_stats(roles: Sequence[Sequence[str]], head_dims: Sequence[int], mat_stats, T: int, budget=None,
+                        tau=1.0, s_min=None, eta=1e-6, budget_pct=None, rule="scr_frob", seed=0) -> Schedule:
+    """A rule's schedule from per-matrix statistics (``mat_stats`` [n, 6], the rows an earlier
+    ``schedule_build`` returned); ``roles[l]`` lists unit l's matrix roles in that order."""
+    L = len(roles)
+    st = np.ascontiguousarray(mat_stats, dtype=np.float64)
+    keep = []
+    cunits = (sgd_unit * L)()
+    for l, rl in enumerate(roles):
+        arr = (sgd_matrix * len(rl))()
+        for i, r in enumerate(rl):
+            arr[i].role = SGD_ROLE[r]
+        keep.append(arr)
+        cunits[l].mats = C.cast(arr, C.POINTER(sgd_matrix))
+        cunits[l].n_mats = len(rl)
+        cunits[l].head_dim = int(head_dims[l])
+    assert st.shape == (sum(len(r) for r in roles), 6)
+    sch = Schedule(L, T)
+    p = _params(T, budget, tau, s_min, eta, budget_pct, rule, seed)
+    _check(lib().sgd_schedule_from_stats(cunits, L, st.ctypes.data_as(C.POINTER(C.c_double)), C.byref(p),
+                                         C.byref(sch.c)))
     return sch
 
 

@@ -86,7 +86,7 @@ static bool tridiag_eigenvalues(std::vector<double>& a, std::vector<double>& b) 
 }
 
 struct MatStats {
-    double e_top = 0, e_tail = 0, frob = 0, scr = 0, g = 0;
+    double e_top = 0, e_tail = 0, frob = 0, scr = 0, g = 0, sigma1_sq = 0;
 };
 
 static int rank_k(long m, long n) {
@@ -104,6 +104,7 @@ static MatStats stats_from_eigs(std::vector<double>& lam, double frob, int k, do
     s.scr = B > 0 ? std::log(A / B) : std::numeric_limits<double>::infinity();
     const double rho = (A + B) > 0 ? A / (A + B) : 0.0;
     s.g = std::sqrt(frob) * std::sqrt(rho);
+    s.sigma1_sq = lam.empty() ? 0.0 : lam[0];
     return s;
 }
 
@@ -123,19 +124,29 @@ static int validate_matrix(const sgd_matrix* m) {
     return SGD_OK;
 }
 
-// Score every job with a pool of host workers, each driving its own stream.
-static int run_stats(std::vector<MatJob>& jobs, double eta, hipStream_t user_stream) {
+// Device doubles one worker needs for matrices whose short side is at most n: the Gram
+// matrix, the diagonal, the off-diagonal, the Householder work array and the Gram's
+// diagonal (for ||W||_F^2), each rounded up to 256 bytes.
+static size_t worker_bytes(long n) {
+    auto a = [](size_t b) { return (b + 255) & ~(size_t)255; };
+    return a((size_t)n * n * 8) + 3 * a((size_t)n * 8) + a((size_t)(5 * n + 8) * 8);
+}
+
+// Score every job with a pool of host workers, each driving its own stream and one slot of
+// the caller's workspace.
+static int run_stats(std::vector<MatJob>& jobs, double eta, char* ws, size_t ws_bytes, hipStream_t user_stream) {
     if (jobs.empty()) return SGD_OK;
     int dev = 0;
     SGD_HIP_TRY(hipGetDevice(&dev));
     SGD_HIP_TRY(hipStreamSynchronize(user_stream));
     long nmax = 0;
     for (auto& j : jobs) nmax = std::max(nmax, std::min(j.m->rows, j.m->cols));
+    const size_t per = worker_bytes(nmax);
+    if (!ws || ws_bytes < per) return fail(SGD_E_ARG, "schedule workspace smaller than one worker slot");
+    if ((uintptr_t)ws % 256) return fail(SGD_E_ARG, "schedule workspace must be 256-byte aligned");
     unsigned hc = std::thread::hardware_concurrency();
     int nw = (int)std::min<size_t>(jobs.size(), std::max(1u, std::min(hc ? hc : 1u, 16u)));
-    // keep the Gram buffers within a few GB
-    const double gbytes = (double)nmax * nmax * 8.0;
-    while (nw > 1 && gbytes * nw > 4.0e9) --nw;
+    nw = (int)std::min<size_t>(nw, ws_bytes / per);
 
     std::atomic<size_t> next{0};
     std::mutex emu;
@@ -145,27 +156,19 @@ static int run_stats(std::vector<MatJob>& jobs, double eta, hipStream_t user_str
         std::lock_guard<std::mutex> lk(emu);
         if (first_err == SGD_OK) { first_err = code; err_msg = msg; }
     };
-    auto worker = [&]() {
+    auto worker = [&](int slot) {
         if (hipSetDevice(dev) != hipSuccess) { record(SGD_E_HIP, "hipSetDevice failed in a worker"); return; }
         hipStream_t st = nullptr;
-        double *G = nullptr, *dg = nullptr, *od = nullptr, *work = nullptr, *trace = nullptr;
-        auto cleanup = [&]() {
-            if (G) (void)hipFree(G);
-            if (dg) (void)hipFree(dg);
-            if (od) (void)hipFree(od);
-            if (work) (void)hipFree(work);
-            if (trace) (void)hipFree(trace);
-            if (st) (void)hipStreamDestroy(st);
-        };
+        auto a = [](size_t b) { return (b + 255) & ~(size_t)255; };
+        char* base = ws + (size_t)slot * per;
+        double* G = (double*)base;
+        double* dg = (double*)(base + a((size_t)nmax * nmax * 8));
+        double* od = (double*)((char*)dg + a((size_t)nmax * 8));
+        double* trace = (double*)((char*)od + a((size_t)nmax * 8));
+        double* work = (double*)((char*)trace + a((size_t)nmax * 8));
         hipError_t e = hipStreamCreateWithFlags(&st, hipStreamNonBlocking);
-        if (e == hipSuccess) e = hipMalloc(&G, (size_t)nmax * nmax * sizeof(double));
-        if (e == hipSuccess) e = hipMalloc(&dg, (size_t)nmax * sizeof(double));
-        if (e == hipSuccess) e = hipMalloc(&od, (size_t)nmax * sizeof(double));
-        if (e == hipSuccess) e = hipMalloc(&work, (size_t)(5 * nmax + 8) * sizeof(double));
-        if (e == hipSuccess) e = hipMalloc(&trace, (size_t)nmax * sizeof(double));
         if (e != hipSuccess) {
-            record(SGD_E_HIP, std::string("spectral workspace: ") + hipGetErrorString(e));
-            cleanup();
+            record(SGD_E_HIP, std::string("worker stream: ") + hipGetErrorString(e));
             return;
         }
         std::vector<double> ha, hb, htr;
@@ -209,10 +212,10 @@ static int run_stats(std::vector<MatJob>& jobs, double eta, hipStream_t user_str
             }
             jobs[i].out = stats_from_eigs(ha, frob, rank_k(m->rows, m->cols), eta);
         }
-        cleanup();
+        (void)hipStreamDestroy(st);
     };
     std::vector<std::thread> th;
-    for (int w = 0; w < nw; ++w) th.emplace_back(worker);
+    for (int w = 0; w < nw; ++w) th.emplace_back(worker, w);
     for (auto& t : th) t.join();
     if (first_err != SGD_OK) return fail(first_err, err_msg);
     return SGD_OK;
@@ -220,16 +223,27 @@ static int run_stats(std::vector<MatJob>& jobs, double eta, hipStream_t user_str
 
 // ---------------------------------------------------------------------------- lifetimes
 
-static int check_params(const sgd_sched_params* p, int L) {
+// The parameters with the library's defaults applied: S_min <= 0 -> ceil(T / 10); a
+// percentage budget -> N* = floor(pct L T / 100).  Validates the result.
+static int resolve_params(const sgd_sched_params* p, int L, sgd_sched_params* r) {
     if (!p) return fail(SGD_E_ARG, "params is NULL");
     if (L < 1) return fail(SGD_E_ARG, "L must be >= 1");
     if (p->T < 1) return fail(SGD_E_ARG, "T must be >= 1");
-    if (p->s_min < 1 || p->s_min > p->T) return fail(SGD_E_ARG, "s_min must lie in 1..T");
-    if (p->budget_layer_steps < 0 && !(p->tau > 0)) return fail(SGD_E_ARG, "tau must be > 0 in tau mode");
-    if (!(p->eta >= 0) || !std::isfinite(p->eta)) return fail(SGD_E_ARG, "eta must be finite and >= 0");
-    if (p->budget_layer_steps >= 0) {
-        const long lo = (long)L * p->s_min, hi = (long)L * p->T;
-        if (p->budget_layer_steps < lo || p->budget_layer_steps > hi)
+    *r = *p;
+    if (r->s_min <= 0) r->s_min = sgd_s_min_default(p->T);
+    if (r->s_min > p->T) return fail(SGD_E_ARG, "s_min must lie in 1..T");
+    if (r->budget_layer_steps < 0 && r->budget_pct > 0) {
+        if (r->budget_pct > 100) return fail(SGD_E_ARG, "budget_pct must lie in 1..100");
+        const int64_t n = (int64_t)r->budget_pct * L * p->T / 100;
+        if (n > INT32_MAX) return fail(SGD_E_ARG, "budget above 2^31 layer-steps");
+        r->budget_layer_steps = (int32_t)n;
+    }
+    if (r->budget_layer_steps < 0 && !(r->tau > 0)) return fail(SGD_E_ARG, "tau must be > 0 in tau mode");
+    if (!(r->eta >= 0) || !std::isfinite(r->eta)) return fail(SGD_E_ARG, "eta must be finite and >= 0");
+    if (r->rule < 0 || r->rule >= SGD_RULE_COUNT) return fail(SGD_E_ARG, "unknown ranking rule");
+    if (r->budget_layer_steps >= 0) {
+        const long lo = (long)L * r->s_min, hi = (long)L * p->T;
+        if (r->budget_layer_steps < lo || r->budget_layer_steps > hi)
             return fail(SGD_E_BUDGET, "budget outside [L*s_min, L*T]");
     }
     return SGD_OK;
@@ -272,21 +286,111 @@ int lifetimes_from_scores(const double* score, int L, const sgd_sched_params* p,
             for (int l = 0; l < L; ++l) out->active[(size_t)(s - 1) * L + l] = (uint8_t)(s <= S[l]);
     out->layer_steps = total;
     out->cut_margin = margin;
+    out->s_min = p->s_min;
     return SGD_OK;
+}
+
+// SplitMix64 (Steele, Lea and Flood, "Fast splittable pseudorandom number generators",
+// OOPSLA 2014): output i of the stream seeded with `seed` mixes seed + i * golden gamma.
+static uint64_t splitmix64(uint64_t seed, uint64_t i) {
+    uint64_t z = seed + i * 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// Matrix statistic of a ranking rule (g(W) for the method).
+static double rule_stat(const MatStats& s, int rule) {
+    switch (rule) {
+        case SGD_RULE_FROB: return std::sqrt(s.frob);
+        case SGD_RULE_SPECTRAL: return std::sqrt(s.sigma1_sq);
+        case SGD_RULE_STABLE_RANK: return s.frob > 0 ? s.sigma1_sq / s.frob : 0.0;
+        case SGD_RULE_FROB_SRANK: return s.frob > 0 ? std::sqrt(s.frob) * (s.sigma1_sq / s.frob) : 0.0;
+        case SGD_RULE_RAW_SCR: {
+            const double g = s.g, f = std::sqrt(s.frob);
+            return f > 0 ? g / f : 0.0;
+        }
+        default: return s.g;
+    }
 }
 
 }  // namespace sgd
 
 using namespace sgd;
 
+// Unit raw scores of the rule from the matrices' statistics (Eqs. app-attn-score,
+// app-xattn-score, app-mlp-score, app-conv-score, app-block-score with the rule's statistic
+// in place of g), normalised (Eq. app-score-normalization) and mapped to lifetimes.
+static int rank_units(const sgd_unit* units, int L, const std::vector<MatStats>& st, const sgd_sched_params& p,
+                      sgd_schedule* out) {
+    std::vector<double> raw(L, 0.0);
+    if (p.rule == SGD_RULE_DEPTH) {
+        for (int l = 0; l < L; ++l) raw[l] = (double)(l + 1);
+    } else if (p.rule == SGD_RULE_RANDOM) {
+        for (int l = 0; l < L; ++l) raw[l] = (double)(splitmix64(p.seed, (uint64_t)l + 1) >> 11) * 0x1.0p-53;
+    } else {
+        size_t ji = 0;
+        for (int l = 0; l < L; ++l) {
+            const sgd_unit& u = units[l];
+            double g[SGD_ROLE_CONV + 1];
+            bool have[SGD_ROLE_CONV + 1] = {};
+            double conv = 0.0;
+            for (int i = 0; i < u.n_mats; ++i, ++ji) {
+                const int r = u.mats[i].role;
+                const double v = rule_stat(st[ji], p.rule);
+                if (r == SGD_ROLE_CONV) { conv += v; continue; }
+                have[r] = true;
+                g[r] = v;
+            }
+            const double sdh = std::sqrt((double)u.head_dim);
+            double q = 0.0;
+            if (have[SGD_ROLE_Q] && have[SGD_ROLE_K] && have[SGD_ROLE_V] && have[SGD_ROLE_O])
+                q += g[SGD_ROLE_O] * g[SGD_ROLE_V] * (1.0 + g[SGD_ROLE_Q] * g[SGD_ROLE_K] / sdh);
+            if (have[SGD_ROLE_XQ] && have[SGD_ROLE_XK] && have[SGD_ROLE_XV] && have[SGD_ROLE_XO])
+                q += g[SGD_ROLE_XO] * g[SGD_ROLE_XV] * (1.0 + g[SGD_ROLE_XQ] * g[SGD_ROLE_XK] / sdh);
+            if (have[SGD_ROLE_W1] && have[SGD_ROLE_W2]) q += g[SGD_ROLE_W2] * g[SGD_ROLE_W1];
+            q += conv;
+            raw[l] = q;
+        }
+    }
+    double mx = 0.0;
+    for (double v : raw) {
+        if (!std::isfinite(v)) return fail(SGD_E_NUMERIC, "non-finite unit score");
+        mx = std::max(mx, v);
+    }
+    std::vector<double> score(L);
+    for (int l = 0; l < L; ++l) score[l] = raw[l] / (mx + 1e-12);
+    int rc = lifetimes_from_scores(score.data(), L, &p, out);
+    if (rc) return rc;
+    if (out->unit_raw) std::memcpy(out->unit_raw, raw.data(), L * sizeof(double));
+    if (out->unit_score) std::memcpy(out->unit_score, score.data(), L * sizeof(double));
+    if (out->mat_stats)
+        for (size_t i = 0; i < st.size(); ++i) {
+            const MatStats& m = st[i];
+            double* o = out->mat_stats + 6 * i;
+            o[0] = m.e_top; o[1] = m.e_tail; o[2] = m.frob; o[3] = m.scr; o[4] = m.g; o[5] = m.sigma1_sq;
+        }
+    return SGD_OK;
+}
+
+extern "C" int32_t sgd_s_min_default(int32_t T) { return T >= 1 ? (T + 9) / 10 : 0; }
+
+extern "C" int sgd_budget_layer_steps(int32_t pct, int32_t L, int32_t T, int64_t* n_star) {
+    if (!n_star) return fail(SGD_E_ARG, "NULL argument");
+    if (pct < 0 || pct > 100 || L < 1 || T < 1) return fail(SGD_E_ARG, "need 0 <= pct <= 100, L >= 1, T >= 1");
+    *n_star = (int64_t)pct * L * T / 100;
+    return SGD_OK;
+}
+
 extern "C" int sgd_schedule_from_scores(const double* unit_score, int32_t L, const sgd_sched_params* params,
                                         sgd_schedule* out) {
     if (!unit_score || !out || !out->lifetimes || !out->active) return fail(SGD_E_ARG, "NULL argument");
-    int rc = check_params(params, L);
+    sgd_sched_params p;
+    int rc = resolve_params(params, L, &p);
     if (rc) return rc;
     for (int l = 0; l < L; ++l)
         if (!std::isfinite(unit_score[l]) || unit_score[l] < 0) return fail(SGD_E_NUMERIC, "scores must be finite and >= 0");
-    rc = lifetimes_from_scores(unit_score, L, params, out);
+    rc = lifetimes_from_scores(unit_score, L, &p, out);
     if (rc) return rc;
     if (out->unit_score)
         for (int l = 0; l < L; ++l) out->unit_score[l] = unit_score[l];
@@ -297,9 +401,11 @@ extern "C" int sgd_schedule_from_lifetimes(int32_t L, int32_t T, const int32_t* 
     if (!lifetimes || !out || !out->lifetimes || !out->active) return fail(SGD_E_ARG, "NULL argument");
     if (L < 1 || T < 1) return fail(SGD_E_ARG, "L and T must be >= 1");
     long total = 0;
+    int smin = T;
     for (int l = 0; l < L; ++l) {
         if (lifetimes[l] < 1 || lifetimes[l] > T) return fail(SGD_E_ARG, "lifetimes must lie in 1..T");
         total += lifetimes[l];
+        smin = std::min(smin, (int)lifetimes[l]);
     }
     out->L = L;
     out->T = T;
@@ -308,81 +414,100 @@ extern "C" int sgd_schedule_from_lifetimes(int32_t L, int32_t T, const int32_t* 
         for (int l = 0; l < L; ++l) out->active[(size_t)(s - 1) * L + l] = (uint8_t)(s <= lifetimes[l]);
     out->layer_steps = total;
     out->cut_margin = std::numeric_limits<double>::infinity();
+    out->s_min = smin;
     return SGD_OK;
 }
 
-extern "C" int sgd_matrix_stats(const sgd_matrix* m, double eta, void* hip_stream, double out[5]) {
+extern "C" int sgd_schedule_workspace_bytes(const sgd_unit* units, int32_t L, int32_t workers, size_t* bytes) {
+    if (!bytes || (!units && L > 0)) return fail(SGD_E_ARG, "NULL argument");
+    if (workers < 1 || workers > 16) return fail(SGD_E_ARG, "workers must lie in 1..16");
+    long nmax = 0;
+    for (int l = 0; l < L; ++l) {
+        if (units[l].n_mats > 0 && !units[l].mats) return fail(SGD_E_ARG, "unit without matrices");
+        for (int i = 0; i < units[l].n_mats; ++i)
+            nmax = std::max<long>(nmax, std::min(units[l].mats[i].rows, units[l].mats[i].cols));
+    }
+    *bytes = nmax > 0 ? (size_t)workers * worker_bytes(nmax) : 0;
+    return SGD_OK;
+}
+
+extern "C" int sgd_matrix_stats(const sgd_matrix* m, double eta, void* workspace, size_t workspace_bytes,
+                                void* hip_stream, double out[6]) {
     if (!out) return fail(SGD_E_ARG, "out is NULL");
     int rc = validate_matrix(m);
     if (rc) return rc;
     if (!(eta >= 0) || !std::isfinite(eta)) return fail(SGD_E_ARG, "eta must be finite and >= 0");
     std::vector<MatJob> jobs{{m, {}}};
-    rc = run_stats(jobs, eta, (hipStream_t)hip_stream);
+    rc = run_stats(jobs, eta, (char*)workspace, workspace_bytes, (hipStream_t)hip_stream);
     if (rc) return rc;
     const MatStats& s = jobs[0].out;
-    out[0] = s.e_top; out[1] = s.e_tail; out[2] = s.frob; out[3] = s.scr; out[4] = s.g;
+    out[0] = s.e_top; out[1] = s.e_tail; out[2] = s.frob; out[3] = s.scr; out[4] = s.g; out[5] = s.sigma1_sq;
     return SGD_OK;
 }
 
-extern "C" int sgd_schedule_build(const sgd_unit* units, int32_t L, const sgd_sched_params* params,
-                                  void* hip_stream, sgd_schedule* out) {
-    if (!units || !out || !out->lifetimes || !out->active) return fail(SGD_E_ARG, "NULL argument");
-    int rc = check_params(params, L);
+extern "C" int sgd_schedule_build(const sgd_unit* units, int32_t L, const sgd_sched_params* params, void* workspace,
+                                  size_t workspace_bytes, void* hip_stream, sgd_schedule* out) {
+    if (!out || !out->lifetimes || !out->active) return fail(SGD_E_ARG, "NULL argument");
+    sgd_sched_params p;
+    int rc = resolve_params(params, L, &p);
     if (rc) return rc;
+    const bool unit_rule = p.rule == SGD_RULE_DEPTH || p.rule == SGD_RULE_RANDOM;
+    if (!units && !unit_rule) return fail(SGD_E_ARG, "units is NULL");
     std::vector<MatJob> jobs;
+    if (units) {
+        for (int l = 0; l < L; ++l) {
+            const sgd_unit& u = units[l];
+            if (u.n_mats < 1 || !u.mats) return fail(SGD_E_ARG, "unit without matrices");
+            if (u.head_dim < 1) return fail(SGD_E_ARG, "head_dim must be >= 1");
+            bool seen[SGD_ROLE_CONV + 1] = {};
+            for (int i = 0; i < u.n_mats; ++i) {
+                rc = validate_matrix(&u.mats[i]);
+                if (rc) return rc;
+                const int r = u.mats[i].role;
+                if (r != SGD_ROLE_CONV && seen[r]) return fail(SGD_E_ARG, "a unit lists the same role twice");
+                seen[r] = true;
+                jobs.push_back({&u.mats[i], {}});
+            }
+        }
+    }
+    // unit rules only rank units; spectra are computed when matrices are given (mat_stats)
+    if (!unit_rule || (units && out->mat_stats)) {
+        rc = run_stats(jobs, p.eta, (char*)workspace, workspace_bytes, (hipStream_t)hip_stream);
+        if (rc) return rc;
+    }
+    std::vector<MatStats> st(jobs.size());
+    for (size_t i = 0; i < jobs.size(); ++i) st[i] = jobs[i].out;
+    return rank_units(units, L, st, p, out);
+}
+
+extern "C" int sgd_schedule_from_stats(const sgd_unit* units, int32_t L, const double* mat_stats,
+                                       const sgd_sched_params* params, sgd_schedule* out) {
+    if (!units || !mat_stats || !out || !out->lifetimes || !out->active) return fail(SGD_E_ARG, "NULL argument");
+    sgd_sched_params p;
+    int rc = resolve_params(params, L, &p);
+    if (rc) return rc;
+    std::vector<MatStats> st;
     for (int l = 0; l < L; ++l) {
         const sgd_unit& u = units[l];
         if (u.n_mats < 1 || !u.mats) return fail(SGD_E_ARG, "unit without matrices");
         if (u.head_dim < 1) return fail(SGD_E_ARG, "head_dim must be >= 1");
+        bool seen[SGD_ROLE_CONV + 1] = {};
         for (int i = 0; i < u.n_mats; ++i) {
-            rc = validate_matrix(&u.mats[i]);
-            if (rc) return rc;
-            jobs.push_back({&u.mats[i], {}});
-        }
-    }
-    rc = run_stats(jobs, params->eta, (hipStream_t)hip_stream);
-    if (rc) return rc;
-    // combine: component scores -> unit raw score -> normalised score
-    std::vector<double> raw(L, 0.0);
-    size_t ji = 0;
-    for (int l = 0; l < L; ++l) {
-        const sgd_unit& u = units[l];
-        double g[SGD_ROLE_CONV + 1];
-        bool have[SGD_ROLE_CONV + 1] = {};
-        double conv = 0.0;
-        for (int i = 0; i < u.n_mats; ++i, ++ji) {
             const int r = u.mats[i].role;
-            if (r == SGD_ROLE_CONV) { conv += jobs[ji].out.g; continue; }
-            if (have[r]) return fail(SGD_E_ARG, "a unit lists the same role twice");
-            have[r] = true;
-            g[r] = jobs[ji].out.g;
+            if (r < SGD_ROLE_Q || r > SGD_ROLE_CONV) return fail(SGD_E_ARG, "unknown matrix role");
+            if (r != SGD_ROLE_CONV && seen[r]) return fail(SGD_E_ARG, "a unit lists the same role twice");
+            seen[r] = true;
+            const double* o = mat_stats + 6 * st.size();
+            MatStats m;
+            m.e_top = o[0]; m.e_tail = o[1]; m.frob = o[2]; m.scr = o[3]; m.g = o[4]; m.sigma1_sq = o[5];
+            for (int c = 0; c < 6; ++c)
+                if (!std::isfinite(o[c]) && c != 3) return fail(SGD_E_NUMERIC, "non-finite matrix statistic");
+            st.push_back(m);
         }
-        const double sdh = std::sqrt((double)u.head_dim);
-        double q = 0.0;
-        if (have[SGD_ROLE_Q] && have[SGD_ROLE_K] && have[SGD_ROLE_V] && have[SGD_ROLE_O])
-            q += g[SGD_ROLE_O] * g[SGD_ROLE_V] * (1.0 + g[SGD_ROLE_Q] * g[SGD_ROLE_K] / sdh);
-        if (have[SGD_ROLE_XQ] && have[SGD_ROLE_XK] && have[SGD_ROLE_XV] && have[SGD_ROLE_XO])
-            q += g[SGD_ROLE_XO] * g[SGD_ROLE_XV] * (1.0 + g[SGD_ROLE_XQ] * g[SGD_ROLE_XK] / sdh);
-        if (have[SGD_ROLE_W1] && have[SGD_ROLE_W2]) q += g[SGD_ROLE_W2] * g[SGD_ROLE_W1];
-        q += conv;
-        raw[l] = q;
     }
-    double mx = 0.0;
-    for (double v : raw) {
-        if (!std::isfinite(v)) return fail(SGD_E_NUMERIC, "non-finite unit score");
-        mx = std::max(mx, v);
-    }
-    std::vector<double> score(L);
-    for (int l = 0; l < L; ++l) score[l] = raw[l] / (mx + 1e-12);
-    rc = lifetimes_from_scores(score.data(), L, params, out);
-    if (rc) return rc;
-    if (out->unit_raw) std::memcpy(out->unit_raw, raw.data(), L * sizeof(double));
-    if (out->unit_score) std::memcpy(out->unit_score, score.data(), L * sizeof(double));
-    if (out->mat_stats)
-        for (size_t i = 0; i < jobs.size(); ++i) {
-            const MatStats& s = jobs[i].out;
-            double* o = out->mat_stats + 5 * i;
-            o[0] = s.e_top; o[1] = s.e_tail; o[2] = s.frob; o[3] = s.scr; o[4] = s.g;
-        }
-    return SGD_OK;
+    double* keep = out->mat_stats;
+    out->mat_stats = nullptr;  // the statistics are inputs here
+    rc = rank_units(units, L, st, p, out);
+    out->mat_stats = keep;
+    return rc;
 }

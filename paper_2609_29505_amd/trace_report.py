@@ -1,14 +1,14 @@
 """Summary of a rocprofv3 kernel trace of bench.py, as markdown.
 
     rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o <w> -- \\
-        python3 bench.py --config <w> --no-cpu-baseline --no-kernel-table --taus "" \\
+        python3 bench.py --config <w> --no-cpu-baseline --no-kernel-table --taus "" --rules "" \\
         --lifetimes <lifetimes.json>
     python -m paper_2609_29505_amd.trace_report --workload <w> --trace <dir>/<w>_kernel_trace.csv \\
         --lifetimes <lifetimes.json>
 
 Prints the per-kernel statistics of the traced run and the frozen path's HBM rate from the
 trace's own durations: bench.py launches the budgets in increasing order, each as T warm-up
-and 2T timed steps from step 1 (then the all-active schedule, and the headline budget again
+steps and three timed T-step trajectories (then the all-active schedule, and the headline budget again
 with per-launch events), so the frozen-run dispatches appear in a known order and each
 one's algorithmic bytes follow from the schedule (maximal runs of frozen units, as the
 launcher fuses them).
@@ -53,7 +53,7 @@ def frozen_rates(cfg, rows, lifetimes):
     import bench
 
     T, L = cfg.T, cfg.L
-    W, K = T, 2 * T
+    W, K = T, 3 * T  # bench.py's defaults: T warm-up steps, three whole trajectories
     fr = sorted((r for r in rows if "frozen_run_kernel" in r["Kernel_Name"]), key=lambda r: int(r["Start_Timestamp"]))
     i, out = 0, []
     # the budgets in increasing order, then the headline (smallest) budget once more: the run

@@ -9,6 +9,35 @@ from oracle import schedule as osch
 from oracle import spectral as osp
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
+# Ceiling of the free-running bf16 trajectory bound: the bound follows the oracle's own
+# divergence under tiny input perturbations (the bf16-quantised trajectory map is chaotic),
+# but never exceeds this.
+FREE_RUNNING_CEIL = 8e-2
+
+
+def load_fullsize_golden(name):
+    """The oracle's statistics of every scored matrix of a full-size workload and its unit
+    raw scores, as written by tests/golden/make_fullsize_scores.py.
+    Returns (stats: list over units of {role: MatrixStats}, raw: float64 [L])."""
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", f"fullsize_{name}.txt")
+    stats, raw = [], []
+    for line in open(path):
+        f = line.split()
+        if not f or f[0].startswith("#"):
+            continue
+        if f[0] == "mat":
+            u, role, m, n = int(f[1]), f[2], int(f[3]), int(f[4])
+            e_top, e_tail, frob, s1, g = map(float, f[5:10])
+            while len(stats) <= u:
+                stats.append({})
+            a, b = e_top + 1e-6 * frob, e_tail + 1e-6 * frob
+            stats[u][role] = osp.MatrixStats(m, n, osp.rank_k(m, n), e_top, e_tail, frob,
+                                             float(np.log(a / b)) if b > 0 else float("inf"), g, s1)
+        elif f[0] == "raw":
+            assert int(f[1]) == len(raw)
+            raw.append(float(f[2]))
+    return stats, np.array(raw, np.float64)
 
 
 def rel_err(x: np.ndarray, ref: np.ndarray) -> float:

@@ -86,3 +86,80 @@ def test_from_lifetimes_and_errors():
     with pytest.raises(P.SgdError) as e:
         P.schedule_from_scores([0.5, 0.2], 10, tau=-1.0)
     assert e.value.code == -1
+
+
+def test_library_defaults_match_oracle_readings():
+    """The minimum-lifetime default and the percentage budget live in the library; they
+    equal the oracle's readings (ceil(T / 10); floor(pct L T / 100))."""
+    _lib_or_skip()
+    for T in range(1, 201):
+        assert P.s_min_default(T) == osch.s_min_default(T)
+    rng = np.random.default_rng(0)
+    for _ in range(300):
+        pct, L, T = int(rng.integers(0, 101)), int(rng.integers(1, 64)), int(rng.integers(1, 201))
+        assert P.budget_layer_steps(pct, L, T) == osch.budget_layer_steps(pct, L, T)
+    with pytest.raises(P.SgdError):
+        P.budget_layer_steps(101, 4, 10)
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_default_s_min_and_pct_budget(seed):
+    """s_min = 0 and a percentage budget: the library applies its defaults."""
+    _lib_or_skip()
+    rng = np.random.default_rng(100 + seed)
+    L, T = int(rng.integers(2, 40)), int(rng.integers(10, 101))
+    lam = rng.random(L)
+    pct = int(rng.integers(35, 100))
+    n = osch.budget_layer_steps(pct, L, T)
+    ref = osch.lifetimes_budget(lam, T, n, osch.s_min_default(T))
+    got = P.schedule_from_scores(lam, T, budget_pct=pct)  # s_min None -> 0 -> library default
+    assert got.s_min == osch.s_min_default(T)
+    assert np.array_equal(got.lifetimes, ref.lifetimes)
+    assert got.layer_steps == n
+
+
+@pytest.mark.parametrize("rule", ["depth", "random"])
+def test_unit_rules_build_without_spectra(rule):
+    """The depth and random rankings (Sec. "Static ranking comparisons") need no weights:
+    sgd_schedule_build runs them on the host, bit for bit the oracle's lifetimes."""
+    _lib_or_skip()
+    from oracle import rules as ru
+    for L, T, pct in ((4, 10, 50), (32, 64, 35), (28, 50, 50), (7, 13, 70)):
+        n = osch.budget_layer_steps(pct, L, T)
+        got = P.schedule_build(None, None, T, budget_pct=pct, rule=rule, seed=99, L=L)
+        ref = ru.lifetimes(rule, [], 1, T, n, osch.s_min_default(T), seed=99, L=L)
+        assert np.array_equal(got.lifetimes, ref.lifetimes), (rule, L, T)
+        assert np.array_equal(got.unit_raw, ru.raw_scores(rule, [], 1, seed=99, L=L))
+        assert got.layer_steps == n
+
+
+@pytest.mark.parametrize("rule", ["scr_frob", "frob", "spectral", "stable_rank", "frob_srank", "raw_scr"])
+def test_rule_schedules_from_stats_match_oracle(rule):
+    """Every matrix rule from given statistics (no GPU): the library's unit scores and
+    lifetimes against the oracle's rules on the same statistics, bit for bit."""
+    _lib_or_skip()
+    from oracle import rules as ru
+    from oracle import spectral as sp
+    rng = np.random.default_rng(7)
+    L, T, dh = 9, 30, 64
+    roles, rows, stats = [], [], []
+    for l in range(L):
+        rl = ["q", "k", "v", "o", "w1", "w2"] + (["xq", "xk", "xv", "xo"] if l % 3 == 0 else [])
+        u = {}
+        for r in rl:
+            ev = np.sort(rng.random(40) ** (3 * rng.random()))[::-1] * rng.uniform(0.5, 4)
+            k = 4
+            F = float(ev.sum())
+            a, b = ev[:k].sum() + 1e-6 * F, ev[k:].sum() + 1e-6 * F
+            st = sp.MatrixStats(40, 40, k, float(ev[:k].sum()), float(ev[k:].sum()), F, float(np.log(a / b)),
+                                float(np.sqrt(F) * np.sqrt(a / (a + b))), float(ev[0]))
+            u[r] = st
+            rows.append([st.energy_top, st.energy_tail, st.frob_sq, st.scr, st.g, st.sigma1_sq])
+        roles.append(rl)
+        stats.append(u)
+    for pct in (35, 50, 70):
+        n = osch.budget_layer_steps(pct, L, T)
+        ref = ru.lifetimes(rule, stats, dh, T, n, osch.s_min_default(T))
+        got = P.schedule_from_stats(roles, [dh] * L, np.array(rows), T, budget_pct=pct, rule=rule)
+        assert np.array_equal(got.unit_raw, ru.raw_scores(rule, stats, dh))
+        assert np.array_equal(got.lifetimes, ref.lifetimes)

@@ -4,9 +4,8 @@ bench.py times.
 * Step parity, teacher-forced: step 1 (every unit active) and step 2 with every other unit
   frozen (lifetimes 1 / T) match the oracle at the per-step bar (2e-2 bf16, 1e-4 fp32); step 1
   run twice gives bitwise the same state.
-* Schedule: budget, bounds and nesting properties at any size; the schedule equals the
-  host budget reading of its own scores; sampled matrices' statistics and one unit's raw
-  score match the oracle computed one by one.
+* Schedule: every matrix's statistics and every unit's score against the oracle's stored
+  full-size values, lifetimes and masks bit for bit, for the method and every ranking rule.
 """
 import os
 import time
@@ -20,7 +19,7 @@ from oracle import schedule as osch
 from oracle import spectral as osp
 from oracle.numerics import decode
 
-from helpers import TOL, rel_err
+from helpers import TOL, load_fullsize_golden, rel_err
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -98,43 +97,54 @@ def test_fullsize_step_parity(P, name):
     dm.close()
 
 
-@pytest.mark.parametrize("name", ["dit", "uvit", "sdxl", "llada"])
+@pytest.mark.parametrize("name", ["tiny", "dit", "uvit", "sdxl", "llada"])
 def test_fullsize_schedule(P, name):
+    """The GPU's scores and schedules at full size against the oracle's stored statistics
+    (tests/golden/fullsize_<workload>.txt, written by the oracle alone): every matrix's E_k,
+    tail, ||W||_F^2, ||W||_2^2 and g, every unit's raw score to 1e-10, and the lifetimes and
+    mask bit for bit at every budget, for the method and for every static ranking rule."""
+    from oracle import rules as ru
     cfg, w, x = load(name)
     dm = P.DeviceModel(cfg, w, x)
     T, L = cfg.T, cfg.L
     smin = osch.s_min_default(T)
     units = dm.scored_units()
-    pct = min(cfg.budgets)
-    n = osch.budget_layer_steps(pct, L, T)
+    gstats, graw = load_fullsize_golden(name)
     progress(f"{name}: schedule build on the GPU")
-    sched = P.schedule_build(units, [cfg.dh] * L, T, budget=n)
-    S = sched.lifetimes.astype(np.int64)
-    # properties that hold at any size
-    assert sched.layer_steps == n == int(S.sum())
-    assert S.min() >= smin and S.max() <= T
-    assert np.array_equal(sched.active, osch.active_mask(S, T))
-    order = np.argsort(sched.unit_score, kind="stable")
-    assert np.all(np.diff(S[order]) >= 0)  # lower scores never outlive higher ones
-    assert sched.unit_score.max() <= 1.0 and np.all(sched.unit_score >= 0)
-    # the same schedule by the oracle's budget reading of the GPU's scores is a host-logic
-    # check (bit-exact); the scores themselves are checked against the oracle below
-    ref = osch.lifetimes_budget(sched.unit_score, T, n, smin)
-    assert np.array_equal(ref.lifetimes, S)
-    # sampled matrices, computed one by one by the oracle
-    roles = [r for r, _ in units[0]]
-    picks = [(0, roles.index("q")), (L - 1, roles.index("w2"))]
-    row0 = sum(len(u) for u in units[:L - 1])
-    for l, i in picks:
-        progress(f"{name}: oracle spectrum of unit {l} {roles[i]}")
-        mats = osp.unit_matrices(w[l], cfg.d, cfg.dtype)
-        st = osp.matrix_stats(mats[roles[i]], eta=1e-6)
-        got = sched.mat_stats[(0 if l == 0 else row0) + i]
-        assert got[2] == pytest.approx(st.frob_sq, rel=1e-12)
-        assert abs(got[0] - st.energy_top) <= 1e-11 * st.frob_sq
-        assert got[4] == pytest.approx(st.g, rel=1e-11)
-    if cfg.d <= 1280:
-        progress(f"{name}: oracle score of unit 0")
-        raw0 = osp.unit_score(osp.unit_matrices(w[0], cfg.d, cfg.dtype), cfg.dh).raw
-        assert sched.unit_raw[0] == pytest.approx(raw0, rel=1e-10)
+    sched = P.schedule_build(units, [cfg.dh] * L, T, budget_pct=min(cfg.budgets))
+    assert sched.s_min == smin
+    # every matrix against the oracle's statistics
+    row = 0
+    for l, mats in enumerate(units):
+        for role, _ in mats:
+            ref = gstats[l][role]
+            got = sched.mat_stats[row]
+            row += 1
+            F = ref.frob_sq
+            assert got[2] == pytest.approx(F, rel=1e-12), (l, role)
+            assert abs(got[0] - ref.energy_top) <= 1e-11 * F and abs(got[1] - ref.energy_tail) <= 1e-11 * F
+            assert got[5] == pytest.approx(ref.sigma1_sq, rel=1e-11), (l, role)
+            assert got[4] == pytest.approx(ref.g, rel=1e-11), (l, role)
+    assert np.allclose(sched.unit_raw, graw, rtol=1e-10, atol=0)
+    roles = [[r for r, _ in mats] for mats in units]
+    for rule in ru.RULES:
+        lam = osp.normalise(ru.raw_scores(rule, gstats, cfg.dh, seed=5, L=L))
+        for pct in cfg.budgets:
+            n = osch.budget_layer_steps(pct, L, T)
+            ref = osch.lifetimes_budget(lam, T, n, smin)
+            if rule == "scr_frob" and pct == min(cfg.budgets):
+                got = sched
+            else:  # the same statistics re-ranked by the library (host arithmetic)
+                got = P.schedule_from_stats(roles, [cfg.dh] * L, sched.mat_stats, T, budget_pct=pct, rule=rule,
+                                            seed=5)
+            if rule not in ("depth", "random"):  # scores from float statistics: far from a tie
+                assert ref.cut_margin > 1e-8, (rule, pct, ref.cut_margin)
+            assert np.array_equal(got.lifetimes, ref.lifetimes), (rule, pct)
+            assert np.array_equal(got.active, osch.active_mask(ref.lifetimes, T))
+            assert got.layer_steps == n == int(got.lifetimes.sum())
+    # one matrix rule end to end on the GPU (spectra recomputed under that rule)
+    got = P.schedule_build(units, [cfg.dh] * L, T, budget_pct=min(cfg.budgets), rule="stable_rank")
+    lam = osp.normalise(ru.raw_scores("stable_rank", gstats, cfg.dh))
+    ref = osch.lifetimes_budget(lam, T, osch.budget_layer_steps(min(cfg.budgets), L, T), smin)
+    assert np.array_equal(got.lifetimes, ref.lifetimes)
     dm.close()

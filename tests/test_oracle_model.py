@@ -226,3 +226,94 @@ def test_generator_spectrum_is_planted():
     pl = u["_planted"]["w1"]
     s = np.linalg.svd(np.asarray(u["w1"], np.float64), compute_uv=False)
     assert np.allclose(s, pl.s, rtol=1e-6)
+
+
+# ---------------------------------------------------------------- cross-attention branch
+# Pins of the SDXL cross-attention branch (the component scored by Eq. app-xattn-score):
+# the keys and values are projections of the conditioning sequence by W_K^x and W_V^x
+# (stored stacked as w_xkv = [W_K^x; W_V^x]), the queries come from the LayerNorm of the
+# current stream, and the branch output is the attention output through W_O^x plus b_O^x.
+
+def _sdxl_f32(**kw):
+    """The reduced SDXL workload in fp32 storage: no bf16 rounding points, so the branch is
+    exact float64 arithmetic and can be compared with an independent computation."""
+    return load("sdxl_mini", dtype="f32", **kw)
+
+
+def test_xattn_one_token_context_is_value_projection():
+    """With a single context token the softmax weight is 1 for every query, so every query
+    receives that token's value projection: out = (c W_V^x^T) W_O^x^T + b_O^x.  A K/V swap
+    in the w_xkv split would give the key projection instead."""
+    cfg, w, x = _sdxl_f32(ctx_len=1)
+    d = cfg.d
+    m = om.Model(cfg, w, x)
+    u = m.units[0]
+    rng = np.random.default_rng(11)
+    h = rng.standard_normal((cfg.B, 7, d))
+    out = m.xattn_branch(u, h, *m.cross_kv(u))
+    c = np.asarray(x["ctx"], np.float64)  # [B, 1, ctx_dim]
+    wv = u["w_xkv"][d:]                   # W_V^x: rows d..2d of the stacked storage
+    wk = u["w_xkv"][:d]
+    for b in range(cfg.B):
+        v = c[b, 0] @ wv.T
+        ref = v @ u["w_xo"].T + u["b_xo"]
+        assert np.allclose(out[b], np.broadcast_to(ref, out[b].shape), rtol=1e-12, atol=1e-12)
+        wrong = (c[b, 0] @ wk.T) @ u["w_xo"].T + u["b_xo"]
+        assert not np.allclose(out[b, 0], wrong, rtol=1e-3)
+
+
+def test_xattn_zero_output_projection_gives_bias():
+    cfg, w, x = _sdxl_f32()
+    m = om.Model(cfg, w, x)
+    u = dict(m.units[0])
+    u["w_xo"] = np.zeros_like(u["w_xo"])
+    h = np.random.default_rng(12).standard_normal((cfg.B, 5, cfg.d))
+    out = m.xattn_branch(u, h, *m.cross_kv(u))
+    assert np.array_equal(out, np.broadcast_to(u["b_xo"], out.shape))
+
+
+def test_xattn_textbook_per_head():
+    """Per-head cross-attention written out independently: LayerNorm (biased variance,
+    eps 1e-5, gain and shift) of the stream, one query row at a time against the 77
+    context keys of each head, softmax, weighted value sum, heads concatenated."""
+    cfg, w, x = _sdxl_f32()
+    d, H, dh = cfg.d, cfg.H, cfg.dh
+    m = om.Model(cfg, w, x)
+    u = m.units[1]
+    rng = np.random.default_rng(13)
+    h = rng.standard_normal((cfg.B, 3, d)) * 2.0 + 0.5
+    out = m.xattn_branch(u, h, *m.cross_kv(u))
+    c = np.asarray(x["ctx"], np.float64)
+    wq, wk, wv = u["w_xq"], u["w_xkv"][:d], u["w_xkv"][d:]
+    for b in range(cfg.B):
+        keys = [[float(np.dot(c[b, j], wk[r])) for r in range(d)] for j in range(cfg.ctx_len)]
+        vals = [[float(np.dot(c[b, j], wv[r])) for r in range(d)] for j in range(cfg.ctx_len)]
+        for i in range(h.shape[1]):
+            row = h[b, i]
+            mu = sum(row) / d
+            var = sum((v - mu) ** 2 for v in row) / d
+            xn = [(row[t] - mu) / math.sqrt(var + 1e-5) * u["normx_w"][t] + u["normx_b"][t] for t in range(d)]
+            qv = [float(np.dot(xn, wq[r])) for r in range(d)]
+            o = []
+            for hh in range(H):
+                sl = slice(hh * dh, (hh + 1) * dh)
+                logits = [sum(a * bb for a, bb in zip(qv[sl], keys[j][sl])) / math.sqrt(dh)
+                          for j in range(cfg.ctx_len)]
+                mx = max(logits)
+                e = [math.exp(a - mx) for a in logits]
+                tot = sum(e)
+                o += [sum(e[j] / tot * vals[j][hh * dh + t] for j in range(cfg.ctx_len)) for t in range(dh)]
+            ref = np.array([float(np.dot(o, u["w_xo"][r])) for r in range(d)]) + u["b_xo"]
+            assert np.allclose(out[b, i], ref, rtol=1e-10, atol=1e-10 * np.abs(ref).max())
+
+
+def test_xattn_norm_is_layernorm():
+    """LayerNorm removes a per-row constant offset (RMSNorm would not)."""
+    cfg, w, x = _sdxl_f32()
+    m = om.Model(cfg, w, x)
+    u = m.units[0]
+    h = np.random.default_rng(14).standard_normal((cfg.B, 4, cfg.d))
+    kv = m.cross_kv(u)
+    a = m.xattn_branch(u, h, *kv)
+    b = m.xattn_branch(u, h + 3.0, *kv)
+    assert np.allclose(a, b, rtol=1e-9, atol=1e-9 * np.abs(a).max())

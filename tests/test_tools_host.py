@@ -88,7 +88,7 @@ def test_traffic_record_groups_split_launches(tmp_path):
 
 
 def _trace_rows(cfg, lifetimes, extra=0):
-    """Frozen-run dispatches in bench.py's order: every budget (T warm-up + 2T timed steps), then
+    """Frozen-run dispatches in bench.py's order: every budget (T warm-up + 3T timed steps), then
     the headline budget once more; launch i lasts 1 + i ns."""
     import bench
 
@@ -97,7 +97,7 @@ def _trace_rows(cfg, lifetimes, extra=0):
     rows, t = [], 0
     for pct in runs + [runs[0]]:
         act = np.arange(1, T + 1)[:, None] <= np.asarray(lifetimes[str(pct)])[None, :]
-        for j in range(3 * T):
+        for j in range(4 * T):
             for _ in bench.frozen_launch_bytes(cfg, act[j % T]):
                 rows.append({"Kernel_Name": "sgd::frozen_run_kernel(sgd::FrozenRun)",
                              "Start_Timestamp": str(t), "End_Timestamp": str(t + 1 + len(rows))})
@@ -121,7 +121,7 @@ def test_trace_report_frozen_accounting():
     assert [o[0] for o in out] == [50]
     pct, n, nbytes, secs = out[0]
     act = np.arange(1, cfg.T + 1)[:, None] <= np.asarray(lifetimes["50"])[None, :]
-    per_step = [bench.frozen_launch_bytes(cfg, act[j % cfg.T]) for j in range(2 * cfg.T)]
+    per_step = [bench.frozen_launch_bytes(cfg, act[j % cfg.T]) for j in range(3 * cfg.T)]
     assert n == sum(len(p) for p in per_step)
     assert nbytes == sum(sum(p) for p in per_step)
     # the timed launches of the first run follow its T warm-up steps' launches
