@@ -98,6 +98,9 @@ def main() -> int:
                     help="tau-mode schedules (Eq. schedule at a fixed tau) timed beside the budgets; '' for none")
     ap.add_argument("--rules", default="random,depth,frob,spectral,stable_rank,frob_srank,raw_scr",
                     help="static ranking rules timed at the headline budget; '' for none")
+    ap.add_argument("--no-input-aware", action="store_true",
+                    help="skip the activation-drift policy and the oracle-replay search")
+    ap.add_argument("--tau-agree", type=float, default=5e-3, help="oracle-replay tolerance")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the library has no multi-GPU path (batches would shard by "
@@ -187,12 +190,17 @@ def main() -> int:
         for s in range(1, steps + 1):
             dm.step(z, s, sched, cache)
 
-    def timed(sched, profile=None):
+    def timed(sched, profile=None, stepper=None):
         """W warm-up steps, then n_traj whole trajectories, each bracketed by HIP events on
-        the step stream.  Returns the per-trajectory times (ms) and the profile record."""
+        the step stream.  Returns the per-trajectory times (ms) and the profile record.
+        ``stepper(s)`` replaces the scheduled step (the input-aware policies)."""
+        step_fn = stepper or (lambda s: dm.step(z, s, sched, cache))
         w = W
         while w > 0:
-            trajectory(sched, min(w, T))
+            cache.reset()
+            z.copy_(z0)
+            for s in range(1, min(w, T) + 1):
+                step_fn(s)
             w -= T
         torch.cuda.synchronize()
         if profile:
@@ -204,7 +212,7 @@ def main() -> int:
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
             for s in range(1, T + 1):
-                dm.step(z, s, sched, cache)
+                step_fn(s)
             e1.record(stream)
             evs.append((e0, e1))
         torch.cuda.synchronize()
@@ -221,6 +229,8 @@ def main() -> int:
         results[pct] = times
         log(f"budget {pct}%: {n_traj} trajectories of {T} steps, median {np.median(times):.2f} ms "
             f"-> {rate(times):.2f} steps/s")
+    value_head = rate(results[head])
+    act_head = np.asarray(scheds[head].active, np.uint8)
     t_all, _ = timed(all_active)
     z_full = z.clone()  # the all-active trajectory's final state
     log(f"all-active: median {np.median(t_all):.2f} ms per trajectory -> {rate(t_all):.2f} steps/s")
@@ -256,6 +266,40 @@ def main() -> int:
         rule_res[r] = (times, deviation())
         log(f"rule {r}: lifetimes {sch.lifetimes.tolist()} -> {rate(times):.2f} steps/s, "
             f"deviation {rule_res[r][1]['rel_l2']:.3e} (method {dev_head['rel_l2']:.3e})")
+
+    input_aware = None
+    if not args.no_input_aware:
+        # appendix "Dynamic baselines": the causal activation-drift policy at the headline
+        # schedule's per-step active counts, and the oracle-replay pattern under the headline
+        # budget as its ceiling (search not timed; one replay of the pattern is)
+        drift_buf = dm.drift_buffer()
+        d_rows = []
+
+        def drift_step(s):
+            row, _ = dm.drift_step(z, s, scheds[head], cache, drift_buf)
+            d_rows.append(row)
+
+        times, _ = timed(scheds[head], stepper=drift_step)
+        d_dev = deviation()
+        last = np.array(d_rows[-T:])
+        input_aware = {"drift": {"steps_per_s": round(rate(times), 3), "speedup": round(rate(times) / all_rate, 4),
+                                 "layer_steps": int(last.sum()), "deviation": d_dev,
+                                 "rows_differ_from_static": int(np.sum(np.any(last != act_head, axis=1)))}}
+        log(f"drift policy: {rate(times):.2f} steps/s (static {value_head:.2f}), deviation {d_dev['rel_l2']:.3e}")
+        del drift_buf
+        t0 = time.time()
+        life, evals, _ = dm.replay_search(z0, tau_agree=args.tau_agree, max_layer_steps=scheds[head].layer_steps)
+        torch.cuda.synchronize()
+        t_search = time.time() - t0
+        rsch = P.schedule_from_lifetimes(life, T)
+        times, _ = timed(rsch)
+        r_dev = deviation()
+        input_aware["replay"] = {"steps_per_s": round(rate(times), 3), "speedup": round(rate(times) / all_rate, 4),
+                                 "layer_steps": rsch.layer_steps, "ceiling": scheds[head].layer_steps,
+                                 "tau_agree": args.tau_agree, "lifetimes": life.tolist(), "deviation": r_dev,
+                                 "search_s": round(t_search, 2), "search_evaluations": evals}
+        log(f"oracle replay: search {t_search:.1f}s ({evals} evaluations), lifetimes {life.tolist()} -> "
+            f"{rate(times):.2f} steps/s, deviation {r_dev['rel_l2']:.3e}")
 
     value = rate(results[head])
     head_ms = float(np.median(results[head]))
@@ -336,6 +380,7 @@ def main() -> int:
                   **{r: {"steps_per_s": round(rate(tm), 3), "speedup": round(rate(tm) / all_rate, 4),
                          "layer_steps": rule_scheds[r].layer_steps, "deviation": dv}
                      for r, (tm, dv) in rule_res.items()}},
+        "input_aware": input_aware,
         "roofline": roofline,
         "kernels": kernels,
         "frozen_path": frozen,

@@ -282,6 +282,74 @@ typedef struct {
 int sgd_denoise_step(sgd_model* model, void* state, int32_t step, const sgd_schedule* sched,
                      sgd_cache* cache, const sgd_step_args* args, void* hip_stream);
 
+/* -------------------------------------------------- input-aware baselines */
+
+/* One step with an arbitrary set of active units (Alg. 2 with a per-step active set that
+ * need not be nested in s).  active: host [L], nonzero = the unit computes its branches.
+ * An active unit refreshes its cached update at every active step (except at step T, which
+ * no later step reads); a frozen unit adds the update of its latest active step, which must
+ * exist (SGD_E_CACHE otherwise).  Steps arrive in order 1..T on the cache, as for
+ * sgd_denoise_step; the two calls may not be mixed on one trajectory. */
+int sgd_denoise_step_masked(sgd_model* model, void* state, int32_t step, const uint8_t* active, sgd_cache* cache,
+                            const sgd_step_args* args, void* hip_stream);
+
+/* Device bytes of the drift record of sgd_drift_step (caller-allocated, 256-byte aligned).
+ * Layout: L slots of align256(B N d 4) bytes holding each unit's fp32 input [B, N, d] of
+ * the last recorded step, then L x 256 x 2 fp64 partial sums (256-byte aligned), then L x 2
+ * fp64 sums: sum over the input's elements of (h_s - h_{s-1})^2 and of h_s^2 per unit. */
+int sgd_drift_bytes(const sgd_model* model, size_t* bytes);
+
+/* One step of the causal activation-drift policy (appendix "Protocol Details", "Dynamic
+ * baselines", "Causal activation drift"; Table "Static versus input-aware scheduling at
+ * matched per-step active counts").  After step s-1 the policy holds, for every unit l,
+ *   d_{l,s-1} = ||h_{l-1,s-1} - h_{l-1,s-2}||_2 / (||h_{l-1,s-1}||_2 + 1e-8)
+ * of the unit's input h_{l-1} (the residual stream arriving at the unit; norms over the whole
+ * [B, N, d] tensor).  Step s activates the m_s units of largest lagged drift, m_s being the
+ * active count of `sched` at step s, ties to the lower unit index; step 1 is full, and at
+ * step 2 no lagged drift exists (every drift counts as 0).  The step then runs as
+ * sgd_denoise_step_masked and records this step's unit inputs for the next one.
+ *   drift_buf   device buffer of sgd_drift_bytes, the same for a whole trajectory
+ *   active_out  host [L] or NULL: the active set this step used
+ *   drift_out   host [L] or NULL: the lagged drift d_{l,s-1} the choice used
+ * Steps s >= 3 synchronise hip_stream first, to read the drift step s-1 recorded. */
+int sgd_drift_step(sgd_model* model, void* state, int32_t step, const sgd_schedule* sched, sgd_cache* cache,
+                   const sgd_step_args* args, void* drift_buf, size_t drift_bytes, uint8_t* active_out,
+                   double* drift_out, void* hip_stream);
+
+/* Oracle replay (appendix "Protocol Details", "Dynamic baselines", "Oracle replay"): a
+ * non-deployable headroom search.  Parameters:
+ *   tau_agree        tolerance on the relative output deviation (the paper uses 5e-3)
+ *   max_layer_steps  ceiling on the active layer-steps of the whole trajectory (<= 0: L T) */
+typedef struct {
+    double tau_agree;
+    int64_t max_layer_steps;
+} sgd_replay_params;
+
+/* Device bytes of the search's buffer (caller-allocated, 256-byte aligned): the state, two
+ * output buffers and 2 L cached-update slots of B N d fp32 values each, plus the SDXL
+ * context projections and reduction scratch. */
+int sgd_replay_bytes(const sgd_model* model, size_t* bytes);
+
+/* Runs the search from z_1 (device fp32 [B, N, d], not modified) along the unscheduled
+ * trajectory z_{s+1} = alpha z_s - beta eps(z_s):
+ *   at step s >= 2 the frozen set F (cumulative: it starts as the set of step s-1) grows
+ *   greedily: every unit j not in F is evaluated frozen together with F, each frozen unit
+ *   adding its update from the unscheduled evaluation of its last active step, and the
+ *   deviation delta = ||eps_F+j - eps||_2 / (||eps||_2 + 1e-8) over the rows the sampler
+ *   updates is measured against the unscheduled output eps(z_s); the candidate of least
+ *   deviation (ties to the lower index) joins F while delta <= tau_agree, or, ignoring the
+ *   tolerance, while keeping the current active count for the remaining steps would exceed
+ *   the ceiling.  Step 1 is full (no update exists yet).
+ *   lifetimes   host [L]: S_l = the last step before unit l joined F (T if it never did), a
+ *               nested schedule for sgd_schedule_from_lifetimes
+ *   evaluations host, optional: network evaluations the search ran
+ *   delta_log   host [T L L] or NULL: delta of candidate j in round r of step s at
+ *               [((s-1) L + r) L + j], NaN where nothing was evaluated
+ * args supplies alpha, beta and the step workspace.  Synchronises hip_stream. */
+int sgd_replay_search(sgd_model* model, const void* z1, const sgd_replay_params* params, const sgd_step_args* args,
+                      void* replay_buf, size_t replay_bytes, int32_t* lifetimes, int64_t* evaluations,
+                      double* delta_log, void* hip_stream);
+
 /* ------------------------------------------------------------- profiling */
 
 /* Kernel classes the launcher can time with HIP events. */
@@ -289,7 +357,7 @@ enum sgd_kernel_class {
     SGD_K_NORM = 0, SGD_K_GEMM_QKV = 1, SGD_K_ATTN = 2, SGD_K_GEMM_O = 3,
     SGD_K_GEMM_W1 = 4, SGD_K_GEMM_W2 = 5, SGD_K_FROZEN = 6, SGD_K_STATE = 7,
     SGD_K_COND = 8, SGD_K_GEMM_SKIP = 9, SGD_K_GEMM_X = 10, SGD_K_ATTN_X = 11,
-    SGD_K_COUNT = 12
+    SGD_K_DRIFT = 12, SGD_K_COUNT = 13
 };
 
 /* Start timing every launch of kernel class `kclass` (or -1 to stop): the launcher records

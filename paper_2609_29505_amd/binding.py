@@ -20,7 +20,7 @@ SGD_RULE = {"scr_frob": 0, "random": 1, "depth": 2, "frob": 3, "spectral": 4, "s
             "frob_srank": 6, "raw_scr": 7}
 SGD_ROLE = {"q": 0, "k": 1, "v": 2, "o": 3, "xq": 4, "xk": 5, "xv": 6, "xo": 7, "w1": 8, "w2": 9, "conv": 10}
 SGD_K = {"norm": 0, "gemm_qkv": 1, "attn": 2, "gemm_o": 3, "gemm_w1": 4, "gemm_w2": 5, "frozen": 6,
-         "state": 7, "cond": 8, "gemm_skip": 9, "gemm_x": 10, "attn_x": 11}
+         "state": 7, "cond": 8, "gemm_skip": 9, "gemm_x": 10, "attn_x": 11, "drift": 12}
 ERRORS = {-1: "SGD_E_ARG", -2: "SGD_E_SHAPE", -3: "SGD_E_DTYPE", -4: "SGD_E_BUDGET", -5: "SGD_E_STEP",
           -6: "SGD_E_CACHE", -7: "SGD_E_HIP", -8: "SGD_E_NUMERIC"}
 
@@ -71,6 +71,10 @@ class sgd_model_desc(C.Structure):
                 ("units", C.POINTER(sgd_unit_weights))]
 
 
+class sgd_replay_params(C.Structure):
+    _fields_ = [("tau_agree", C.c_double), ("max_layer_steps", C.c_int64)]
+
+
 class sgd_step_args(C.Structure):
     _fields_ = [("alpha", C.c_float), ("beta", C.c_float), ("workspace", C.c_void_p),
                 ("workspace_bytes", C.c_size_t)]
@@ -85,6 +89,7 @@ EXPORTS = ["sgd_last_error", "sgd_version", "sgd_s_min_default", "sgd_budget_lay
            "sgd_schedule_from_stats",
            "sgd_schedule_from_lifetimes", "sgd_model_create", "sgd_model_destroy", "sgd_workspace_bytes",
            "sgd_cache_bytes", "sgd_cache_bind", "sgd_cache_reset", "sgd_cache_destroy", "sgd_denoise_step",
+           "sgd_denoise_step_masked", "sgd_drift_bytes", "sgd_drift_step", "sgd_replay_bytes", "sgd_replay_search",
            "sgd_profile_begin", "sgd_profile_end", "sgd_op_linear", "sgd_op_attention", "sgd_op_norm",
            "sgd_op_frozen_run", "sgd_op_heads", "sgd_op_residual", "sgd_op_adaln_mod"]
 
@@ -117,6 +122,13 @@ def lib() -> C.CDLL:
             "sgd_cache_reset": [vp],
             "sgd_cache_destroy": [vp],
             "sgd_denoise_step": [vp, vp, i32, C.POINTER(sgd_schedule), vp, C.POINTER(sgd_step_args), vp],
+            "sgd_denoise_step_masked": [vp, vp, i32, C.POINTER(C.c_uint8), vp, C.POINTER(sgd_step_args), vp],
+            "sgd_drift_bytes": [vp, C.POINTER(C.c_size_t)],
+            "sgd_drift_step": [vp, vp, i32, C.POINTER(sgd_schedule), vp, C.POINTER(sgd_step_args), vp, C.c_size_t,
+                               C.POINTER(C.c_uint8), C.POINTER(C.c_double), vp],
+            "sgd_replay_bytes": [vp, C.POINTER(C.c_size_t)],
+            "sgd_replay_search": [vp, vp, C.POINTER(sgd_replay_params), C.POINTER(sgd_step_args), vp, C.c_size_t,
+                                  C.POINTER(C.c_int32), C.POINTER(i64), C.POINTER(C.c_double), vp],
             "sgd_profile_begin": [vp, i32, i32],
             "sgd_profile_end": [vp, C.POINTER(C.c_double), C.POINTER(i64)],
             "sgd_op_linear": [i32, vp, i64, vp, i64, vp, vp, i64, i32, i32, i32, i32, i32, i32, vp],
@@ -438,15 +450,67 @@ class DeviceModel:
 
     def step(self, state, s: int, sched: Optional[Schedule], cache: Optional["Cache"], alpha=1.0, beta=None,
              stream=None) -> None:
+        a = self._args(alpha, beta)
+        _check(lib().sgd_denoise_step(self.h, C.c_void_p(state.data_ptr()), s,
+                                      C.byref(sched.c) if sched is not None else None,
+                                      cache.h if cache is not None else None, C.byref(a),
+                                      C.c_void_p(_stream_ptr(stream))))
+
+    def _args(self, alpha=1.0, beta=None):
         a = sgd_step_args()
         a.alpha = alpha
         a.beta = (1.0 / self.cfg.T) if beta is None else beta
         a.workspace = self.workspace.data_ptr()
         a.workspace_bytes = self.workspace.numel()
-        _check(lib().sgd_denoise_step(self.h, C.c_void_p(state.data_ptr()), s,
-                                      C.byref(sched.c) if sched is not None else None,
-                                      cache.h if cache is not None else None, C.byref(a),
-                                      C.c_void_p(_stream_ptr(stream))))
+        return a
+
+    def step_masked(self, state, s: int, active_row, cache: "Cache", alpha=1.0, beta=None, stream=None) -> None:
+        """One step with an arbitrary active set (``active_row``: L flags)."""
+        row = np.ascontiguousarray(active_row, dtype=np.uint8)
+        a = self._args(alpha, beta)
+        _check(lib().sgd_denoise_step_masked(self.h, C.c_void_p(state.data_ptr()), s,
+                                             row.ctypes.data_as(C.POINTER(C.c_uint8)), cache.h, C.byref(a),
+                                             C.c_void_p(_stream_ptr(stream))))
+
+    def drift_buffer(self):
+        """A device buffer of sgd_drift_bytes for drift_step."""
+        nb = C.c_size_t()
+        _check(lib().sgd_drift_bytes(self.h, C.byref(nb)))
+        return _workspace(nb.value)
+
+    def drift_step(self, state, s: int, sched: Schedule, cache: "Cache", drift_buf, alpha=1.0, beta=None,
+                   stream=None):
+        """One step of the causal activation-drift policy; returns (active row, lagged drift)."""
+        L = self.cfg.L
+        row = np.zeros(L, np.uint8)
+        dr = np.zeros(L, np.float64)
+        a = self._args(alpha, beta)
+        _check(lib().sgd_drift_step(self.h, C.c_void_p(state.data_ptr()), s, C.byref(sched.c), cache.h, C.byref(a),
+                                    C.c_void_p(drift_buf.data_ptr()), drift_buf.numel(),
+                                    row.ctypes.data_as(C.POINTER(C.c_uint8)),
+                                    dr.ctypes.data_as(C.POINTER(C.c_double)), C.c_void_p(_stream_ptr(stream))))
+        return row, dr
+
+    def replay_search(self, z1, tau_agree=5e-3, max_layer_steps=0, alpha=1.0, beta=None, log=False, stream=None):
+        """Oracle-replay search from z1; returns (lifetimes, evaluations, delta log or None)."""
+        L, T = self.cfg.L, self.cfg.T
+        nb = C.c_size_t()
+        _check(lib().sgd_replay_bytes(self.h, C.byref(nb)))
+        buf = _workspace(nb.value)
+        p = sgd_replay_params()
+        p.tau_agree = tau_agree
+        p.max_layer_steps = max_layer_steps
+        life = np.zeros(L, np.int32)
+        ev = C.c_int64()
+        dlog = np.zeros(T * L * L, np.float64) if log else None
+        a = self._args(alpha, beta)
+        _check(lib().sgd_replay_search(self.h, C.c_void_p(z1.data_ptr()), C.byref(p), C.byref(a),
+                                       C.c_void_p(buf.data_ptr()), buf.numel(),
+                                       life.ctypes.data_as(C.POINTER(C.c_int32)), C.byref(ev),
+                                       dlog.ctypes.data_as(C.POINTER(C.c_double)) if log else None,
+                                       C.c_void_p(_stream_ptr(stream))))
+        del buf
+        return life, int(ev.value), (dlog.reshape(T, L, L) if log else None)
 
     def profile_begin(self, kclass: str, max_launches: int = 4096) -> None:
         _check(lib().sgd_profile_begin(self.h, SGD_K[kclass] if kclass else -1, max_launches))

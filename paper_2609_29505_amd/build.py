@@ -20,7 +20,7 @@ BUILD = os.path.join(PKG, "_build")
 LIBDIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIBDIR, "libsgd.so")
 
-SOURCES = ["api.cpp", "schedule.cpp", "gemm.hip", "gemm_bf16.hip", "attention.hip", "norm.hip", "elementwise.hip", "spectral.hip"]
+SOURCES = ["api.cpp", "dynamic.cpp", "schedule.cpp", "gemm.hip", "gemm_bf16.hip", "attention.hip", "norm.hip", "elementwise.hip", "spectral.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -13,6 +13,7 @@
 
 #include "internal.h"
 #include "kernels.h"
+#include "model.h"
 
 namespace sgd {
 
@@ -28,47 +29,20 @@ int hip_fail(hipError_t e, const char* what) {
     return SGD_E_HIP;
 }
 
-static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace sgd
 
 using namespace sgd;
 
-struct sgd_model {
-    sgd_model_desc d;
-    std::vector<sgd_unit_weights> u;
-    int dt = 1;       // 0 fp32, 1 bf16
-    size_t es = 2;    // element bytes of activations
-    int np = 64;      // tokens padded to 64
-    int npc = 64;     // context tokens padded to 64
-    long M = 0;
-    // workspace layout
-    size_t w_h, w_xb, w_q, w_k, w_vt, w_ob, w_hid, w_siluc, w_mod, w_hb, w_skip, w_ckv, w_total;
-    // cache layout
-    size_t c_delta, c_ctx, c_total;
-    size_t ckv_unit;  // bytes of one unit's context K and V^T
-    // profiling
-    int prof_class = -1;
-    int prof_max = 0;
-    int prof_n = 0;
-    std::vector<hipEvent_t> prof_ev;
-};
-
-struct sgd_cache {
-    sgd_model* m;
-    char* base;
-    size_t bytes;
-    int last_step;
-    std::vector<int> written;
-    bool ctx_valid;
-};
-
 extern "C" const char* sgd_last_error(void) { return sgd::g_last_error.c_str(); }
 extern "C" int sgd_version(void) { return 1; }
 
-namespace {
-
+namespace sgd {
 bool arch_gated(int a) { return a == SGD_ARCH_LLADA || a == SGD_ARCH_SDXL; }
+}  // namespace sgd
+
+namespace {
 
 int check_unit(const sgd_model_desc& d, const sgd_unit_weights& w, int l) {
     auto need = [&](const void* p, const char* name) -> int {
@@ -281,39 +255,39 @@ struct Step {
 
 }  // namespace
 
-extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const sgd_schedule* sched,
-                                sgd_cache* cache, const sgd_step_args* args, void* hip_stream) {
-    if (!m || !state || !args) return fail(SGD_E_ARG, "NULL argument");
-    const sgd_model_desc& d = m->d;
-    if (!args->workspace || args->workspace_bytes < m->w_total) return fail(SGD_E_ARG, "workspace missing or too small");
-    if ((uintptr_t)args->workspace % 256) return fail(SGD_E_ARG, "workspace must be 256-byte aligned");
-    if ((uintptr_t)state % 16) return fail(SGD_E_ARG, "state must be 16-byte aligned");
-    if (step < 1 || step > d.T) return fail(SGD_E_STEP, "step outside 1..T");
-    const int L = d.L;
-    std::vector<uint8_t> act(L, 1);
-    std::vector<int> life(L, d.T);
-    if (sched) {
-        if (!cache) return fail(SGD_E_ARG, "a scheduled step needs a cache");
-        if (cache->m != m) return fail(SGD_E_ARG, "cache bound to another model");
-        if (sched->L != L || sched->T != d.T || !sched->lifetimes || !sched->active)
-            return fail(SGD_E_ARG, "schedule does not match the model");
-        if (step != cache->last_step + 1) return fail(SGD_E_STEP, "steps must arrive in order 1, 2, ..., T");
-        for (int l = 0; l < L; ++l) {
-            life[l] = sched->lifetimes[l];
-            act[l] = sched->active[(size_t)(step - 1) * L + l];
-            if (life[l] < 1 || life[l] > d.T) return fail(SGD_E_ARG, "lifetime outside 1..T");
-            if ((act[l] != 0) != (step <= life[l])) return fail(SGD_E_ARG, "active mask disagrees with lifetimes");
-            if (!act[l] && !cache->written[l])
-                return fail(SGD_E_CACHE, "unit " + std::to_string(l) + " is frozen but its cache slot was never written");
-        }
-    }
+namespace sgd {
 
-    Step S{m, (hipStream_t)hip_stream, (char*)args->workspace};
+// Shape check of every GEMM the step launches (nothing is enqueued on failure).
+int check_step_shapes(const sgd_model* m) {
+    const sgd_model_desc& d = m->d;
+    const bool gated = arch_gated(d.arch);
+    GemmArgs g;
+    EpiParams e;
+    g.M = (int)m->M; g.K = d.d; g.N = 3 * d.d; e.kind = EP_HEADS; e.rope = d.arch == SGD_ARCH_LLADA; e.dh = d.head_dim;
+    e.d = d.d;
+    bool ok = gemm_shape_ok(m->dt, g, e);
+    e.rope = 0; e.kind = EP_RESID; g.N = d.d; ok = ok && gemm_shape_ok(m->dt, g, e);
+    e.kind = gated ? EP_GATED : EP_ACT; g.N = gated ? 2 * d.F : d.F; ok = ok && gemm_shape_ok(m->dt, g, e);
+    e.kind = EP_RESID; g.N = d.d; g.K = d.F; ok = ok && gemm_shape_ok(m->dt, g, e);
+    if (!ok) return fail(SGD_E_SHAPE, "GEMM shapes not supported by the kernels");
+    return SGD_OK;
+}
+
+// One network evaluation at step `step` (Alg. 2) as the plan describes it: the units in
+// stack order, active ones computing every branch, maximal runs of frozen ones adding their
+// cached updates in one pass; then the sampler update (or h_L left in the stream buffer).
+// Arguments are validated by the callers.
+int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sgd_step_args* args,
+             hipStream_t stream) {
+    const sgd_model_desc& d = m->d;
+    Step S{m, stream, (char*)args->workspace};
     const int dt = m->dt;
     const long M = m->M;
+    const int L = d.L;
     const int dd = d.d, F = d.F, H = d.H, dh = d.head_dim, N = d.N;
     const size_t Md = (size_t)M * dd;
-    float* h = (float*)(S.ws + m->w_h);
+    const uint8_t* act = plan.act;
+    float* h = plan.h ? plan.h : (float*)(S.ws + m->w_h);
     void* xb = S.ws + m->w_xb;
     void* qb = S.ws + m->w_q;
     void* kb = S.ws + m->w_k;
@@ -324,7 +298,6 @@ extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const s
     float* mod = (float*)(S.ws + m->w_mod);
     auto hb = [&](int i) { return (void*)(S.ws + m->w_hb + i * Md * m->es); };
     auto skipbuf = [&](int i) { return (void*)(S.ws + m->w_skip + (size_t)i * align256(Md * m->es)); };
-    auto delta = [&](int l) { return (float*)(cache->base + m->c_delta + (size_t)l * align256(Md * 4)); };
     const bool uvit = d.arch == SGD_ARCH_UVIT, dit = d.arch == SGD_ARCH_DIT, sdxl = d.arch == SGD_ARCH_SDXL;
     const int half = L / 2;
     const float t = (float)(1000.0 * (double)(d.T - step + 1) / (double)d.T);
@@ -332,25 +305,14 @@ extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const s
     const float norm_eps = dit ? 1e-6f : 1e-5f;
     const bool gated = arch_gated(d.arch);
     const int mlp_act = d.arch == SGD_ARCH_LLADA ? ACT_SILU : dit ? ACT_GELU_TANH : ACT_GELU_ERF;
-
-    // shape check of every GEMM before enqueueing anything
-    {
-        GemmArgs g;
-        EpiParams e;
-        g.M = (int)M; g.K = dd; g.N = 3 * dd; e.kind = EP_HEADS; e.rope = d.arch == SGD_ARCH_LLADA; e.dh = dh; e.d = dd;
-        bool ok = gemm_shape_ok(dt, g, e);
-        e.rope = 0; e.kind = EP_RESID; g.N = dd; ok = ok && gemm_shape_ok(dt, g, e);
-        e.kind = gated ? EP_GATED : EP_ACT; g.N = gated ? 2 * F : F; ok = ok && gemm_shape_ok(dt, g, e);
-        e.kind = EP_RESID; g.N = dd; g.K = F; ok = ok && gemm_shape_ok(dt, g, e);
-        if (!ok) return fail(SGD_E_SHAPE, "GEMM shapes not supported by the kernels");
-    }
+    const DriftRec* dr = plan.drift;
 
     // ---- stream set-up and per-step conditioning
     S.run(SGD_K_STATE, [&] { return launch_stream_init((const float*)state, h, d.B, N, dd, uvit ? 1 : 0, t, S.st); });
     if (dit) S.run(SGD_K_COND, [&] { return launch_cond_silu((const float*)d.class_emb, siluc, d.B, dd, t, S.st); });
 
-    // SDXL: context keys/values are step-invariant; the scheduled path computes them once
-    // per trajectory into the cache, the unscheduled path into the workspace per unit.
+    // SDXL: context keys/values are step-invariant; a trajectory computes them once into its
+    // cache, an unscheduled evaluation per active unit into the workspace.
     const size_t cheads = (size_t)d.B * H * m->npc * dh;
     auto ctx_kv = [&](int l, char* dst) {
         GemmArgs g;
@@ -361,8 +323,8 @@ extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const s
         e.ntok = d.ctx_len; e.np = m->npc; e.H = H; e.dh = dh; e.d = dd;
         S.run(SGD_K_GEMM_X, [&] { return launch_gemm(dt, g, e, S.st); });
     };
-    if (sdxl && sched && !cache->ctx_valid)
-        for (int l = 0; l < L; ++l) ctx_kv(l, cache->base + m->c_ctx + (size_t)l * m->ckv_unit);
+    if (sdxl && plan.ckv && plan.ckv_fill)
+        for (int l = 0; l < L; ++l) ctx_kv(l, plan.ckv + (size_t)l * m->ckv_unit);
 
     auto norm = [&](const float* w, const float* b, const float* shift, const float* scale) {
         NormArgs a{h, xb, (int)M, dd, norm_kind, norm_eps, w, b, shift, scale, 6L * dd, N};
@@ -381,6 +343,14 @@ extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const s
         AttnArgs a{q, k, vt, ob, d.B, H, dh, N, m->np, nk, npk};
         S.run(kclass, [&] { return launch_attention(dt, a, S.st); });
     };
+    // the input-aware baseline: this unit's input against the previous recorded step's
+    auto record_drift = [&](int l) {
+        if (!dr) return;
+        S.run(SGD_K_DRIFT, [&] {
+            return launch_sumsq(h, dr->prev + (size_t)l * (align256(Md * 4) / 4), dr->prev + (size_t)l * (align256(Md * 4) / 4),
+                                d.B, N, dd, 0, N, dr->have_prev ? 1 : 0, dr->partial + (size_t)l * kSumBlocks * 2, S.st);
+        });
+    };
 
     int hb_cur = 0;
     // where unit l's output copy (for a long skip or the next out-block) goes, or NULL
@@ -395,13 +365,15 @@ extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const s
     while (l < L && S.err == hipSuccess) {
         const sgd_unit_weights& w = m->u[l];
         const bool out_block = uvit && l > half;
-        const bool store_delta = sched && step == life[l] && life[l] < d.T;
         if (!act[l] && !out_block) {
-            // maximal run of frozen units that need no skip linear in between
+            // maximal run of frozen units that need no skip linear in between (single units
+            // while drift is recorded: each unit's input is measured before its update)
             FrozenRun fr{};
             fr.h = h; fr.n = (long)Md; fr.r = 0; fr.snap_bf16 = dt;
-            while (l < L && !act[l] && !(uvit && l > half) && fr.r < kMaxRun) {
-                fr.delta[fr.r] = delta(l);
+            const int cap = dr ? 1 : kMaxRun;
+            if (dr) record_drift(l);
+            while (l < L && !act[l] && !(uvit && l > half) && fr.r < cap) {
+                fr.delta[fr.r] = plan.dread[l];
                 fr.snap[fr.r] = out_copy(l);
                 fr.r++;
                 ++l;
@@ -409,6 +381,7 @@ extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const s
             S.run(SGD_K_FROZEN, [&] { return launch_frozen_run(fr, S.st); });
             continue;
         }
+        record_drift(l);
         if (out_block) {
             // U-ViT skip linear (always executed): h <- [h ; skip] W_skip^T + b (+ Delta if frozen)
             GemmArgs g;
@@ -417,12 +390,12 @@ extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const s
             hb_cur ^= 1;
             EpiParams e;
             e.kind = EP_SKIP; e.bias = (const float*)w.b_skip; e.h = h; e.d = dd;
-            if (!act[l]) { e.delta = delta(l); e.delta_mode = 1; e.hcopy = out_copy(l); }
+            if (!act[l]) { e.delta = (float*)plan.dread[l]; e.delta_mode = 1; e.hcopy = out_copy(l); }
             S.run(SGD_K_GEMM_SKIP, [&] { return launch_gemm(dt, g, e, S.st); });
             if (!act[l]) { ++l; continue; }
         }
         // ---- active unit: every branch, in order
-        float* dl = store_delta ? delta(l) : nullptr;
+        float* dl = plan.dwrite ? plan.dwrite[l] : nullptr;
         const float* mod_l = nullptr;
         if (dit) {
             S.run(SGD_K_COND, [&] {
@@ -445,8 +418,8 @@ extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const s
         resid(SGD_K_GEMM_O, ob, dd, dd, w.w_o, w.b_o, mod_l ? mod_l + 2 * dd : nullptr, dl, dl ? 1 : 0, nullptr);
         // cross-attention branch (SDXL)
         if (sdxl) {
-            char* ckv = sched ? cache->base + m->c_ctx + (size_t)l * m->ckv_unit : S.ws + m->w_ckv;
-            if (!sched) ctx_kv(l, ckv);
+            char* ckv = plan.ckv ? plan.ckv + (size_t)l * m->ckv_unit : S.ws + m->w_ckv;
+            if (!plan.ckv) ctx_kv(l, ckv);
             norm((const float*)w.normx_w, (const float*)w.normx_b, nullptr, nullptr);
             GemmArgs g;
             g.A0 = xb; g.lda0 = dd; g.B = w.w_xq; g.ldb = dd; g.M = (int)M; g.N = dd; g.K = dd;
@@ -470,18 +443,119 @@ extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const s
         resid(SGD_K_GEMM_W2, hid, F, F, w.w2, w.b2, mod_l ? mod_l + 5 * dd : nullptr, dl, dl ? 2 : 0, out_copy(l));
         ++l;
     }
-    S.run(SGD_K_STATE, [&] {
-        return launch_state_update((float*)state, h, d.B, N, dd, d.update_row_begin, d.update_row_end, args->alpha,
-                                   args->beta, S.st);
-    });
+    if (dr && dr->have_prev) S.run(SGD_K_DRIFT, [&] { return launch_sumsq_finish(dr->partial, L, dr->sums, S.st); });
+    if (plan.sampler)
+        S.run(SGD_K_STATE, [&] {
+            return launch_state_update((float*)state, h, d.B, N, dd, d.update_row_begin, d.update_row_end, args->alpha,
+                                       args->beta, S.st);
+        });
     if (S.err != hipSuccess) return hip_fail(S.err, "enqueue");
+    return SGD_OK;
+}
+
+int check_step_args(const sgd_model* m, void* state, int32_t step, const sgd_step_args* args) {
+    if (!m || !state || !args) return fail(SGD_E_ARG, "NULL argument");
+    if (!args->workspace || args->workspace_bytes < m->w_total) return fail(SGD_E_ARG, "workspace missing or too small");
+    if ((uintptr_t)args->workspace % 256) return fail(SGD_E_ARG, "workspace must be 256-byte aligned");
+    if ((uintptr_t)state % 16) return fail(SGD_E_ARG, "state must be 16-byte aligned");
+    if (step < 1 || step > m->d.T) return fail(SGD_E_STEP, "step outside 1..T");
+    return check_step_shapes(m);
+}
+
+int check_cache(const sgd_model* m, const sgd_cache* cache, int32_t step) {
+    if (!cache) return fail(SGD_E_ARG, "a scheduled step needs a cache");
+    if (cache->m != m) return fail(SGD_E_ARG, "cache bound to another model");
+    if (step != cache->last_step + 1) return fail(SGD_E_STEP, "steps must arrive in order 1, 2, ..., T");
+    return SGD_OK;
+}
+
+float* cache_delta(const sgd_model* m, const sgd_cache* c, int l) {
+    return (float*)(c->base + m->c_delta + (size_t)l * align256((size_t)m->M * m->d.d * 4));
+}
+
+// The masked step shared by sgd_denoise_step_masked and the drift policy: active units
+// refresh their cached update (except at the last step, which no later step reads).
+int masked_step(sgd_model* m, void* state, int32_t step, const uint8_t* row, sgd_cache* cache,
+                const sgd_step_args* args, const DriftRec* drift, hipStream_t st) {
+    const int L = m->d.L;
+    std::vector<const float*> dread(L, nullptr);
+    std::vector<float*> dwrite(L, nullptr);
+    std::vector<uint8_t> act(L);
+    for (int l = 0; l < L; ++l) {
+        act[l] = row[l] ? 1 : 0;
+        if (!act[l] && !cache->written[l])
+            return fail(SGD_E_CACHE, "unit " + std::to_string(l) + " is frozen but its cache slot was never written");
+        dread[l] = cache_delta(m, cache, l);
+        if (act[l] && step < m->d.T) dwrite[l] = cache_delta(m, cache, l);
+    }
+    StepPlan plan;
+    plan.act = act.data();
+    plan.dread = dread.data();
+    plan.dwrite = dwrite.data();
+    plan.ckv = m->d.arch == SGD_ARCH_SDXL ? cache->base + m->c_ctx : nullptr;
+    plan.ckv_fill = m->d.arch == SGD_ARCH_SDXL && !cache->ctx_valid;
+    plan.drift = drift;
+    int rc = run_step(m, state, step, plan, args, st);
+    if (rc) return rc;
+    cache->last_step = step;
+    for (int l = 0; l < L; ++l)
+        if (dwrite[l]) cache->written[l] = 1;
+    if (m->d.arch == SGD_ARCH_SDXL) cache->ctx_valid = true;
+    return SGD_OK;
+}
+
+}  // namespace sgd
+
+extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const sgd_schedule* sched,
+                                sgd_cache* cache, const sgd_step_args* args, void* hip_stream) {
+    int rc = check_step_args(m, state, step, args);
+    if (rc) return rc;
+    const sgd_model_desc& d = m->d;
+    const int L = d.L;
+    std::vector<uint8_t> act(L, 1);
+    std::vector<int> life(L, d.T);
+    std::vector<const float*> dread(L, nullptr);
+    std::vector<float*> dwrite(L, nullptr);
+    if (sched) {
+        if ((rc = check_cache(m, cache, step))) return rc;
+        if (sched->L != L || sched->T != d.T || !sched->lifetimes || !sched->active)
+            return fail(SGD_E_ARG, "schedule does not match the model");
+        for (int l = 0; l < L; ++l) {
+            life[l] = sched->lifetimes[l];
+            act[l] = sched->active[(size_t)(step - 1) * L + l];
+            if (life[l] < 1 || life[l] > d.T) return fail(SGD_E_ARG, "lifetime outside 1..T");
+            if ((act[l] != 0) != (step <= life[l])) return fail(SGD_E_ARG, "active mask disagrees with lifetimes");
+            if (!act[l] && !cache->written[l])
+                return fail(SGD_E_CACHE, "unit " + std::to_string(l) + " is frozen but its cache slot was never written");
+            dread[l] = cache_delta(m, cache, l);
+            // the update every later frozen step reads is the one of the last active step
+            if (step == life[l] && life[l] < d.T) dwrite[l] = cache_delta(m, cache, l);
+        }
+    }
+    StepPlan plan;
+    plan.act = act.data();
+    plan.dread = dread.data();
+    plan.dwrite = dwrite.data();
+    plan.ckv = d.arch == SGD_ARCH_SDXL && sched ? cache->base + m->c_ctx : nullptr;
+    plan.ckv_fill = d.arch == SGD_ARCH_SDXL && sched && !cache->ctx_valid;
+    rc = run_step(m, state, step, plan, args, (hipStream_t)hip_stream);
+    if (rc) return rc;
     if (sched) {
         cache->last_step = step;
         for (int u = 0; u < L; ++u)
             if (step == life[u]) cache->written[u] = 1;
-        if (sdxl) cache->ctx_valid = true;
+        if (d.arch == SGD_ARCH_SDXL) cache->ctx_valid = true;
     }
     return SGD_OK;
+}
+
+extern "C" int sgd_denoise_step_masked(sgd_model* m, void* state, int32_t step, const uint8_t* active,
+                                       sgd_cache* cache, const sgd_step_args* args, void* hip_stream) {
+    int rc = check_step_args(m, state, step, args);
+    if (rc) return rc;
+    if (!active) return fail(SGD_E_ARG, "NULL active row");
+    if ((rc = check_cache(m, cache, step))) return rc;
+    return masked_step(m, state, step, active, cache, args, nullptr, (hipStream_t)hip_stream);
 }
 
 // ---------------------------------------------------------------------------- single ops

@@ -59,6 +59,77 @@ hipError_t launch_frozen_run(const FrozenRun& f, hipStream_t st) {
     return hipGetLastError();
 }
 
+// Squared norms for the input-aware baselines (drift of a unit's input, deviation of an
+// output): per block, sum (x - y)^2 and sum x^2 over the selected rows, float4 loads, fp64
+// accumulation, wave then workgroup reduction in a fixed order, so repeated runs give the
+// same bits.  A thread's copy store follows its own loads of the same element (copy may be y).
+__global__ __launch_bounds__(256) void sumsq_kernel(const float* x, const float* y, float* copy, int B, int N,
+                                                    int d, int r0, int r1, int have_y, double* partial) {
+    const long per_sample = (long)(r1 - r0) * d / 4;
+    const long n4 = (long)B * per_sample;
+    double a = 0.0, b = 0.0;
+    for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n4; i += (long)gridDim.x * 256) {
+        const long s = i / per_sample;
+        const long off = ((long)s * N + r0) * d / 4 + (i - s * per_sample);
+        const float4 v = ((const float4*)x)[off];
+        if (have_y) {
+            const float4 p = ((const float4*)y)[off];
+            const float dx = v.x - p.x, dy = v.y - p.y, dz = v.z - p.z, dw = v.w - p.w;
+            a += (double)dx * dx + (double)dy * dy + (double)dz * dz + (double)dw * dw;
+        }
+        b += (double)v.x * v.x + (double)v.y * v.y + (double)v.z * v.z + (double)v.w * v.w;
+        if (copy) ((float4*)copy)[off] = v;
+    }
+    __shared__ double red[2][4];
+    a = warp_sum(a);
+    b = warp_sum(b);
+    const int wv = threadIdx.x / 64;
+    if ((threadIdx.x & 63) == 0) {
+        red[0][wv] = a;
+        red[1][wv] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        partial[2 * blockIdx.x] = ((red[0][0] + red[0][1]) + red[0][2]) + red[0][3];
+        partial[2 * blockIdx.x + 1] = ((red[1][0] + red[1][1]) + red[1][2]) + red[1][3];
+    }
+}
+
+hipError_t launch_sumsq(const float* x, const float* y, float* copy, int B, int N, int d, int r0, int r1,
+                        int have_y, double* partial, hipStream_t st) {
+    hipLaunchKernelGGL(sumsq_kernel, dim3(kSumBlocks), dim3(256), 0, st, x, y, copy, B, N, d, r0, r1, have_y,
+                       partial);
+    return hipGetLastError();
+}
+
+// one workgroup per tensor: kSumBlocks partial pairs -> one pair, fixed order
+__global__ __launch_bounds__(256) void sumsq_finish_kernel(const double* partial, double* out) {
+    const double* p = partial + (size_t)blockIdx.x * 2 * kSumBlocks;
+    double a = 0.0, b = 0.0;
+    for (int i = threadIdx.x; i < kSumBlocks; i += 256) {
+        a += p[2 * i];
+        b += p[2 * i + 1];
+    }
+    __shared__ double red[2][4];
+    a = warp_sum(a);
+    b = warp_sum(b);
+    const int wv = threadIdx.x / 64;
+    if ((threadIdx.x & 63) == 0) {
+        red[0][wv] = a;
+        red[1][wv] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        out[2 * blockIdx.x] = ((red[0][0] + red[0][1]) + red[0][2]) + red[0][3];
+        out[2 * blockIdx.x + 1] = ((red[1][0] + red[1][1]) + red[1][2]) + red[1][3];
+    }
+}
+
+hipError_t launch_sumsq_finish(const double* partial, int count, double* out, hipStream_t st) {
+    hipLaunchKernelGGL(sumsq_finish_kernel, dim3(count), dim3(256), 0, st, partial, out);
+    return hipGetLastError();
+}
+
 // sinusoidal timestep embedding [cos(t f_i), sin(t f_i)], f_i = 10000^(-i/half); evaluated
 // in double precision (a few thousand values per step)
 __device__ __forceinline__ float temb(float t, int k, int dim) {

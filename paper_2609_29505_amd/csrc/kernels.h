@@ -95,6 +95,16 @@ hipError_t launch_adaln_mod(int dtype, const float* x, const void* W, const floa
 // fp32 -> bf16 copy
 hipError_t launch_to_bf16(const float* x, void* y, long n, hipStream_t st);
 
+// Deterministic squared norms over rows [r0, r1) of every sample of fp32 [B, N, d] tensors:
+// partial[2 b] = sum (x - y)^2 (0 unless have_y), partial[2 b + 1] = sum x^2 for the
+// elements of block b (kSumBlocks blocks, fixed assignment and reduction order, fp64);
+// copy (may alias y) receives x.  launch_sumsq_finish sums the partials of `count` tensors
+// (partial + i * 2 kSumBlocks) into out[2 i], out[2 i + 1].
+constexpr int kSumBlocks = 256;
+hipError_t launch_sumsq(const float* x, const float* y, float* copy, int B, int N, int d, int r0, int r1,
+                        int have_y, double* partial, hipStream_t st);
+hipError_t launch_sumsq_finish(const double* partial, int count, double* out, hipStream_t st);
+
 // ---------------------------------------------------------------- spectra (fp64)
 // G = X^T X (trans = 0, X rows x cols, G cols x cols) or X X^T (trans = 1, G rows x rows)
 hipError_t launch_gram(int dtype, const void* X, long rows, long cols, int trans, double* G, hipStream_t st);
