@@ -47,9 +47,11 @@ def unit_flops(cfg) -> dict:
         "gemm_w1": 2.0 * M * (2 * F if cfg.gated else F) * d,
         "gemm_w2": 2.0 * M * d * F,
     }
-    if cfg.arch == "sdxl":
+    if cfg.arch in ("sdxl", "sdxl_unet"):
         f["gemm_x"] = 2.0 * M * d * d * 2
         f["attn_x"] = 4.0 * B * H * N * cfg.ctx_len * dh
+    if cfg.arch == "sdxl_unet":
+        f["gemm_conv"] = 2.0 * M * d * 9 * d  # per 3x3 convolution (two per ResNet block)
     return f
 
 
@@ -400,8 +402,10 @@ def kernel_table(cfg, n_traj, T, profile) -> dict:
     peak = PEAK_BF16 if cfg.dtype == "bf16" else PEAK_F32
     fl = unit_flops(cfg)
     classes = ["gemm_qkv", "attn", "gemm_o", "gemm_w1", "gemm_w2", "norm"]
-    if cfg.arch == "sdxl":
+    if cfg.arch in ("sdxl", "sdxl_unet"):
         classes += ["gemm_x", "attn_x"]
+    if cfg.arch == "sdxl_unet":
+        classes += ["gemm_conv", "gnorm"]
     if cfg.arch == "uvit":
         classes += ["gemm_skip"]
         fl["gemm_skip"] = 2.0 * M * d * 2 * d
@@ -413,7 +417,13 @@ def kernel_table(cfg, n_traj, T, profile) -> dict:
         if not n:
             continue
         rec = {"launches": n, "avg_us": round(ms * 1000.0 / n, 2)}
-        if c == "norm":
+        if c == "gnorm":
+            # GroupNorm + SiLU: fp32 stream in (first) or bf16 convolution output in (second),
+            # bf16 out; launches alternate
+            nbytes = M * d * ((4 + 2) + (2 + 2)) / 2
+            rec.update({"GB/s": round(nbytes * n / (ms / 1000.0) / 1e9, 1),
+                        "frac_hbm": round(nbytes * n / (ms / 1000.0) / PEAK_HBM, 4)})
+        elif c == "norm":
             nbytes = M * d * (4 + es)  # fp32 stream in, normalised rows out
             rec.update({"GB/s": round(nbytes * n / (ms / 1000.0) / 1e9, 1),
                         "frac_hbm": round(nbytes * n / (ms / 1000.0) / PEAK_HBM, 4)})
@@ -450,7 +460,7 @@ def cpu_baseline(cfg, weights, inputs, mean_active, seconds):
     t0 = time.time()
     n = 0
     while n < cfg.L and (n < 2 or time.time() - t0 < seconds):
-        cross = m.cross_kv(m.units[n]) if cfg.arch == "sdxl" else None
+        cross = m.cross_kv(m.units[n]) if cfg.arch in ("sdxl", "sdxl_unet") else None
         if cfg.arch == "uvit" and n > cfg.L // 2:
             break  # out-blocks need the skip inputs of the whole in-stack; in-blocks suffice
         h, _ = m.unit_active(n, h, om.timestep_value(1, cfg.T), cross)

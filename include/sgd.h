@@ -60,7 +60,10 @@ enum sgd_arch {
     SGD_ARCH_LLADA = 1,  /* RMSNorm, MHA with RoPE, SwiGLU MLP                          */
     SGD_ARCH_DIT = 2,    /* LayerNorm + AdaLN shift/scale/gate, biased MHA, GELU(tanh)  */
     SGD_ARCH_UVIT = 3,   /* LayerNorm, MHA, GELU(erf) MLP, long skips via a skip linear */
-    SGD_ARCH_SDXL = 4    /* LayerNorm, self-attn, cross-attn to a context, GEGLU MLP    */
+    SGD_ARCH_SDXL = 4,   /* LayerNorm, self-attn, cross-attn to a context, GEGLU MLP    */
+    SGD_ARCH_SDXL_UNET = 5 /* SDXL UNet stage unit: a ResNet block (GroupNorm, SiLU, 3x3
+                            * convolution + time projection, GroupNorm, SiLU, 3x3
+                            * convolution) followed by the SDXL transformer block        */
 };
 
 /* Role of a scored matrix inside its unit (appendix "Exact Block-Level Scores"). */
@@ -221,13 +224,18 @@ int sgd_schedule_from_lifetimes(int32_t L, int32_t T, const int32_t* lifetimes, 
  *   w2     [d x F]                                b2    fp32 [d]
  *   w_xq   [d x d], w_xkv [2d x ctx_dim] = [W_K^x; W_V^x], w_xo [d x d], b_xo fp32 [d]  (SDXL)
  *   w_ada  [6d x d], b_ada fp32 [6d]: shift1, scale1, gate1, shift2, scale2, gate2  (DiT)
- *   w_skip [d x 2d], b_skip fp32 [d]  (U-ViT out-blocks: h <- [h ; skip] W_skip^T + b)      */
+ *   w_skip [d x 2d], b_skip fp32 [d]  (U-ViT out-blocks: h <- [h ; skip] W_skip^T + b)
+ *   SDXL UNet ResNet block (channels d in and out): GroupNorm gains/shifts gn{1,2}_{w,b} fp32
+ *   [d]; 3x3 convolutions w_conv{1,2} [d x 9d] unfolded tap-major (column (3 ky + kx) d + c
+ *   multiplies input channel c at grid offset (ky - 1, kx - 1)), b_conv{1,2} fp32 [d]; time
+ *   projection w_temb [d x d], b_temb fp32 [d] applied to SiLU(emb(t) + class_emb[b])      */
 typedef struct {
     const void *norm1_w, *norm1_b, *w_qkv, *b_qkv, *w_o, *b_o;
     const void *norm2_w, *norm2_b, *w1, *b1, *w2, *b2;
     const void *normx_w, *normx_b, *w_xq, *w_xkv, *w_xo, *b_xo;
     const void *w_ada, *b_ada;
     const void *w_skip, *b_skip;
+    const void *gn1_w, *gn1_b, *w_conv1, *b_conv1, *w_temb, *b_temb, *gn2_w, *gn2_b, *w_conv2, *b_conv2;
 } sgd_unit_weights;
 
 /* Model description.  B samples of N tokens, width d = H * head_dim, MLP width F,
@@ -236,6 +244,9 @@ typedef struct {
  * ctx: SDXL context, dtype [B x ctx_len x ctx_dim].  U-ViT: L odd; units < L/2 are
  * in-blocks, unit L/2 the mid block, unit l > L/2 takes the skip of in-block L-1-l;
  * token 0 of each sample is the time token, rewritten every step.
+ * SDXL UNet units: the N tokens of a sample are a row-major grid x grid latent (N = grid^2),
+ * GroupNorm has `groups` groups of d / groups channels (a multiple of 4), class_emb is the
+ * per-sample conditioning vector of the time projection.
  * Shape limits: d % 128 == 0, F % 64 == 0, ctx_dim % 64 == 0, head_dim in {64, 72, 128}
  * (LLaDA: 128).  Every unit weight, bias, gain and shift pointer is a device pointer,
  * 16-byte aligned (the kernels read them in 16-byte vectors; SGD_E_ARG otherwise). */
@@ -247,6 +258,7 @@ typedef struct {
     const void* class_emb;
     const void* ctx;
     const sgd_unit_weights* units; /* [L], copied by sgd_model_create */
+    int32_t grid, groups;          /* SDXL UNet units only */
 } sgd_model_desc;
 
 typedef struct sgd_model sgd_model;
@@ -357,7 +369,7 @@ enum sgd_kernel_class {
     SGD_K_NORM = 0, SGD_K_GEMM_QKV = 1, SGD_K_ATTN = 2, SGD_K_GEMM_O = 3,
     SGD_K_GEMM_W1 = 4, SGD_K_GEMM_W2 = 5, SGD_K_FROZEN = 6, SGD_K_STATE = 7,
     SGD_K_COND = 8, SGD_K_GEMM_SKIP = 9, SGD_K_GEMM_X = 10, SGD_K_ATTN_X = 11,
-    SGD_K_DRIFT = 12, SGD_K_COUNT = 13
+    SGD_K_DRIFT = 12, SGD_K_GEMM_CONV = 13, SGD_K_GNORM = 14, SGD_K_COUNT = 15
 };
 
 /* Start timing every launch of kernel class `kclass` (or -1 to stop): the launcher records

@@ -75,6 +75,26 @@ int sgd_op_frozen_run(float* h, const float* const* deltas, int32_t r, int64_t n
 int sgd_op_adaln_mod(int32_t dtype, const float* x, const void* W, const float* bias, float* mod, int32_t B,
                      int32_t d, int32_t n_out, void* hip_stream);
 
+/* SDXL UNet ResNet block: y = SiLU(GroupNorm(x) w + b) in bf16 for x [B, N, C] of dtype
+ * in_dtype (the fp32 stream or a bf16 convolution output); groups of C / groups consecutive
+ * channels (a multiple of 4) normalised over all N positions of a sample (biased variance,
+ * eps), then the per-channel gain w and shift b (fp32 [C]).  C <= 4096.  scratch: caller
+ * device memory of sgd_op_group_norm_scratch_bytes (per-block partial sums and the group
+ * statistics).  x, w, b, scratch 16-byte aligned, y 8-byte aligned. */
+int sgd_op_group_norm_scratch_bytes(int32_t B, int32_t N, int32_t groups, size_t* bytes);
+int sgd_op_group_norm_silu(int32_t in_dtype, const void* x, void* y, int32_t B, int32_t N, int32_t C,
+                           int32_t groups, float eps, const float* w, const float* b, void* scratch,
+                           size_t scratch_bytes, void* hip_stream);
+
+/* 3x3 convolution, stride 1, zero padding 1, of bf16 A [M x Cin] holding M / side^2 row-major
+ * side x side grids, with the bf16 kernel W [N x 9 Cin] unfolded tap-major (column
+ * (3 ky + kx) Cin + c multiplies channel c at grid offset (ky - 1, kx - 1)), as an implicit
+ * GEMM on the matrix cores.  h == NULL: out [M x N] bf16 = conv + bias + rowbias[sample]
+ * (rowbias fp32 [M / side^2 x N] or NULL); h != NULL: h [M x N] fp32 += conv + bias.
+ * Cin % 64 == 0, N % 4 == 0.  tile: 0 auto, or 2 (256x128), 4 (128x128), 5 (256x192). */
+int sgd_op_conv3x3(const void* A, const void* W, const float* bias, const float* rowbias, int32_t side, void* out,
+                   float* h, int32_t M, int32_t N, int32_t Cin, int32_t tile, void* hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -67,7 +67,7 @@ def trajectory(model: om.Model, z0: np.ndarray, static_mask: np.ndarray, steps: 
     the drift the policy would have used."""
     cfg = model.cfg
     steps = cfg.T if steps is None else steps
-    cross = [model.cross_kv(u) for u in model.units] if model.arch == "sdxl" else None
+    cross = [model.cross_kv(u) for u in model.units] if model.arch in om.CROSS_ARCHS else None
     cache: Dict[int, np.ndarray] = {}
     z = np.array(z0, dtype=np.float64)
     prev: Optional[Dict[int, np.ndarray]] = None

@@ -24,7 +24,7 @@ inputs and the SDXL context projections.  The softmax probabilities are
 not rounded.
 
 A multi-branch unit's update Delta is the sum of its branch updates in
-execution order (attention, then cross-attention, then MLP), and the
+execution order (ResNet block, attention, cross-attention, MLP), and the
 active path adds each branch to the stream as it is produced, exactly as
 the unscheduled forward does.
 """
@@ -42,7 +42,9 @@ from .numerics import Precision, decode
 RMS_EPS = 1e-5
 LN_EPS_DIT = 1e-6
 LN_EPS = 1e-5
+GN_EPS = 1e-5
 ROPE_THETA = 10000.0
+CROSS_ARCHS = ("sdxl", "sdxl_unet")  # architectures with a cross-attention branch
 
 
 # --------------------------------------------------------------------------
@@ -64,6 +66,32 @@ def layernorm(x, w=None, b=None, eps=LN_EPS):
     if b is not None:
         y = y + b
     return y
+
+
+def group_norm(x, groups, w, b, eps=GN_EPS):
+    """GroupNorm of [B, N, C] (N grid positions, C channels): per sample and per group of
+    C / groups consecutive channels, (x - mean) / sqrt(biased variance + eps) over the group's
+    positions and channels, then the per-channel gain and shift."""
+    B, N, C = x.shape
+    g = x.reshape(B, N, groups, C // groups)
+    mu = np.mean(g, axis=(1, 3), keepdims=True)
+    var = np.mean((g - mu) ** 2, axis=(1, 3), keepdims=True)
+    y = ((g - mu) / np.sqrt(var + eps)).reshape(B, N, C)
+    return y * w + b
+
+
+def conv3x3(x, w_unf, side):
+    """3 x 3 convolution, stride 1, zero padding 1, on [B, side * side, C_in] (row-major grid)
+    with the kernel unfolded to W [C_out, 9 C_in], column (3 ky + kx) C_in + c:
+    out[b, (y, x), o] = sum_{ky, kx, c} W[o, (3 ky + kx) C_in + c] in[b, (y + ky - 1, x + kx - 1), c],
+    positions outside the grid reading 0.  Written as the unfolded (im2col) matrix times W^T."""
+    B, N, ci = x.shape
+    img = x.reshape(B, side, side, ci)
+    pad = np.zeros((B, side + 2, side + 2, ci), dtype=np.float64)
+    pad[:, 1:-1, 1:-1] = img
+    cols = [pad[:, ky:ky + side, kx:kx + side, :] for ky in range(3) for kx in range(3)]
+    unf = np.concatenate(cols, axis=-1).reshape(B, N, 9 * ci)
+    return unf @ w_unf.T
 
 
 def gelu_erf(x):
@@ -237,7 +265,7 @@ class Model:
             z = z + u["b1"]
         if self.arch == "llada":
             hid = silu(z[..., :F]) * z[..., F:]
-        elif self.arch == "sdxl":
+        elif self.arch in CROSS_ARCHS:
             hid = z[..., F:] * gelu_erf(z[..., :F])
         elif self.arch == "dit":
             hid = gelu_tanh(z)
@@ -255,14 +283,36 @@ class Model:
         q = self.prec.q
         return np.concatenate([q(h), q(skip)], axis=-1) @ u["w_skip"].T + u["b_skip"]
 
+    def temb(self, u, t: float) -> np.ndarray:
+        """SDXL UNet ResNet block: the time-embedding projection SiLU(c) W_t^T + b_t per sample,
+        c = emb(t) + y (the conditioning keeps propagating, Table "Scope and executor
+        semantics")."""
+        c = timestep_embedding(t, self.cfg.d)[None, :] + self.class_emb
+        return silu(c) @ u["w_temb"].T + u["b_temb"]
+
+    def resnet_branch(self, u, h, t: float):
+        """SDXL UNet ResNet block (channels in = out, identity shortcut): GroupNorm, SiLU,
+        3 x 3 convolution plus the time-embedding projection, GroupNorm, SiLU, 3 x 3
+        convolution.  Its update is added to the stream like any residual branch."""
+        cfg, q = self.cfg, self.prec.q
+        x1 = q(silu(group_norm(h, cfg.groups, u["gn1_w"], u["gn1_b"])))
+        u1 = q(conv3x3(x1, u["w_conv1"], cfg.grid) + u["b_conv1"] + self.temb(u, t)[:, None, :])
+        x2 = q(silu(group_norm(u1, cfg.groups, u["gn2_w"], u["gn2_b"])))
+        return conv3x3(x2, u["w_conv2"], cfg.grid) + u["b_conv2"]
+
     def unit_active(self, l: int, h: np.ndarray, t: float, cross=None):
         """Run unit l's branches on the current stream.  Returns (h_out, Delta_l)."""
         u = self.units[l]
         mod = self.adaln(u, t) if self.arch == "dit" else None
+        delta = None
+        if self.arch == "sdxl_unet":
+            r = self.resnet_branch(u, h, t)
+            h = h + r
+            delta = r
         a = self.attn_branch(u, h, mod)
         h = h + a
-        delta = a
-        if self.arch == "sdxl":
+        delta = a if delta is None else delta + a
+        if self.arch in CROSS_ARCHS:
             x = self.xattn_branch(u, h, *cross)
             h = h + x
             delta = delta + x
@@ -344,7 +394,7 @@ def trajectory(model: Model, z0: np.ndarray, active_mask: Optional[np.ndarray],
     cfg = model.cfg
     steps = cfg.T if steps is None else steps
     cross = None
-    if model.arch == "sdxl":
+    if model.arch in CROSS_ARCHS:
         cross = [model.cross_kv(u) for u in model.units]
     cache: Dict[int, np.ndarray] = {}
     z = np.array(z0, dtype=np.float64)

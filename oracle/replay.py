@@ -60,7 +60,7 @@ def search(model: om.Model, z0: np.ndarray, tau_agree: float = 5e-3,
     cfg = model.cfg
     L, T = cfg.L, cfg.T
     ceiling = max_layer_steps if max_layer_steps and max_layer_steps > 0 else L * T
-    cross = [model.cross_kv(u) for u in model.units] if model.arch == "sdxl" else None
+    cross = [model.cross_kv(u) for u in model.units] if model.arch in om.CROSS_ARCHS else None
     z = np.array(z0, dtype=np.float64)
     frozen = [False] * L
     S = np.full(L, T, dtype=np.int64)

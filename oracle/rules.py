@@ -92,8 +92,9 @@ def unit_raw(stats: Dict[str, sp.MatrixStats], head_dim: int, rule: str) -> floa
         raw += sp.q_attn(g["xq"], g["xk"], g["xv"], g["xo"], head_dim)
     if all(r in g for r in sp.MLP_ROLES):
         raw += sp.q_mlp(g["w1"], g["w2"])
-    if "conv" in g:
-        raw += sp.q_conv(g["conv"])
+    for role in sorted(g):
+        if role.startswith("conv"):
+            raw += sp.q_conv(g[role])
     return raw
 
 

@@ -139,6 +139,12 @@ def unit_matrices(weights: Dict[str, np.ndarray], d: int, dtype: str) -> Dict[st
     out["o"] = decode(weights["w_o"], dtype)
     out["w1"] = decode(weights["w1"], dtype)
     out["w2"] = decode(weights["w2"], dtype)
+    if "w_conv1" in weights:
+        # SDXL UNet ResNet block: the kernels as stored unfolded, [C_out, 9 C_in]; the paper
+        # unfolds to C_out x (C_in k_h k_w), a column permutation of this matrix, which has
+        # the same singular values (Eq. app-conv-score)
+        out["conv1"] = decode(weights["w_conv1"], dtype)
+        out["conv2"] = decode(weights["w_conv2"], dtype)
     if "w_xq" in weights:
         out["xq"] = decode(weights["w_xq"], dtype)
         xkv = decode(weights["w_xkv"], dtype)
@@ -157,7 +163,8 @@ def unit_score(mats: Dict[str, np.ndarray], head_dim: int, eta: float = DEFAULT_
     """q~_l = sum of the unit's component scores (Eq. app-block-score).
 
     A transformer block holds a self-attention and an MLP component; an SDXL
-    spatial-transformer block adds a cross-attention component.
+    spatial-transformer block adds a cross-attention component; an SDXL UNet unit adds its
+    ResNet block's two convolutions, one q_conv component each.
     """
     stats = {role: matrix_stats(w, eta) for role, w in mats.items()}
     g = {role: s.g for role, s in stats.items()}
@@ -168,6 +175,7 @@ def unit_score(mats: Dict[str, np.ndarray], head_dim: int, eta: float = DEFAULT_
         raw += q_attn(g["xq"], g["xk"], g["xv"], g["xo"], head_dim)
     if all(r in g for r in MLP_ROLES):
         raw += q_mlp(g["w1"], g["w2"])
-    if "conv" in g:
-        raw += q_conv(g["conv"])
+    for role in sorted(g):
+        if role.startswith("conv"):
+            raw += q_conv(g[role])
     return UnitScore(stats, raw)

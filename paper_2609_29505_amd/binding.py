@@ -15,12 +15,12 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 lib_path = os.path.join(_PKG, "lib", "libsgd.so")
 
 SGD_F32, SGD_BF16 = 0, 1
-SGD_ARCH = {"tiny": 0, "llada": 1, "dit": 2, "uvit": 3, "sdxl": 4}
+SGD_ARCH = {"tiny": 0, "llada": 1, "dit": 2, "uvit": 3, "sdxl": 4, "sdxl_unet": 5}
 SGD_RULE = {"scr_frob": 0, "random": 1, "depth": 2, "frob": 3, "spectral": 4, "stable_rank": 5,
             "frob_srank": 6, "raw_scr": 7}
 SGD_ROLE = {"q": 0, "k": 1, "v": 2, "o": 3, "xq": 4, "xk": 5, "xv": 6, "xo": 7, "w1": 8, "w2": 9, "conv": 10}
 SGD_K = {"norm": 0, "gemm_qkv": 1, "attn": 2, "gemm_o": 3, "gemm_w1": 4, "gemm_w2": 5, "frozen": 6,
-         "state": 7, "cond": 8, "gemm_skip": 9, "gemm_x": 10, "attn_x": 11, "drift": 12}
+         "state": 7, "cond": 8, "gemm_skip": 9, "gemm_x": 10, "attn_x": 11, "drift": 12, "gemm_conv": 13, "gnorm": 14}
 ERRORS = {-1: "SGD_E_ARG", -2: "SGD_E_SHAPE", -3: "SGD_E_DTYPE", -4: "SGD_E_BUDGET", -5: "SGD_E_STEP",
           -6: "SGD_E_CACHE", -7: "SGD_E_HIP", -8: "SGD_E_NUMERIC"}
 
@@ -56,7 +56,8 @@ class sgd_schedule(C.Structure):
 
 
 _W_FIELDS = ["norm1_w", "norm1_b", "w_qkv", "b_qkv", "w_o", "b_o", "norm2_w", "norm2_b", "w1", "b1", "w2", "b2",
-             "normx_w", "normx_b", "w_xq", "w_xkv", "w_xo", "b_xo", "w_ada", "b_ada", "w_skip", "b_skip"]
+             "normx_w", "normx_b", "w_xq", "w_xkv", "w_xo", "b_xo", "w_ada", "b_ada", "w_skip", "b_skip",
+             "gn1_w", "gn1_b", "w_conv1", "b_conv1", "w_temb", "b_temb", "gn2_w", "gn2_b", "w_conv2", "b_conv2"]
 
 
 class sgd_unit_weights(C.Structure):
@@ -68,7 +69,7 @@ class sgd_model_desc(C.Structure):
                 ("H", C.c_int32), ("head_dim", C.c_int32), ("F", C.c_int32), ("L", C.c_int32), ("T", C.c_int32),
                 ("ctx_len", C.c_int32), ("ctx_dim", C.c_int32), ("update_row_begin", C.c_int32),
                 ("update_row_end", C.c_int32), ("class_emb", C.c_void_p), ("ctx", C.c_void_p),
-                ("units", C.POINTER(sgd_unit_weights))]
+                ("units", C.POINTER(sgd_unit_weights)), ("grid", C.c_int32), ("groups", C.c_int32)]
 
 
 class sgd_replay_params(C.Structure):
@@ -91,7 +92,8 @@ EXPORTS = ["sgd_last_error", "sgd_version", "sgd_s_min_default", "sgd_budget_lay
            "sgd_cache_bytes", "sgd_cache_bind", "sgd_cache_reset", "sgd_cache_destroy", "sgd_denoise_step",
            "sgd_denoise_step_masked", "sgd_drift_bytes", "sgd_drift_step", "sgd_replay_bytes", "sgd_replay_search",
            "sgd_profile_begin", "sgd_profile_end", "sgd_op_linear", "sgd_op_attention", "sgd_op_norm",
-           "sgd_op_frozen_run", "sgd_op_heads", "sgd_op_residual", "sgd_op_adaln_mod"]
+           "sgd_op_frozen_run", "sgd_op_heads", "sgd_op_residual", "sgd_op_adaln_mod", "sgd_op_group_norm_silu",
+           "sgd_op_group_norm_scratch_bytes", "sgd_op_conv3x3"]
 
 
 def lib() -> C.CDLL:
@@ -138,6 +140,9 @@ def lib() -> C.CDLL:
             "sgd_op_heads": [i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, vp],
             "sgd_op_residual": [i32, vp, i64, vp, vp, vp, vp, i32, vp, i64, i32, i32, i32, i32, i32, vp],
             "sgd_op_adaln_mod": [i32, vp, vp, vp, vp, i32, i32, i32, vp],
+            "sgd_op_group_norm_scratch_bytes": [i32, i32, i32, C.POINTER(C.c_size_t)],
+            "sgd_op_group_norm_silu": [i32, vp, vp, i32, i32, i32, i32, C.c_float, vp, vp, vp, C.c_size_t, vp],
+            "sgd_op_conv3x3": [vp, vp, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -380,6 +385,24 @@ def op_adaln_mod(x, W, mod, bias=None, stream=None) -> None:
                                   C.c_void_p(_stream_ptr(stream))))
 
 
+def op_group_norm_silu(x, y, groups, w, b, eps=1e-5, stream=None) -> None:
+    """y = SiLU(GroupNorm(x) w + b) for x [B, N, C] (fp32 or bf16), y bf16 [B, N, C]."""
+    B, N, Cc = x.shape
+    nb = C.c_size_t()
+    _check(lib().sgd_op_group_norm_scratch_bytes(B, N, groups, C.byref(nb)))
+    scratch = _workspace(nb.value)
+    _check(lib().sgd_op_group_norm_silu(_dtype_code(x), _p(x), _p(y), B, N, Cc, groups, eps, _p(w), _p(b),
+                                        _p(scratch), scratch.numel(), C.c_void_p(_stream_ptr(stream))))
+
+
+def op_conv3x3(A, W, side, out=None, h=None, bias=None, rowbias=None, tile=0, stream=None) -> None:
+    """3x3 convolution of A [M, Cin] (grids of side x side) with W [N, 9 Cin] (see sgd_ops.h)."""
+    M, Cin = A.shape
+    N = W.shape[0]
+    _check(lib().sgd_op_conv3x3(_p(A), _p(W), _p(bias), _p(rowbias), side, _p(out), _p(h), M, N, Cin, tile,
+                                C.c_void_p(_stream_ptr(stream))))
+
+
 def op_frozen_run(h, deltas, stream=None) -> None:
     arr = (C.c_void_p * len(deltas))(*[t.data_ptr() for t in deltas])
     _check(lib().sgd_op_frozen_run(_p(h), arr, len(deltas), h.numel(), C.c_void_p(_stream_ptr(stream))))
@@ -423,6 +446,7 @@ class DeviceModel:
         d.class_emb = self.class_emb.data_ptr() if self.class_emb is not None else None
         d.ctx = self.ctx.data_ptr() if self.ctx is not None else None
         d.units = C.cast(cw, C.POINTER(sgd_unit_weights))
+        d.grid, d.groups = cfg.grid, cfg.groups
         h = C.c_void_p()
         _check(lib().sgd_model_create(C.byref(d), C.byref(h)))
         self.h = h
@@ -441,6 +465,8 @@ class DeviceModel:
         for dev in self.tensors:
             qkv = dev["w_qkv"]
             mats = [("q", qkv[:d]), ("k", qkv[d:2 * d]), ("v", qkv[2 * d:]), ("o", dev["w_o"])]
+            if "w_conv1" in dev:
+                mats += [("conv", dev["w_conv1"]), ("conv", dev["w_conv2"])]
             if "w_xq" in dev:
                 xkv = dev["w_xkv"]
                 mats += [("xq", dev["w_xq"]), ("xk", xkv[:d]), ("xv", xkv[d:]), ("xo", dev["w_xo"])]

@@ -39,7 +39,8 @@ extern "C" const char* sgd_last_error(void) { return sgd::g_last_error.c_str(); 
 extern "C" int sgd_version(void) { return 1; }
 
 namespace sgd {
-bool arch_gated(int a) { return a == SGD_ARCH_LLADA || a == SGD_ARCH_SDXL; }
+bool arch_gated(int a) { return a == SGD_ARCH_LLADA || a == SGD_ARCH_SDXL || a == SGD_ARCH_SDXL_UNET; }
+bool arch_cross(int a) { return a == SGD_ARCH_SDXL || a == SGD_ARCH_SDXL_UNET; }
 }  // namespace sgd
 
 namespace {
@@ -63,13 +64,21 @@ int check_unit(const sgd_model_desc& d, const sgd_unit_weights& w, int l) {
             break;
         case SGD_ARCH_UVIT:
         case SGD_ARCH_SDXL:
+        case SGD_ARCH_SDXL_UNET:
             if ((rc = need(w.norm1_w, "norm1_w")) || (rc = need(w.norm1_b, "norm1_b")) ||
                 (rc = need(w.norm2_w, "norm2_w")) || (rc = need(w.norm2_b, "norm2_b")))
                 return rc;
             break;
     }
+    if (d.arch == SGD_ARCH_SDXL_UNET) {
+        if ((rc = need(w.gn1_w, "gn1_w")) || (rc = need(w.gn1_b, "gn1_b")) || (rc = need(w.w_conv1, "w_conv1")) ||
+            (rc = need(w.b_conv1, "b_conv1")) || (rc = need(w.w_temb, "w_temb")) || (rc = need(w.b_temb, "b_temb")) ||
+            (rc = need(w.gn2_w, "gn2_w")) || (rc = need(w.gn2_b, "gn2_b")) || (rc = need(w.w_conv2, "w_conv2")) ||
+            (rc = need(w.b_conv2, "b_conv2")))
+            return rc;
+    }
     if (d.arch == SGD_ARCH_UVIT && l > d.L / 2 && (rc = need(w.w_skip, "w_skip"))) return rc;
-    if (d.arch == SGD_ARCH_SDXL) {
+    if (arch_cross(d.arch)) {
         if ((rc = need(w.normx_w, "normx_w")) || (rc = need(w.normx_b, "normx_b")) || (rc = need(w.w_xq, "w_xq")) ||
             (rc = need(w.w_xkv, "w_xkv")) || (rc = need(w.w_xo, "w_xo")))
             return rc;
@@ -77,7 +86,8 @@ int check_unit(const sgd_model_desc& d, const sgd_unit_weights& w, int l) {
     // the kernels read weights, biases, gains and shifts in 16-byte vectors
     const void* ptrs[] = {w.norm1_w, w.norm1_b, w.w_qkv, w.b_qkv, w.w_o, w.b_o, w.norm2_w, w.norm2_b, w.w1, w.b1,
                           w.w2, w.b2, w.normx_w, w.normx_b, w.w_xq, w.w_xkv, w.w_xo, w.b_xo, w.w_ada, w.b_ada,
-                          w.w_skip, w.b_skip};
+                          w.w_skip, w.b_skip, w.gn1_w, w.gn1_b, w.w_conv1, w.b_conv1, w.w_temb, w.b_temb,
+                          w.gn2_w, w.gn2_b, w.w_conv2, w.b_conv2};
     for (const void* p : ptrs)
         if ((uintptr_t)p % 16) return fail(SGD_E_ARG, "unit " + std::to_string(l) + ": weights must be 16-byte aligned");
     return SGD_OK;
@@ -88,7 +98,7 @@ int check_unit(const sgd_model_desc& d, const sgd_unit_weights& w, int l) {
 extern "C" int sgd_model_create(const sgd_model_desc* desc, sgd_model** out) {
     if (!desc || !out || !desc->units) return fail(SGD_E_ARG, "NULL argument");
     const sgd_model_desc& d = *desc;
-    if (d.arch < SGD_ARCH_TINY || d.arch > SGD_ARCH_SDXL) return fail(SGD_E_ARG, "unknown arch");
+    if (d.arch < SGD_ARCH_TINY || d.arch > SGD_ARCH_SDXL_UNET) return fail(SGD_E_ARG, "unknown arch");
     if (d.dtype != SGD_F32 && d.dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
     if (d.dtype == SGD_F32 && (arch_gated(d.arch) || d.arch == SGD_ARCH_LLADA))
         return fail(SGD_E_DTYPE, "fp32 is supported for the tiny, DiT and U-ViT architectures");
@@ -102,10 +112,16 @@ extern "C" int sgd_model_create(const sgd_model_desc* desc, sgd_model** out) {
     if (d.arch == SGD_ARCH_LLADA && d.head_dim != 128) return fail(SGD_E_SHAPE, "rotary heads need head_dim 128");
     if (d.update_row_begin < 0 || d.update_row_end > d.N || d.update_row_begin > d.update_row_end)
         return fail(SGD_E_ARG, "update rows outside [0, N]");
-    if (d.arch == SGD_ARCH_DIT && !d.class_emb) return fail(SGD_E_ARG, "DiT needs class_emb");
+    if ((d.arch == SGD_ARCH_DIT || d.arch == SGD_ARCH_SDXL_UNET) && !d.class_emb)
+        return fail(SGD_E_ARG, "DiT and SDXL UNet units need class_emb");
+    if (d.arch == SGD_ARCH_SDXL_UNET) {
+        if (d.grid < 1 || (long)d.grid * d.grid != d.N) return fail(SGD_E_SHAPE, "SDXL UNet units need N = grid^2");
+        if (d.groups < 1 || d.d % d.groups || (d.d / d.groups) % 4 || d.d > 4096)
+            return fail(SGD_E_SHAPE, "GroupNorm groups must split d (<= 4096) into multiples of 4 channels");
+    }
     if (d.arch == SGD_ARCH_UVIT && (d.L % 2 == 0 || d.L < 3)) return fail(SGD_E_SHAPE, "U-ViT needs an odd L >= 3");
     if (d.arch == SGD_ARCH_UVIT && d.N < 2) return fail(SGD_E_SHAPE, "U-ViT needs the time and class tokens");
-    if (d.arch == SGD_ARCH_SDXL) {
+    if (arch_cross(d.arch)) {
         if (!d.ctx) return fail(SGD_E_ARG, "SDXL needs ctx");
         if (d.ctx_len < 1 || d.ctx_dim < 64 || d.ctx_dim % 64) return fail(SGD_E_SHAPE, "ctx_len >= 1, ctx_dim % 64 == 0");
     }
@@ -121,7 +137,7 @@ extern "C" int sgd_model_create(const sgd_model_desc* desc, sgd_model** out) {
     m->dt = d.dtype == SGD_BF16 ? 1 : 0;
     m->es = m->dt ? 2 : 4;
     m->np = (d.N + 63) / 64 * 64;
-    m->npc = d.arch == SGD_ARCH_SDXL ? (d.ctx_len + 63) / 64 * 64 : 64;
+    m->npc = arch_cross(d.arch) ? (d.ctx_len + 63) / 64 * 64 : 64;
     m->M = (long)d.B * d.N;
     const size_t Md = (size_t)m->M * d.d;
     const size_t heads = (size_t)d.B * d.H * m->np * d.head_dim;
@@ -135,16 +151,18 @@ extern "C" int sgd_model_create(const sgd_model_desc* desc, sgd_model** out) {
     m->w_vt = take(heads * m->es);
     m->w_ob = take(Md * m->es);
     m->w_hid = take((size_t)m->M * d.F * m->es);
-    m->w_siluc = take(d.arch == SGD_ARCH_DIT ? (size_t)d.B * d.d * 4 : 0);
-    m->w_mod = take(d.arch == SGD_ARCH_DIT ? (size_t)d.B * 6 * d.d * 4 : 0);
+    const bool cond = d.arch == SGD_ARCH_DIT || d.arch == SGD_ARCH_SDXL_UNET;
+    m->w_siluc = take(cond ? (size_t)d.B * d.d * 4 : 0);
+    m->w_mod = take(cond ? (size_t)d.B * (d.arch == SGD_ARCH_DIT ? 6 : 1) * d.d * 4 : 0);
     m->w_hb = take(d.arch == SGD_ARCH_UVIT ? 2 * Md * m->es : 0);
     m->w_skip = take(d.arch == SGD_ARCH_UVIT ? (size_t)(d.L / 2) * align256(Md * m->es) : 0);
     m->ckv_unit = align256(2 * cheads * m->es);
-    m->w_ckv = take(d.arch == SGD_ARCH_SDXL ? m->ckv_unit : 0);
+    m->w_ckv = take(arch_cross(d.arch) ? m->ckv_unit : 0);
+    m->w_gn = take(d.arch == SGD_ARCH_SDXL_UNET ? group_norm_scratch_bytes(d.B, d.N, d.groups) : 0);
     m->w_total = o;
     o = 0;
     m->c_delta = take((size_t)d.L * align256(Md * 4));
-    m->c_ctx = take(d.arch == SGD_ARCH_SDXL ? (size_t)d.L * m->ckv_unit : 0);
+    m->c_ctx = take(arch_cross(d.arch) ? (size_t)d.L * m->ckv_unit : 0);
     m->c_total = o;
     *out = m;
     return SGD_OK;
@@ -269,6 +287,11 @@ int check_step_shapes(const sgd_model* m) {
     e.rope = 0; e.kind = EP_RESID; g.N = d.d; ok = ok && gemm_shape_ok(m->dt, g, e);
     e.kind = gated ? EP_GATED : EP_ACT; g.N = gated ? 2 * d.F : d.F; ok = ok && gemm_shape_ok(m->dt, g, e);
     e.kind = EP_RESID; g.N = d.d; g.K = d.F; ok = ok && gemm_shape_ok(m->dt, g, e);
+    if (d.arch == SGD_ARCH_SDXL_UNET) {
+        g.K = 9 * d.d; g.lda0 = d.d; g.ldb = 9 * d.d; g.conv_side = d.grid; g.conv_c = d.d;
+        ok = ok && gemm_shape_ok(m->dt, g, e);
+        e.kind = EP_ACT; e.ldo = d.d; ok = ok && gemm_shape_ok(m->dt, g, e);
+    }
     if (!ok) return fail(SGD_E_SHAPE, "GEMM shapes not supported by the kernels");
     return SGD_OK;
 }
@@ -298,7 +321,8 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
     float* mod = (float*)(S.ws + m->w_mod);
     auto hb = [&](int i) { return (void*)(S.ws + m->w_hb + i * Md * m->es); };
     auto skipbuf = [&](int i) { return (void*)(S.ws + m->w_skip + (size_t)i * align256(Md * m->es)); };
-    const bool uvit = d.arch == SGD_ARCH_UVIT, dit = d.arch == SGD_ARCH_DIT, sdxl = d.arch == SGD_ARCH_SDXL;
+    const bool uvit = d.arch == SGD_ARCH_UVIT, dit = d.arch == SGD_ARCH_DIT, sdxl = arch_cross(d.arch);
+    const bool unet = d.arch == SGD_ARCH_SDXL_UNET;
     const int half = L / 2;
     const float t = (float)(1000.0 * (double)(d.T - step + 1) / (double)d.T);
     const int norm_kind = (d.arch == SGD_ARCH_TINY || d.arch == SGD_ARCH_LLADA) ? 0 : dit ? 2 : 1;
@@ -309,7 +333,8 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
 
     // ---- stream set-up and per-step conditioning
     S.run(SGD_K_STATE, [&] { return launch_stream_init((const float*)state, h, d.B, N, dd, uvit ? 1 : 0, t, S.st); });
-    if (dit) S.run(SGD_K_COND, [&] { return launch_cond_silu((const float*)d.class_emb, siluc, d.B, dd, t, S.st); });
+    if (dit || unet)
+        S.run(SGD_K_COND, [&] { return launch_cond_silu((const float*)d.class_emb, siluc, d.B, dd, t, S.st); });
 
     // SDXL: context keys/values are step-invariant; a trajectory computes them once into its
     // cache, an unscheduled evaluation per active unit into the workspace.
@@ -403,6 +428,31 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
             });
             mod_l = mod;
         }
+        if (unet) {
+            // ResNet block: the unit's time projection, GroupNorm + SiLU, 3x3 convolution (+ bias
+            // + time projection) into the hidden buffer, GroupNorm + SiLU, 3x3 convolution added
+            // to the stream (the first branch: it stores the cached update)
+            S.run(SGD_K_COND, [&] {
+                return launch_adaln_mod(dt, siluc, w.w_temb, (const float*)w.b_temb, mod, d.B, dd, dd, S.st);
+            });
+            GroupNormArgs gn{h, xb, d.B, N, dd, d.groups, 1e-5f, (const float*)w.gn1_w, (const float*)w.gn1_b};
+            S.run(SGD_K_GNORM, [&] { return launch_group_norm_silu(0, gn, S.ws + m->w_gn, S.st); });
+            GemmArgs g;
+            g.A0 = xb; g.lda0 = dd; g.B = w.w_conv1; g.ldb = 9L * dd; g.M = (int)M; g.N = dd; g.K = 9 * dd;
+            g.conv_side = d.grid; g.conv_c = dd;
+            EpiParams e;
+            e.kind = EP_ACT; e.bias = (const float*)w.b_conv1; e.out = hid; e.ldo = dd; e.act = ACT_NONE;
+            e.rowbias = mod; e.rowbias_ld = dd; e.ntok = N;
+            S.run(SGD_K_GEMM_CONV, [&] { return launch_gemm(dt, g, e, S.st); });
+            GroupNormArgs gn2{hid, xb, d.B, N, dd, d.groups, 1e-5f, (const float*)w.gn2_w, (const float*)w.gn2_b};
+            S.run(SGD_K_GNORM, [&] { return launch_group_norm_silu(1, gn2, S.ws + m->w_gn, S.st); });
+            GemmArgs g2 = g;
+            g2.B = w.w_conv2;
+            EpiParams e2;
+            e2.kind = EP_RESID; e2.bias = (const float*)w.b_conv2; e2.h = h; e2.d = dd; e2.delta = dl;
+            e2.delta_mode = dl ? 1 : 0; e2.ntok = N;
+            S.run(SGD_K_GEMM_CONV, [&] { return launch_gemm(dt, g2, e2, S.st); });
+        }
         // attention branch
         norm((const float*)w.norm1_w, (const float*)w.norm1_b, mod_l, mod_l ? mod_l + dd : nullptr);
         {
@@ -415,7 +465,8 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
             S.run(SGD_K_GEMM_QKV, [&] { return launch_gemm(dt, g, e, S.st); });
         }
         attention(qb, kb, vtb, N, m->np, SGD_K_ATTN);
-        resid(SGD_K_GEMM_O, ob, dd, dd, w.w_o, w.b_o, mod_l ? mod_l + 2 * dd : nullptr, dl, dl ? 1 : 0, nullptr);
+        resid(SGD_K_GEMM_O, ob, dd, dd, w.w_o, w.b_o, mod_l ? mod_l + 2 * dd : nullptr, dl, dl ? (unet ? 2 : 1) : 0,
+              nullptr);
         // cross-attention branch (SDXL)
         if (sdxl) {
             char* ckv = plan.ckv ? plan.ckv + (size_t)l * m->ckv_unit : S.ws + m->w_ckv;
@@ -492,15 +543,15 @@ int masked_step(sgd_model* m, void* state, int32_t step, const uint8_t* row, sgd
     plan.act = act.data();
     plan.dread = dread.data();
     plan.dwrite = dwrite.data();
-    plan.ckv = m->d.arch == SGD_ARCH_SDXL ? cache->base + m->c_ctx : nullptr;
-    plan.ckv_fill = m->d.arch == SGD_ARCH_SDXL && !cache->ctx_valid;
+    plan.ckv = arch_cross(m->d.arch) ? cache->base + m->c_ctx : nullptr;
+    plan.ckv_fill = arch_cross(m->d.arch) && !cache->ctx_valid;
     plan.drift = drift;
     int rc = run_step(m, state, step, plan, args, st);
     if (rc) return rc;
     cache->last_step = step;
     for (int l = 0; l < L; ++l)
         if (dwrite[l]) cache->written[l] = 1;
-    if (m->d.arch == SGD_ARCH_SDXL) cache->ctx_valid = true;
+    if (arch_cross(m->d.arch)) cache->ctx_valid = true;
     return SGD_OK;
 }
 
@@ -536,15 +587,15 @@ extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const s
     plan.act = act.data();
     plan.dread = dread.data();
     plan.dwrite = dwrite.data();
-    plan.ckv = d.arch == SGD_ARCH_SDXL && sched ? cache->base + m->c_ctx : nullptr;
-    plan.ckv_fill = d.arch == SGD_ARCH_SDXL && sched && !cache->ctx_valid;
+    plan.ckv = arch_cross(d.arch) && sched ? cache->base + m->c_ctx : nullptr;
+    plan.ckv_fill = arch_cross(d.arch) && sched && !cache->ctx_valid;
     rc = run_step(m, state, step, plan, args, (hipStream_t)hip_stream);
     if (rc) return rc;
     if (sched) {
         cache->last_step = step;
         for (int u = 0; u < L; ++u)
             if (step == life[u]) cache->written[u] = 1;
-        if (d.arch == SGD_ARCH_SDXL) cache->ctx_valid = true;
+        if (arch_cross(d.arch)) cache->ctx_valid = true;
     }
     return SGD_OK;
 }
@@ -667,5 +718,46 @@ extern "C" int sgd_op_adaln_mod(int32_t dtype, const float* x, const void* W, co
     if (B < 1 || n_out < 1 || d < 64 || d % 64) return fail(SGD_E_SHAPE, "modulation shape not supported");
     if ((uintptr_t)x % 16 || (uintptr_t)W % 16) return fail(SGD_E_ARG, "x and W must be 16-byte aligned");
     SGD_HIP_TRY(launch_adaln_mod(dtype == SGD_BF16 ? 1 : 0, x, W, bias, mod, B, d, n_out, (hipStream_t)hip_stream));
+    return SGD_OK;
+}
+
+extern "C" int sgd_op_group_norm_scratch_bytes(int32_t B, int32_t N, int32_t groups, size_t* bytes) {
+    if (!bytes || B < 1 || N < 1 || groups < 1) return fail(SGD_E_ARG, "bad arguments");
+    *bytes = group_norm_scratch_bytes(B, N, groups);
+    return SGD_OK;
+}
+
+extern "C" int sgd_op_group_norm_silu(int32_t in_dtype, const void* x, void* y, int32_t B, int32_t N, int32_t C,
+                                      int32_t groups, float eps, const float* w, const float* b, void* scratch,
+                                      size_t scratch_bytes, void* hip_stream) {
+    if (!x || !y || !w || !b || !scratch) return fail(SGD_E_ARG, "NULL argument");
+    if (in_dtype != SGD_F32 && in_dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
+    if (B < 1 || N < 1 || groups < 1 || C % groups || (C / groups) % 4 || C > 4096)
+        return fail(SGD_E_SHAPE, "group shape not supported");
+    if (scratch_bytes < group_norm_scratch_bytes(B, N, groups)) return fail(SGD_E_ARG, "scratch too small");
+    if ((uintptr_t)x % 16 || (uintptr_t)w % 16 || (uintptr_t)b % 16 || (uintptr_t)y % 8 || (uintptr_t)scratch % 16)
+        return fail(SGD_E_ARG, "operands must be 16-byte aligned (output: 8)");
+    GroupNormArgs a{x, y, B, N, C, groups, eps, w, b};
+    SGD_HIP_TRY(launch_group_norm_silu(in_dtype == SGD_BF16 ? 1 : 0, a, scratch, (hipStream_t)hip_stream));
+    return SGD_OK;
+}
+
+extern "C" int sgd_op_conv3x3(const void* A, const void* W, const float* bias, const float* rowbias, int32_t side,
+                              void* out, float* h, int32_t M, int32_t N, int32_t Cin, int32_t tile, void* hip_stream) {
+    if (!A || !W || (!out && !h)) return fail(SGD_E_ARG, "NULL argument");
+    if (side < 1 || M < 1 || N < 1 || Cin < 1) return fail(SGD_E_SHAPE, "bad convolution shape");
+    if (tile < 0 || tile > kGemmTiles) return fail(SGD_E_ARG, "bad tile");
+    GemmArgs g;
+    g.A0 = A; g.lda0 = Cin; g.B = W; g.ldb = 9L * Cin; g.M = M; g.N = N; g.K = 9 * Cin;
+    g.conv_side = side; g.conv_c = Cin;
+    EpiParams e;
+    e.bias = bias; e.ntok = side * side;
+    if (h) {
+        e.kind = EP_RESID; e.h = h; e.d = N;
+    } else {
+        e.kind = EP_ACT; e.out = out; e.ldo = N; e.act = ACT_NONE; e.rowbias = rowbias; e.rowbias_ld = N;
+    }
+    if (!gemm_shape_ok(1, g, e, tile)) return fail(SGD_E_SHAPE, "convolution shape not supported");
+    SGD_HIP_TRY(launch_gemm(1, g, e, (hipStream_t)hip_stream, tile));
     return SGD_OK;
 }

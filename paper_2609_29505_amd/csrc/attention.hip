@@ -80,7 +80,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
 
     // this lane's query fragments (B operand of S^T = K Q^T)
     bf16x8 qf[KS];
-    const int qrow = min(q, a.npq - 1);
+    const int qrow = min(q, a.nq - 1);  // rows past nq repeat the last query: padded rows are never read
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
         const int c = ks * 16 + half * 8;
@@ -292,7 +292,7 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
 
     // this lane's query fragments (B operand of S^T = K Q^T)
     bf16x8 qf[KS];
-    const int qrow = min(q, a.npq - 1);
+    const int qrow = min(q, a.nq - 1);  // rows past nq repeat the last query: padded rows are never read
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
         const int c = ks * 16 + half * 8;

@@ -114,7 +114,7 @@ ReplayLayout replay_layout(const sgd_model* m) {
     o.hcand = 2 * sb;
     o.slots = 3 * sb;
     o.ckv = o.slots + 2 * (size_t)L * sb;
-    o.partial = o.ckv + (m->d.arch == SGD_ARCH_SDXL ? (size_t)L * m->ckv_unit : 0);
+    o.partial = o.ckv + (arch_cross(m->d.arch) ? (size_t)L * m->ckv_unit : 0);
     o.sums = o.partial + align256((size_t)L * kSumBlocks * 2 * sizeof(double));
     o.total = o.sums + align256((size_t)L * 2 * sizeof(double));
     return o;
@@ -173,7 +173,7 @@ extern "C" int sgd_replay_search(sgd_model* m, const void* z1, const sgd_replay_
         full.act = act.data();
         full.dread = dread.data();
         full.dwrite = dwrite.data();
-        full.ckv = d.arch == SGD_ARCH_SDXL ? base + lay.ckv : nullptr;
+        full.ckv = arch_cross(d.arch) ? base + lay.ckv : nullptr;
         full.ckv_fill = s == 1;
         full.h = href;
         full.sampler = false;
@@ -195,7 +195,7 @@ extern "C" int sgd_replay_search(sgd_model* m, const void* z1, const sgd_replay_
                 pl.act = act.data();
                 pl.dread = dread.data();
                 pl.dwrite = nullptr;
-                pl.ckv = d.arch == SGD_ARCH_SDXL ? base + lay.ckv : nullptr;
+                pl.ckv = arch_cross(d.arch) ? base + lay.ckv : nullptr;
                 pl.h = hcand;
                 pl.sampler = false;
                 if ((rc = run_step(m, z, s, pl, args, st))) return rc;

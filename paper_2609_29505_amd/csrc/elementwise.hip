@@ -74,8 +74,10 @@ __global__ __launch_bounds__(256) void sumsq_kernel(const float* x, const float*
         const float4 v = ((const float4*)x)[off];
         if (have_y) {
             const float4 p = ((const float4*)y)[off];
-            const float dx = v.x - p.x, dy = v.y - p.y, dz = v.z - p.z, dw = v.w - p.w;
-            a += (double)dx * dx + (double)dy * dy + (double)dz * dz + (double)dw * dw;
+            // differences of fp32 values are exact in fp64
+            const double dx = (double)v.x - p.x, dy = (double)v.y - p.y, dz = (double)v.z - p.z,
+                         dw = (double)v.w - p.w;
+            a += dx * dx + dy * dy + dz * dz + dw * dw;
         }
         b += (double)v.x * v.x + (double)v.y * v.y + (double)v.z * v.z + (double)v.w * v.w;
         if (copy) ((float4*)copy)[off] = v;

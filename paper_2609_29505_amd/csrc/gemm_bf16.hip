@@ -268,9 +268,11 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
                     if (!EXA && rr >= C::EPR) continue;
                     const f32x4 v = ld4(st + rr * C::EPS + c);
                     if (row >= g.M || n >= g.N) continue;
+                    const f32x4 rb = ep.rowbias ? ld4(ep.rowbias + (long)sample_of(row) * ep.rowbias_ld + n)
+                                                : f32x4{0.f, 0.f, 0.f, 0.f};
                     float o[4];
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) o[q] = act_fn<ACT>(v[q] + bb[q]);
+                    for (int q = 0; q < 4; ++q) o[q] = act_fn<ACT>((v[q] + bb[q]) + rb[q]);
                     store_bf16x4((bf16*)ep.out + (long)row * ep.ldo + n, o);
                 }
             });
@@ -388,7 +390,7 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
 // the period's MFMAs (part p after MFMA slot p * SLOTS / PARTS), so neither the texture
 // unit nor the LDS sees a burst and both SIMD waves keep issuing MFMAs.
 
-template <class C>
+template <class C, bool CONV>
 __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, EpiParams ep) {
     static_assert(C::STAGES == 2, "two LDS stages plus the register stage");
     __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
@@ -421,6 +423,17 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
     unsigned goff[PARTS];  // A rows of both A sources share the row pitch
 #pragma unroll
     for (int p = 0; p < AP; ++p) goff[p] = (unsigned)((long)(m0 + vr + p * RPP) * g.lda0 * 2 + vc * 16);
+    // implicit-GEMM convolution: grid position (y, x) of each A row (y << 16 | x)
+    int gpos[CONV ? AP : 1];
+    if constexpr (CONV) {
+        const int side = g.conv_side, area = side * side;
+#pragma unroll
+        for (int p = 0; p < AP; ++p) {
+            const int pix = (m0 + vr + p * RPP) % area;
+            const int y = pix / side;
+            gpos[p] = (y << 16) | (pix - y * side);
+        }
+    }
 #pragma unroll
     for (int p = 0; p < BP; ++p) {
         const int r = vr + p * RPP;
@@ -442,7 +455,18 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
     auto gload = [&](int kt, int s, int p) {
         const bool in = kt < KT;
         const int k0 = kt * C::BK;
-        if (p < AP) {
+        if (CONV && p < AP) {
+            // the k tile lies inside one tap (conv_c % 64 == 0): shift the row by the tap's
+            // grid offset, or load zeros (an out-of-range offset) where it leaves the grid
+            const int tap = k0 / g.conv_c;
+            const int c0 = k0 - tap * g.conv_c;
+            const int ky = tap / 3, dy = ky - 1, dx = tap - ky * 3 - 1;
+            const int yy = (gpos[p] >> 16) + dy, xx = (gpos[p] & 0xFFFF) + dx;
+            const bool ok = in && (unsigned)yy < (unsigned)g.conv_side && (unsigned)xx < (unsigned)g.conv_side;
+            const int shift = (dy * g.conv_side + dx) * g.lda0 * 2;
+            vreg[s][p] = __builtin_amdgcn_raw_buffer_load_b128(ra0, ok ? (unsigned)((int)goff[p] + shift) : OOB,
+                                                               ok ? c0 * 2 : 0, 0);
+        } else if (p < AP) {
             const bool second = g.A1 && k0 >= g.K0;
             vreg[s][p] = __builtin_amdgcn_raw_buffer_load_b128(second ? ra1 : ra0, in ? goff[p] : OOB,
                                                                in ? (second ? (k0 - g.K0) * 2 : k0 * 2) : 0, 0);
@@ -588,9 +612,12 @@ Shape tile_shape(int tile) {
 // Cost of one launch of `tile` over `rows` rows in units of a 256 x 256 tile at full rate: one
 // workgroup per CU, so n tiles take ceil(n / 256) rounds of tile area / per-CU rate.
 // Infinite when the epilogue cannot use the tile.
+static bool conv_tile(int tile) { return tile == 2 || tile == 4 || tile == 5; }
+
 static double tile_cost(int tile, long rows, const GemmArgs& g, const EpiParams& e) {
     const Shape s = tile_shape(tile);
     if (!s.bm) return 1e300;
+    if (g.conv_side > 0 && !conv_tile(tile)) return 1e300;
     if (e.kind == EP_GATED && g.N % s.bn) return 1e300;
     const long tiles = ((rows + s.bm - 1) / s.bm) * ((g.N + s.bn - 1) / s.bn);
     return (double)((tiles + 255) / 256) * s.bm * s.bn / s.rate / (256.0 * 256.0);
@@ -610,7 +637,7 @@ GemmPlan gemm_bf16_plan(const GemmArgs& g, const EpiParams& e) {
         if (t < best_t * 0.999) { best_t = t; best = GemmPlan{tile, g.M, 0}; }
     }
     const int tail = g.M % 256;
-    if (g.M > 2048 && tail > 0 && tail <= 128) {
+    if (g.M > 2048 && tail > 0 && tail <= 128 && g.conv_side == 0) {
         for (int tile = 1; tile <= kGemmTiles; ++tile) {
             if (tile_shape(tile).bm != 256) continue;
             const double tm = tile_cost(tile, g.M - tail, g, e);
@@ -644,6 +671,13 @@ bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
     const Shape s = tile_shape(tile);
     if (!s.bm) return false;
     if (g.M >= (1 << 21)) return false;  // the epilogue's fp32 row -> sample split is exact below
+    if (g.conv_side > 0) {
+        const long area = (long)g.conv_side * g.conv_side;
+        if (!conv_tile(tile) || g.A1 || g.conv_c % 64 || g.K != 9 * g.conv_c || g.lda0 != g.conv_c ||
+            g.M % area || g.conv_side >= (1 << 15))
+            return false;
+    }
+    if (!aligned(e.rowbias, 16) || e.rowbias_ld % 4) return false;
     if (g.K % 64 || (g.A1 && (g.K0 % 64 || g.lda1 != g.lda0))) return false;
     if (g.N % 4 || g.lda0 % 8 || (g.A1 && g.lda1 % 8) || g.ldb % 8) return false;  // 16-byte rows
     if (e.kind == EP_GATED && (g.N % s.bn || e.ldo % 4)) return false;
@@ -659,16 +693,24 @@ bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
     return true;
 }
 
-template <class C>
+template <class C, bool CONV = false>
 static hipError_t run_tile(const GemmArgs& g, const EpiParams& e, hipStream_t st) {
     const int nt_m = (g.M - g.m_begin + C::BM - 1) / C::BM, nt_n = (g.N + C::BN - 1) / C::BN;
     GemmArgs ga = g;
     ga.band = tile_band(nt_m, nt_n, C::BM, C::BN);
-    hipLaunchKernelGGL((gemm_bf16_kernel<C>), dim3(nt_m * nt_n), dim3(C::NT), 0, st, ga, e);
+    hipLaunchKernelGGL((gemm_bf16_kernel<C, CONV>), dim3(nt_m * nt_n), dim3(C::NT), 0, st, ga, e);
     return hipGetLastError();
 }
 
 static hipError_t launch_tile(const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile) {
+    if (g.conv_side > 0) {
+        switch (tile) {  // implicit-GEMM convolution: the tiles with registers to spare
+            case 2: return run_tile<T256x128, true>(g, e, st);
+            case 4: return run_tile<T128x128, true>(g, e, st);
+            case 5: return run_tile<T256x192, true>(g, e, st);
+            default: return hipErrorInvalidValue;
+        }
+    }
     switch (tile) {
         case 1: return run_tile<T256x256>(g, e, st);
         case 2: return run_tile<T256x128>(g, e, st);

@@ -21,6 +21,11 @@ struct GemmArgs {
     int M = 0, N = 0, K = 0;  // N: product columns (gated: 2F)
     int m_begin = 0;          // first row of the launch's row tiles (rows below belong to another launch)
     int band = 0;             // bf16 GEMM tile order: row tiles per band (set by the dispatcher)
+    // implicit-GEMM 3x3 convolution (bf16): A0 is the [M, conv_c] input of row-major
+    // conv_side x conv_side grids (M = samples x conv_side^2), K = 9 conv_c, and A's column
+    // (3 ky + kx) conv_c + c of row (sample, y, x) is input (sample, y + ky - 1, x + kx - 1, c),
+    // zero outside the grid.  0: a plain GEMM.
+    int conv_side = 0, conv_c = 0;
 };
 
 enum EpKind { EP_HEADS = 0, EP_ACT = 1, EP_GATED = 2, EP_RESID = 3, EP_SKIP = 4 };
@@ -38,6 +43,8 @@ struct EpiParams {
     // (EP_SKIP: 1 = add the cached delta to the skip output); gate[b * gate_ld + n]
     float* h = nullptr; float* delta = nullptr; int delta_mode = 0;
     const float* gate = nullptr; long gate_ld = 0; void* hcopy = nullptr;
+    // EP_ACT: per-sample additive bias rowbias[sample * rowbias_ld + n] (sample = row / ntok)
+    const float* rowbias = nullptr; long rowbias_ld = 0;
 };
 
 // dtype: 0 fp32, 1 bf16.  tile: 0 = pick automatically; 1..kGemmTiles a fixed bf16 block
@@ -69,6 +76,16 @@ struct NormArgs {
     const float* shift; const float* scale; long mod_ld; int ntok;
 };
 hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t st);
+// y = SiLU(GroupNorm(x) w + b) in bf16 for x [B, N, C] fp32 (in_bf16 = 0) or bf16; groups of
+// C / groups consecutive channels (a multiple of 4) over all N positions of a sample
+struct GroupNormArgs {
+    const void* x; void* y; int B, N, C, groups; float eps;
+    const float* w; const float* b;
+};
+// scratch: group_norm_scratch_bytes(B, N, groups) device bytes (per-block partial sums, stats);
+// C / 4 <= 1024 threads per row block
+size_t group_norm_scratch_bytes(int B, int N, int groups);
+hipError_t launch_group_norm_silu(int in_bf16, const GroupNormArgs& a, void* scratch, hipStream_t st);
 
 // ---------------------------------------------------------------- elementwise
 constexpr int kMaxRun = 32;

@@ -16,7 +16,7 @@ struct sgd_model {
     int npc = 64;     // context tokens padded to 64
     long M = 0;
     // workspace layout
-    size_t w_h, w_xb, w_q, w_k, w_vt, w_ob, w_hid, w_siluc, w_mod, w_hb, w_skip, w_ckv, w_total;
+    size_t w_h, w_xb, w_q, w_k, w_vt, w_ob, w_hid, w_siluc, w_mod, w_hb, w_skip, w_ckv, w_gn, w_total;
     // cache layout
     size_t c_delta, c_ctx, c_total;
     size_t ckv_unit;  // bytes of one unit's context K and V^T
@@ -40,6 +40,7 @@ namespace sgd {
 
 size_t align256(size_t x);
 bool arch_gated(int arch);
+bool arch_cross(int arch);  // SDXL-style units with a cross-attention branch
 
 // Drift recording of one step (the input-aware baseline): for every unit, the squared norm
 // of the change of its input since the previous recorded step and the squared norm of the

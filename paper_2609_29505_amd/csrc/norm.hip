@@ -125,4 +125,112 @@ hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t st) {
     return (a.d / 4) % 128 == 0 ? launch_norm_wpr<2>(dtype, a, st) : launch_norm_wpr<1>(dtype, a, st);
 }
 
+// GroupNorm + SiLU of the SDXL UNet ResNet blocks, y = SiLU(GN(x) w + b) in bf16 for x
+// [B, N, C] (the fp32 stream or a bf16 convolution output), in three launches with coalesced
+// rows: (1) per block of kGnRows positions, a workgroup of C / 4 threads (thread t owns
+// channels 4t .. 4t+3, all in one group) sums x and x^2 over its rows and combines the
+// threads of each group in a fixed order into fp64 partials; (2) one thread per (sample,
+// group) adds the partials in order and forms the mean and 1 / sqrt(biased variance + eps);
+// (3) the same row blocks normalise, apply the gain and shift, SiLU, and store bf16.
+template <typename TI>
+__device__ __forceinline__ float4 ld4_any(const TI* p);
+template <>
+__device__ __forceinline__ float4 ld4_any<float>(const float* p) { return *(const float4*)p; }
+template <>
+__device__ __forceinline__ float4 ld4_any<bf16>(const bf16* p) {
+    const bf16x4 v = *(const bf16x4*)p;
+    return make_float4(bf2f(v[0]), bf2f(v[1]), bf2f(v[2]), bf2f(v[3]));
+}
+
+constexpr int kGnRows = 16;
+
+template <typename TI>
+__global__ __launch_bounds__(1024) void gn_partial_kernel(GroupNormArgs a, double* partial) {
+    const int nblk = (a.N + kGnRows - 1) / kGnRows;
+    const int b = blockIdx.x / nblk, blk = blockIdx.x - b * nblk;
+    const int t = threadIdx.x, q4 = (a.C / a.groups) / 4;  // channel quads per group
+    const TI* x = (const TI*)a.x + ((long)b * a.N + (long)blk * kGnRows) * a.C + 4 * t;
+    const int rows = min(kGnRows, a.N - blk * kGnRows);
+    float s = 0.f, ss = 0.f;
+    for (int r = 0; r < rows; ++r) {
+        const float4 v = ld4_any<TI>(x + (long)r * a.C);
+        s += (v.x + v.y) + (v.z + v.w);
+        ss += (v.x * v.x + v.y * v.y) + (v.z * v.z + v.w * v.w);
+    }
+    extern __shared__ double red[];  // [C / 4][2]
+    red[2 * t] = s;
+    red[2 * t + 1] = ss;
+    __syncthreads();
+    if (t < a.groups) {
+        double gs = 0.0, gss = 0.0;
+        for (int i = 0; i < q4; ++i) {
+            gs += red[2 * (t * q4 + i)];
+            gss += red[2 * (t * q4 + i) + 1];
+        }
+        double* o = partial + (((long)b * nblk + blk) * a.groups + t) * 2;
+        o[0] = gs;
+        o[1] = gss;
+    }
+}
+
+__global__ __launch_bounds__(256) void gn_stats_kernel(GroupNormArgs a, const double* partial, float* stats) {
+    const int i = blockIdx.x * 256 + threadIdx.x;  // sample * groups + group
+    if (i >= a.B * a.groups) return;
+    const int b = i / a.groups, g = i - b * a.groups;
+    const int nblk = (a.N + kGnRows - 1) / kGnRows;
+    double s = 0.0, ss = 0.0;
+    for (int blk = 0; blk < nblk; ++blk) {
+        const double* p = partial + (((long)b * nblk + blk) * a.groups + g) * 2;
+        s += p[0];
+        ss += p[1];
+    }
+    const double cnt = (double)a.N * (a.C / a.groups);
+    const double mean = s / cnt;
+    const double var = fmax(ss / cnt - mean * mean, 0.0);
+    stats[2 * i] = (float)mean;
+    stats[2 * i + 1] = (float)(1.0 / sqrt(var + (double)a.eps));
+}
+
+template <typename TI>
+__global__ __launch_bounds__(1024) void gn_apply_kernel(GroupNormArgs a, const float* stats) {
+    const int nblk = (a.N + kGnRows - 1) / kGnRows;
+    const int b = blockIdx.x / nblk, blk = blockIdx.x - b * nblk;
+    const int t = threadIdx.x, cg = a.C / a.groups, c = 4 * t, g = c / cg;
+    const float mean = stats[2 * (b * a.groups + g)], rstd = stats[2 * (b * a.groups + g) + 1];
+    const float4 ww = *(const float4*)(a.w + c), bv = *(const float4*)(a.b + c);
+    const long off = ((long)b * a.N + (long)blk * kGnRows) * a.C + c;
+    const TI* x = (const TI*)a.x + off;
+    bf16* y = (bf16*)a.y + off;
+    const int rows = min(kGnRows, a.N - blk * kGnRows);
+    for (int r = 0; r < rows; ++r) {
+        const float4 v = ld4_any<TI>(x + (long)r * a.C);
+        bf16x4 o;
+        o[0] = f2bf(silu((v.x - mean) * rstd * ww.x + bv.x));
+        o[1] = f2bf(silu((v.y - mean) * rstd * ww.y + bv.y));
+        o[2] = f2bf(silu((v.z - mean) * rstd * ww.z + bv.z));
+        o[3] = f2bf(silu((v.w - mean) * rstd * ww.w + bv.w));
+        *(bf16x4*)(y + (long)r * a.C) = o;
+    }
+}
+
+size_t group_norm_scratch_bytes(int B, int N, int groups) {
+    const int nblk = (N + kGnRows - 1) / kGnRows;
+    return (size_t)B * nblk * groups * 2 * sizeof(double) + (size_t)B * groups * 2 * sizeof(float);
+}
+
+hipError_t launch_group_norm_silu(int in_bf16, const GroupNormArgs& a, void* scratch, hipStream_t st) {
+    const int nblk = (a.N + kGnRows - 1) / kGnRows;
+    double* partial = (double*)scratch;
+    float* stats = (float*)(partial + (size_t)a.B * nblk * a.groups * 2);
+    const dim3 rows(a.B * nblk), threads(a.C / 4);
+    const size_t lds = (size_t)(a.C / 4) * 2 * sizeof(double);
+    if (in_bf16) hipLaunchKernelGGL(gn_partial_kernel<bf16>, rows, threads, lds, st, a, partial);
+    else hipLaunchKernelGGL(gn_partial_kernel<float>, rows, threads, lds, st, a, partial);
+    hipLaunchKernelGGL(gn_stats_kernel, dim3((a.B * a.groups + 255) / 256), dim3(256), 0, st, a,
+                       (const double*)partial, stats);
+    if (in_bf16) hipLaunchKernelGGL(gn_apply_kernel<bf16>, rows, threads, 0, st, a, (const float*)stats);
+    else hipLaunchKernelGGL(gn_apply_kernel<float>, rows, threads, 0, st, a, (const float*)stats);
+    return hipGetLastError();
+}
+
 }  // namespace sgd

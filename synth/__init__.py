@@ -37,7 +37,7 @@ import numpy as np
 # workload configurations
 # --------------------------------------------------------------------------
 
-ARCH_IDS = {"tiny": 0, "llada": 1, "dit": 2, "uvit": 3, "sdxl": 4}
+ARCH_IDS = {"tiny": 0, "llada": 1, "dit": 2, "uvit": 3, "sdxl": 4, "sdxl_unet": 5}
 
 
 @dataclass(frozen=True)
@@ -58,6 +58,8 @@ class Config:
     ctx_dim: int = 0     # SDXL context width
     prompt_rows: int = 0 # LLaDA: leading rows per sample that the sampler never updates
     cfg_id: int = 0      # seed domain
+    grid: int = 0        # SDXL UNet units: side of the square latent grid (N = grid^2)
+    groups: int = 32     # SDXL UNet units: GroupNorm groups
 
     @property
     def M(self) -> int:
@@ -65,7 +67,7 @@ class Config:
 
     @property
     def gated(self) -> bool:
-        return self.arch in ("llada", "sdxl")
+        return self.arch in ("llada", "sdxl", "sdxl_unet")
 
     @property
     def update_rows(self) -> Tuple[int, int]:
@@ -86,6 +88,10 @@ CONFIGS: Dict[str, Config] = {
     "uvit": Config("uvit", "uvit", "bf16", 32, 258, 1024, 16, 64, 4096, 21, 50, (50,), cfg_id=3),
     "sdxl": Config("sdxl", "sdxl", "bf16", 8, 1024, 1280, 20, 64, 5120, 10, 50, (70, 50),
                    ctx_len=77, ctx_dim=2048, cfg_id=4),
+    # SDXL UNet stage units: a ResNet block (two 3x3 convolutions on the 32 x 32 latent grid)
+    # followed by the spatial transformer block, scored as one unit
+    "sdxl_unet": Config("sdxl_unet", "sdxl_unet", "bf16", 8, 1024, 1280, 20, 64, 5120, 10, 50, (70, 50),
+                        ctx_len=77, ctx_dim=2048, cfg_id=5, grid=32, groups=32),
     # reduced shapes of the same architectures: several tiles plus ragged
     # tails, small enough for the CPU oracle to run whole trajectories
     "tiny_ragged": Config("tiny_ragged", "tiny", "f32", 2, 72, 128, 2, 64, 256, 3, 6, (50,), cfg_id=10),
@@ -95,6 +101,8 @@ CONFIGS: Dict[str, Config] = {
     "uvit_mini": Config("uvit_mini", "uvit", "bf16", 2, 66, 256, 4, 64, 512, 5, 8, (50,), cfg_id=13),
     "sdxl_mini": Config("sdxl_mini", "sdxl", "bf16", 2, 96, 256, 4, 64, 512, 3, 8, (50,),
                         ctx_len=77, ctx_dim=384, cfg_id=14),
+    "sdxl_unet_mini": Config("sdxl_unet_mini", "sdxl_unet", "bf16", 2, 100, 256, 4, 64, 512, 3, 8, (50,),
+                             ctx_len=77, ctx_dim=384, cfg_id=15, grid=10, groups=32),
 }
 
 
@@ -151,7 +159,7 @@ def representable(x: np.ndarray, dtype: str) -> np.ndarray:
 
 _DENSE_MAX = 512
 ROLE_IDS = {"q": 0, "k": 1, "v": 2, "o": 3, "w1": 4, "w2": 5, "ada": 6, "skip": 7,
-            "xq": 8, "xk": 9, "xv": 10, "xo": 11}
+            "xq": 8, "xk": 9, "xv": 10, "xo": 11, "conv1": 12, "conv2": 13, "temb": 14}
 
 
 def _rng(cfg_id: int, stream: int, unit: int, role: int, sub: int = 0) -> np.random.Generator:
@@ -284,7 +292,7 @@ def unit_weights(cfg: Config, unit: int, keep_planted: bool = False) -> Dict[str
     arch = cfg.arch
     out["norm1_w"] = _gain(prm, d, dt)
     out["norm2_w"] = _gain(prm, d, dt)
-    if arch in ("uvit", "sdxl"):
+    if arch in ("uvit", "sdxl", "sdxl_unet"):
         out["norm1_b"] = _bias(prm, d, dt)
         out["norm2_b"] = _bias(prm, d, dt)
     if arch == "dit":
@@ -293,14 +301,30 @@ def unit_weights(cfg: Config, unit: int, keep_planted: bool = False) -> Dict[str
         out["b_qkv"] = _bias(prm, 3 * d, dt)
         out["w_ada"] = mat("ada", 6 * d, d)
         out["b_ada"] = _bias(prm, 6 * d, dt)
-    if arch in ("dit", "uvit", "sdxl"):
+    if arch in ("dit", "uvit", "sdxl", "sdxl_unet"):
         out["b_o"] = _bias(prm, d, dt)
         out["b1"] = _bias(prm, 2 * F if cfg.gated else F, dt)
         out["b2"] = _bias(prm, d, dt)
     if arch == "uvit" and unit > cfg.L // 2:
         out["w_skip"] = mat("skip", d, 2 * d)
         out["b_skip"] = _bias(prm, d, dt)
-    if arch == "sdxl":
+    if arch == "sdxl_unet":
+        # ResNet block: GroupNorm, SiLU, 3x3 convolution (+ time-embedding projection),
+        # GroupNorm, SiLU, 3x3 convolution.  A convolution kernel is stored unfolded as
+        # [C_out, 9 C_in] with column (3 ky + kx) C_in + c_in (tap-major, channels contiguous);
+        # it is planted as that unfolded matrix.
+        rrm = _rng(cfg.cfg_id, STREAM_WEIGHTS, unit, 101)
+        out["gn1_w"] = _gain(rrm, d, dt)
+        out["gn1_b"] = _bias(rrm, d, dt)
+        out["w_conv1"] = mat("conv1", d, 9 * d)
+        out["b_conv1"] = _bias(rrm, d, dt)
+        out["w_temb"] = mat("temb", d, d)
+        out["b_temb"] = _bias(rrm, d, dt)
+        out["gn2_w"] = _gain(rrm, d, dt)
+        out["gn2_b"] = _bias(rrm, d, dt)
+        out["w_conv2"] = mat("conv2", d, 9 * d)
+        out["b_conv2"] = _bias(rrm, d, dt)
+    if arch in ("sdxl", "sdxl_unet"):
         out["normx_w"] = _gain(prm, d, dt)
         out["normx_b"] = _bias(prm, d, dt)
         out["w_xq"] = mat("xq", d, d)
@@ -373,9 +397,9 @@ def inputs(cfg: Config) -> Dict[str, np.ndarray]:
         z = rng.standard_normal((B, N, d)).astype(np.float32)
     out["z"] = np.ascontiguousarray(z.astype(np.float32))
     crng = _rng(cfg.cfg_id, STREAM_COND, 0, 0)
-    if cfg.arch == "dit":
+    if cfg.arch in ("dit", "sdxl_unet"):
         out["class_emb"] = crng.standard_normal((B, d)).astype(np.float32)
-    if cfg.arch == "sdxl":
+    if cfg.arch in ("sdxl", "sdxl_unet"):
         ctx = crng.standard_normal((cfg.ctx_len, cfg.ctx_dim))
         out["ctx"] = np.ascontiguousarray(np.broadcast_to(store(ctx, cfg.dtype)[None],
                                                           (B, cfg.ctx_len, cfg.ctx_dim)))

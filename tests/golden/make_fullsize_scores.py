@@ -21,7 +21,7 @@ import synth  # noqa: E402
 from oracle import spectral as sp  # noqa: E402
 
 ETA = 1e-6
-WORKLOADS = ["tiny", "dit", "uvit", "sdxl", "llada"]
+WORKLOADS = ["tiny", "dit", "uvit", "sdxl", "llada", "sdxl_unet"]
 
 
 def write(name: str) -> None:

@@ -23,9 +23,9 @@ def test_exports_match_header():
     _lib_or_skip()
     import subprocess
     hdr = open(os.path.join(ROOT, "include", "sgd.h")).read() + open(os.path.join(ROOT, "include", "sgd_ops.h")).read()
-    declared = set(re.findall(r"\b(sgd_[a-z_]+)\s*\(", hdr))
+    declared = set(re.findall(r"\b(sgd_[a-z_0-9]+)\s*\(", hdr))
     out = subprocess.run(["nm", "-D", "--defined-only", P.lib_path], capture_output=True, text=True).stdout
-    exported = set(re.findall(r"\bT (sgd_[a-z_]+)\b", out))
+    exported = set(re.findall(r"\bT (sgd_[a-z_0-9]+)\b", out))
     assert declared, "no declarations found"
     assert declared <= exported, f"declared but not exported: {declared - exported}"
     assert set(P.binding.EXPORTS) <= exported

@@ -12,7 +12,7 @@ from oracle import spectral as osp
 
 from helpers import load_fullsize_golden
 
-NAMES = ["tiny", "dit", "uvit", "sdxl", "llada"]
+NAMES = ["tiny", "dit", "uvit", "sdxl", "llada", "sdxl_unet"]
 
 
 @pytest.mark.parametrize("name", NAMES)
@@ -20,7 +20,8 @@ def test_golden_consistent(name):
     cfg = synth.get_config(name)
     stats, raw = load_fullsize_golden(name)
     assert len(stats) == len(raw) == cfg.L
-    want = {"q", "k", "v", "o", "w1", "w2"} | ({"xq", "xk", "xv", "xo"} if cfg.arch == "sdxl" else set())
+    want = {"q", "k", "v", "o", "w1", "w2"} | ({"xq", "xk", "xv", "xo"} if cfg.arch in ("sdxl", "sdxl_unet") else set())
+    want |= {"conv1", "conv2"} if cfg.arch == "sdxl_unet" else set()
     for u in stats:
         assert set(u) == want
         for st in u.values():

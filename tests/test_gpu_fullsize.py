@@ -23,7 +23,7 @@ from helpers import TOL, load_fullsize_golden, rel_err
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
-FULL = ["tiny", "dit", "uvit", "sdxl", "llada"]
+FULL = ["tiny", "dit", "uvit", "sdxl", "llada", "sdxl_unet"]
 
 
 def progress(msg):
@@ -65,7 +65,7 @@ def test_fullsize_step_parity(P, name):
     sched = P.schedule_from_lifetimes(S, T)
     # GPU: step 1 from z0; step 2 from the oracle's z_2 with the GPU's own cache
     m = om.Model(cfg, w, x, lazy=(cfg.name == "llada"))
-    cross = [m.cross_kv(u) for u in m.units] if cfg.arch == "sdxl" else None
+    cross = [m.cross_kv(u) for u in m.units] if cfg.arch in om.CROSS_ARCHS else None
     cache = P.Cache(dm)
     cache.reset()
     z = torch.from_numpy(x["z"].copy()).cuda()
@@ -97,7 +97,7 @@ def test_fullsize_step_parity(P, name):
     dm.close()
 
 
-@pytest.mark.parametrize("name", ["tiny", "dit", "uvit", "sdxl", "llada"])
+@pytest.mark.parametrize("name", FULL)
 def test_fullsize_schedule(P, name):
     """The GPU's scores and schedules at full size against the oracle's stored statistics
     (tests/golden/fullsize_<workload>.txt, written by the oracle alone): every matrix's E_k,
@@ -116,7 +116,11 @@ def test_fullsize_schedule(P, name):
     # every matrix against the oracle's statistics
     row = 0
     for l, mats in enumerate(units):
+        nconv = 0
         for role, _ in mats:
+            if role == "conv":  # the unit's convolutions, in order
+                nconv += 1
+                role = f"conv{nconv}"
             ref = gstats[l][role]
             got = sched.mat_stats[row]
             row += 1
