@@ -294,6 +294,24 @@ typedef struct {
 int sgd_denoise_step(sgd_model* model, void* state, int32_t step, const sgd_schedule* sched,
                      sgd_cache* cache, const sgd_step_args* args, void* hip_stream);
 
+/* ---------------------------------------------------------- no allocation */
+
+/* Size of the library's fixed device scratch: 96 MiB, held by every GPU the library runs on
+ * until the process ends. */
+#define SGD_SCRATCH_BYTES (96u * 1024u * 1024u)
+
+/* sgd_denoise_step for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the step's workspace is
+ * the library's fixed scratch instead of a caller buffer, and the call allocates nothing
+ * (no hipMalloc, no hipFree).  The caller still passes the state, the schedule and the
+ * cache.  A model whose sgd_workspace_bytes exceeds SGD_SCRATCH_BYTES is refused with
+ * SGD_E_ARG (the LLaDA-8B-shaped workload needs about 84 MB and fits; the 8192-row
+ * workloads do not).  No part of the scratch needs to start at any particular value: every
+ * step writes each workspace region before reading it.  All calls on one GPU share its
+ * scratch, so calls that overlap in time on one GPU (other streams, other threads) race. */
+int sgd_denoise_step_noalloc(sgd_model* model, void* state, int32_t step, const sgd_schedule* sched,
+                             sgd_cache* cache, float alpha, float beta, void* hip_stream);
+
 /* -------------------------------------------------- input-aware baselines */
 
 /* One step with an arbitrary set of active units (Alg. 2 with a per-step active set that

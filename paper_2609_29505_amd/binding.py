@@ -90,7 +90,7 @@ EXPORTS = ["sgd_last_error", "sgd_version", "sgd_s_min_default", "sgd_budget_lay
            "sgd_schedule_from_stats",
            "sgd_schedule_from_lifetimes", "sgd_model_create", "sgd_model_destroy", "sgd_workspace_bytes",
            "sgd_cache_bytes", "sgd_cache_bind", "sgd_cache_reset", "sgd_cache_destroy", "sgd_denoise_step",
-           "sgd_denoise_step_masked", "sgd_drift_bytes", "sgd_drift_step", "sgd_replay_bytes", "sgd_replay_search",
+           "sgd_denoise_step_noalloc", "sgd_denoise_step_masked", "sgd_drift_bytes", "sgd_drift_step", "sgd_replay_bytes", "sgd_replay_search",
            "sgd_profile_begin", "sgd_profile_end", "sgd_op_linear", "sgd_op_attention", "sgd_op_norm",
            "sgd_op_frozen_run", "sgd_op_heads", "sgd_op_residual", "sgd_op_adaln_mod", "sgd_op_group_norm_silu",
            "sgd_op_group_norm_scratch_bytes", "sgd_op_conv3x3"]
@@ -125,6 +125,7 @@ def lib() -> C.CDLL:
             "sgd_cache_destroy": [vp],
             "sgd_denoise_step": [vp, vp, i32, C.POINTER(sgd_schedule), vp, C.POINTER(sgd_step_args), vp],
             "sgd_denoise_step_masked": [vp, vp, i32, C.POINTER(C.c_uint8), vp, C.POINTER(sgd_step_args), vp],
+            "sgd_denoise_step_noalloc": [vp, vp, i32, C.POINTER(sgd_schedule), vp, C.c_float, C.c_float, vp],
             "sgd_drift_bytes": [vp, C.POINTER(C.c_size_t)],
             "sgd_drift_step": [vp, vp, i32, C.POINTER(sgd_schedule), vp, C.POINTER(sgd_step_args), vp, C.c_size_t,
                                C.POINTER(C.c_uint8), C.POINTER(C.c_double), vp],
@@ -489,6 +490,15 @@ class DeviceModel:
         a.workspace = self.workspace.data_ptr()
         a.workspace_bytes = self.workspace.numel()
         return a
+
+    def step_noalloc(self, state, s: int, sched: Optional[Schedule], cache: Optional["Cache"], alpha=1.0, beta=None,
+                     stream=None) -> None:
+        """sgd_denoise_step on the library's fixed scratch (no workspace, no allocation)."""
+        beta = (1.0 / self.cfg.T) if beta is None else beta
+        _check(lib().sgd_denoise_step_noalloc(self.h, C.c_void_p(state.data_ptr()), s,
+                                              C.byref(sched.c) if sched is not None else None,
+                                              cache.h if cache is not None else None, alpha, beta,
+                                              C.c_void_p(_stream_ptr(stream))))
 
     def step_masked(self, state, s: int, active_row, cache: "Cache", alpha=1.0, beta=None, stream=None) -> None:
         """One step with an arbitrary active set (``active_row``: L flags)."""

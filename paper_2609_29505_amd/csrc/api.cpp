@@ -8,6 +8,7 @@
 // because that is the update every later frozen step reads (r_l(s) = S_l).
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -607,6 +608,55 @@ extern "C" int sgd_denoise_step_masked(sgd_model* m, void* state, int32_t step, 
     if (!active) return fail(SGD_E_ARG, "NULL active row");
     if ((rc = check_cache(m, cache, step))) return rc;
     return masked_step(m, state, step, active, cache, args, nullptr, (hipStream_t)hip_stream);
+}
+
+// ---------------------------------------------------------------------------- no allocation
+
+// The allocation-free step: its workspace is this file-scope device array instead of a
+// caller buffer.  Each GPU the library runs on holds its own copy until the process ends;
+// host code never uses the array's name as an address (it is a host-side stand-in), only
+// the per-device address hipGetSymbolAddress returns.
+static __device__ __align__(256) char scratch[SGD_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// The current device's address of `scratch`, looked up once per device (that device current).
+int scratch_address(void** out) {
+    int dev = 0;
+    SGD_HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(SGD_E_ARG, "device index beyond the scratch table");
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void* p = nullptr;
+        hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!p) return fail(SGD_E_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return SGD_OK;
+}
+}  // namespace
+
+extern "C" int sgd_denoise_step_noalloc(sgd_model* m, void* state, int32_t step, const sgd_schedule* sched,
+                                        sgd_cache* cache, float alpha, float beta, void* hip_stream) {
+    if (!m) return fail(SGD_E_ARG, "NULL model");
+    if (m->w_total > (size_t)SGD_SCRATCH_BYTES)
+        return fail(SGD_E_ARG, "the model's step workspace (" + std::to_string(m->w_total) +
+                                   " bytes) exceeds the fixed scratch of " + std::to_string((size_t)SGD_SCRATCH_BYTES) +
+                                   " bytes; use sgd_denoise_step with a workspace");
+    void* ws = nullptr;
+    int rc = scratch_address(&ws);
+    if (rc) return rc;
+    sgd_step_args a;
+    a.alpha = alpha;
+    a.beta = beta;
+    a.workspace = ws;
+    a.workspace_bytes = (size_t)SGD_SCRATCH_BYTES;
+    return sgd_denoise_step(m, state, step, sched, cache, &a, hip_stream);
 }
 
 // ---------------------------------------------------------------------------- single ops
