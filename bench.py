@@ -55,28 +55,43 @@ def unit_flops(cfg) -> dict:
     return f
 
 
-def frozen_launch_bytes(cfg, active_row) -> list:
-    """Algorithmic HBM bytes of every frozen-run launch of one step (Sec. 3.1 frozen rule).
+def frozen_launches(cfg, active_row):
+    """Algorithmic HBM bytes of every launch of one step that carries frozen units (Sec. 3.1
+    frozen rule), as (standalone frozen-run launches, pre-norms that absorbed a run).
 
     The launcher fuses a maximal run of consecutive frozen units (at most MAX_RUN; U-ViT
     out-blocks, whose skip linear always runs, end a run) into one pass that reads h and the
     r cached updates and writes h: (2 + r) M d fp32 values, plus, for U-ViT in-blocks, a
-    bf16 copy of h after every unit of the run (the long-skip inputs)."""
+    bf16 copy of h after every unit of the run (the long-skip inputs).  A run that ends at an
+    active unit starting with its pre-norm (not a U-ViT out-block, not a UNet unit, no copies)
+    is added by that norm instead, which also writes the normalised rows: (2 + r) M d 4 +
+    M d (element size) bytes."""
     L = cfg.L
     es = 2 if cfg.dtype == "bf16" else 4
     half = L // 2
-    out, l = [], 0
+    uvit = cfg.arch == "uvit"
+    alone, folded, l = [], [], 0
     while l < L:
-        if active_row[l] or (cfg.arch == "uvit" and l > half):
+        if active_row[l] or (uvit and l > half):
             l += 1
             continue
         r = 0
-        while l < L and not active_row[l] and not (cfg.arch == "uvit" and l > half) and r < MAX_RUN:
+        while l < L and not active_row[l] and not (uvit and l > half) and r < MAX_RUN:
             r += 1
             l += 1
-        snaps = r if cfg.arch == "uvit" else 0
-        out.append((2 + r) * cfg.M * cfg.d * 4 + snaps * cfg.M * cfg.d * es)
-    return out
+        snaps = r if uvit else 0  # U-ViT: every unit up to the mid block copies h out
+        fold = (not snaps and l < L and active_row[l] and not (uvit and l > half)
+                and cfg.arch != "sdxl_unet")
+        if fold:
+            folded.append((2 + r) * cfg.M * cfg.d * 4 + cfg.M * cfg.d * es)
+        else:
+            alone.append((2 + r) * cfg.M * cfg.d * 4 + snaps * cfg.M * cfg.d * es)
+    return alone, folded
+
+
+def frozen_launch_bytes(cfg, active_row) -> list:
+    """Bytes of the standalone frozen-run launches of one step (see frozen_launches)."""
+    return frozen_launches(cfg, active_row)[0]
 
 
 def main() -> int:
@@ -241,6 +256,7 @@ def main() -> int:
     # per-launch events: the frozen-run kernel in the headline schedule (the all-active
     # schedule has none), the profiled kernel class in the all-active schedule
     ms_fz, prof_fz = timed(scheds[head], "frozen")
+    _, prof_fold = timed(scheds[head], "fold")
     ms_pk, prof_all = timed(all_active, args.profile_kernel)
     log(f"profiled runs: headline with frozen-run events {np.median(ms_fz):.2f} ms, all-active with "
         f"{args.profile_kernel} events {np.median(ms_pk):.2f} ms per trajectory")
@@ -323,14 +339,27 @@ def main() -> int:
     timed_rows = np.concatenate([act] * n_traj)
     active_frac = float(timed_rows.mean())
     mean_active = float(timed_rows.sum(axis=1).mean())
-    # frozen path: algorithmic bytes of every frozen-run launch of the timed steps / their time
-    fbytes = sum(sum(frozen_launch_bytes(cfg, row)) for row in timed_rows)
+    # frozen path: algorithmic bytes of every launch that carries frozen units in the timed
+    # steps (standalone frozen runs and pre-norms that absorbed a run) / their time
+    fl = [frozen_launches(cfg, row) for row in timed_rows]
+    b_alone = sum(sum(a) for a, _ in fl)
+    b_fold = sum(sum(f) for _, f in fl)
+    n_alone_want = sum(len(a) for a, _ in fl)
+    n_fold_want = sum(len(f) for _, f in fl)
     fms, fn = prof_fz if prof_fz else (0.0, 0)
+    fdms, fdn = prof_fold if prof_fold else (0.0, 0)
     frozen = None
-    if fn:
-        frozen = {"bound": "hbm", "kernel": "frozen_run", "achieved": fbytes / (fms / 1000.0) / 1e9,
-                  "peak": PEAK_HBM / 1e9, "unit": "GB/s", "frac": fbytes / (fms / 1000.0) / PEAK_HBM,
-                  "launches": fn, "avg_launch_us": fms * 1000.0 / fn, "bytes": fbytes,
+    if fn or fdn:
+        tot_b, tot_s = b_alone + b_fold, (fms + fdms) / 1000.0
+        frozen = {"bound": "hbm", "kernel": "frozen_run + pre-norms that absorb a frozen run",
+                  "achieved": tot_b / tot_s / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                  "frac": tot_b / tot_s / PEAK_HBM, "bytes": tot_b,
+                  "standalone": {"launches": fn, "expected": n_alone_want, "bytes": b_alone,
+                                 "avg_launch_us": fms * 1000.0 / fn if fn else None,
+                                 "GB/s": b_alone / (fms / 1000.0) / 1e9 if fn else None},
+                  "folded_into_norm": {"launches": fdn, "expected": n_fold_want, "bytes": b_fold,
+                                       "avg_launch_us": fdms * 1000.0 / fdn if fdn else None,
+                                       "GB/s": b_fold / (fdms / 1000.0) / 1e9 if fdn else None},
                   "note": "h and the cached updates; h may be served from the 256 MB Infinity Cache"}
     tr = committed_traffic(kern, cfg)
     roofline["traffic"] = tr["total_bytes"] if tr else None

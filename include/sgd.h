@@ -387,7 +387,9 @@ enum sgd_kernel_class {
     SGD_K_NORM = 0, SGD_K_GEMM_QKV = 1, SGD_K_ATTN = 2, SGD_K_GEMM_O = 3,
     SGD_K_GEMM_W1 = 4, SGD_K_GEMM_W2 = 5, SGD_K_FROZEN = 6, SGD_K_STATE = 7,
     SGD_K_COND = 8, SGD_K_GEMM_SKIP = 9, SGD_K_GEMM_X = 10, SGD_K_ATTN_X = 11,
-    SGD_K_DRIFT = 12, SGD_K_GEMM_CONV = 13, SGD_K_GNORM = 14, SGD_K_COUNT = 15
+    SGD_K_DRIFT = 12, SGD_K_GEMM_CONV = 13, SGD_K_GNORM = 14,
+    SGD_K_FOLD = 15, /* a pre-norm that also adds the frozen run ending at its unit */
+    SGD_K_COUNT = 16
 };
 
 /* Start timing every launch of kernel class `kclass` (or -1 to stop): the launcher records

@@ -20,7 +20,7 @@ SGD_RULE = {"scr_frob": 0, "random": 1, "depth": 2, "frob": 3, "spectral": 4, "s
             "frob_srank": 6, "raw_scr": 7}
 SGD_ROLE = {"q": 0, "k": 1, "v": 2, "o": 3, "xq": 4, "xk": 5, "xv": 6, "xo": 7, "w1": 8, "w2": 9, "conv": 10}
 SGD_K = {"norm": 0, "gemm_qkv": 1, "attn": 2, "gemm_o": 3, "gemm_w1": 4, "gemm_w2": 5, "frozen": 6,
-         "state": 7, "cond": 8, "gemm_skip": 9, "gemm_x": 10, "attn_x": 11, "drift": 12, "gemm_conv": 13, "gnorm": 14}
+         "state": 7, "cond": 8, "gemm_skip": 9, "gemm_x": 10, "attn_x": 11, "drift": 12, "gemm_conv": 13, "gnorm": 14, "fold": 15}
 ERRORS = {-1: "SGD_E_ARG", -2: "SGD_E_SHAPE", -3: "SGD_E_DTYPE", -4: "SGD_E_BUDGET", -5: "SGD_E_STEP",
           -6: "SGD_E_CACHE", -7: "SGD_E_HIP", -8: "SGD_E_NUMERIC"}
 

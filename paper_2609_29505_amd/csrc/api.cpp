@@ -352,9 +352,16 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
     if (sdxl && plan.ckv && plan.ckv_fill)
         for (int l = 0; l < L; ++l) ctx_kv(l, plan.ckv + (size_t)l * m->ckv_unit);
 
+    // a frozen run that ends at an active unit is added by that unit's first norm kernel
+    // (same additions, same order) instead of a pass of its own
+    std::vector<const float*> fold;
     auto norm = [&](const float* w, const float* b, const float* shift, const float* scale) {
         NormArgs a{h, xb, (int)M, dd, norm_kind, norm_eps, w, b, shift, scale, 6L * dd, N};
-        S.run(SGD_K_NORM, [&] { return launch_norm(dt, a, S.st); });
+        a.nfold = (int)fold.size();
+        for (int i = 0; i < a.nfold; ++i) a.fold[i] = fold[i];
+        const int kclass = fold.empty() ? SGD_K_NORM : SGD_K_FOLD;
+        fold.clear();
+        S.run(kclass, [&] { return launch_norm(dt, a, S.st); });
     };
     auto resid = [&](int kclass, const void* A, long lda, int K, const void* W, const void* bias, const float* gate,
                      float* dlt, int dmode, void* hcopy) {
@@ -398,11 +405,20 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
             fr.h = h; fr.n = (long)Md; fr.r = 0; fr.snap_bf16 = dt;
             const int cap = dr ? 1 : kMaxRun;
             if (dr) record_drift(l);
+            bool snaps = false;
             while (l < L && !act[l] && !(uvit && l > half) && fr.r < cap) {
                 fr.delta[fr.r] = plan.dread[l];
                 fr.snap[fr.r] = out_copy(l);
+                snaps = snaps || fr.snap[fr.r];
                 fr.r++;
                 ++l;
+            }
+            // handed to the next unit's first norm when that unit computes and starts with one
+            // (not a U-ViT out-block, whose skip linear reads h first; not a UNet unit, whose
+            // ResNet block starts with GroupNorm), and no unit of the run copies h out
+            if (!dr && !snaps && l < L && act[l] && !(uvit && l > half) && !unet) {
+                fold.assign(fr.delta, fr.delta + fr.r);
+                continue;
             }
             S.run(SGD_K_FROZEN, [&] { return launch_frozen_run(fr, S.st); });
             continue;

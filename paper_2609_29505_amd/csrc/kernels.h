@@ -69,11 +69,17 @@ struct AttnArgs {
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t st);
 
 // ---------------------------------------------------------------- norms
-// kind 0: RMSNorm(w), 1: LayerNorm(w, b), 2: LayerNorm (no affine) * (1 + scale_b) + shift_b
+constexpr int kMaxRun = 32;  // frozen units fused into one pass at most
+// kind 0: RMSNorm(w), 1: LayerNorm(w, b), 2: LayerNorm (no affine) * (1 + scale_b) + shift_b.
+// nfold > 0: x is the fp32 stream h of the rows and a run of frozen units ends here: the kernel
+// first forms h <- ((h + fold[0]) + fold[1]) + ... (the frozen-run update, same order), writes
+// it back to x, then normalises it.
 struct NormArgs {
     const float* x; void* y; int M, d, kind; float eps;
     const float* w; const float* b;
     const float* shift; const float* scale; long mod_ld; int ntok;
+    int nfold = 0;
+    const float* fold[kMaxRun] = {};
 };
 hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t st);
 // y = SiLU(GroupNorm(x) w + b) in bf16 for x [B, N, C] fp32 (in_bf16 = 0) or bf16; groups of
@@ -88,7 +94,6 @@ size_t group_norm_scratch_bytes(int B, int N, int groups);
 hipError_t launch_group_norm_silu(int in_bf16, const GroupNormArgs& a, void* scratch, hipStream_t st);
 
 // ---------------------------------------------------------------- elementwise
-constexpr int kMaxRun = 32;
 struct FrozenRun {
     float* h; long n;  // elements
     int r;

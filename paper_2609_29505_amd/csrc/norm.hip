@@ -37,7 +37,7 @@ __device__ __forceinline__ float row_sum(float v, float* red) {
     return t;
 }
 
-template <typename OutT, int VPL, int WPR>
+template <typename OutT, int VPL, int WPR, bool FOLD>
 __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
     constexpr int TPR = 64 * WPR;  // threads per row
     __shared__ float red[4];
@@ -52,9 +52,34 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
     for (int i = 0; i < VPL; ++i) {
         const int c = t + i * TPR;
         v[i] = (live && c < nvec) ? ((const float4*)x)[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    if (FOLD && live) {
+        // the frozen run ending at this unit: its cached updates in stack order, written back
+        const long roff = (long)row * nvec;
+        for (int k = 0; k < a.nfold; ++k) {
+            const float4* dk = (const float4*)a.fold[k] + roff;
+#pragma unroll
+            for (int i = 0; i < VPL; ++i) {
+                const int c = t + i * TPR;
+                if (c < nvec) {
+                    const float4 dv = dk[c];
+                    v[i].x = v[i].x + dv.x;
+                    v[i].y = v[i].y + dv.y;
+                    v[i].z = v[i].z + dv.z;
+                    v[i].w = v[i].w + dv.w;
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < VPL; ++i) {
+            const int c = t + i * TPR;
+            if (c < nvec) ((float4*)x)[c] = v[i];
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < VPL; ++i)
         s += (a.kind == 0) ? (v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w)
                            : (v[i].x + v[i].y + v[i].z + v[i].w);
-    }
     s = row_sum<WPR>(s, red);
     const float invd = 1.0f / (float)a.d;
     float mean = 0.f, rstd;
@@ -101,11 +126,16 @@ template <int WPR>
 static hipError_t launch_norm_wpr(int dtype, const NormArgs& a, hipStream_t st) {
     const int vpl = (a.d / 4 + 64 * WPR - 1) / (64 * WPR);
     dim3 grid((a.M + (4 / WPR) - 1) / (4 / WPR)), block(256);
-#define NORM_CASE(V)                                                                              \
-    if (vpl <= V) {                                                                               \
-        if (dtype == 1) hipLaunchKernelGGL((norm_kernel<bf16, V, WPR>), grid, block, 0, st, a);  \
-        else hipLaunchKernelGGL((norm_kernel<float, V, WPR>), grid, block, 0, st, a);            \
-        return hipGetLastError();                                                                 \
+#define NORM_CASE(V)                                                                                       \
+    if (vpl <= V) {                                                                                        \
+        if (a.nfold > 0) {                                                                                 \
+            if (dtype == 1) hipLaunchKernelGGL((norm_kernel<bf16, V, WPR, true>), grid, block, 0, st, a);  \
+            else hipLaunchKernelGGL((norm_kernel<float, V, WPR, true>), grid, block, 0, st, a);            \
+        } else {                                                                                           \
+            if (dtype == 1) hipLaunchKernelGGL((norm_kernel<bf16, V, WPR, false>), grid, block, 0, st, a); \
+            else hipLaunchKernelGGL((norm_kernel<float, V, WPR, false>), grid, block, 0, st, a);           \
+        }                                                                                                  \
+        return hipGetLastError();                                                                          \
     }
     NORM_CASE(2)
     NORM_CASE(4)

@@ -8,7 +8,7 @@
 
 Prints the per-kernel statistics of the traced run and the frozen path's HBM rate from the
 trace's own durations: bench.py launches the budgets in increasing order, each as T warm-up
-steps and three timed T-step trajectories (then the all-active schedule, and the headline budget again
+steps and three timed T-step trajectories (then the all-active schedule, and the headline budget twice
 with per-launch events), so the frozen-run dispatches appear in a known order and each
 one's algorithmic bytes follow from the schedule (maximal runs of frozen units, as the
 launcher fuses them).
@@ -47,25 +47,34 @@ def kernel_stats(rows):
     return sorted(((k, g, n, t, t / n, 100.0 * t / tot) for (k, g), (n, t) in agg.items()), key=lambda x: -x[3])
 
 
-def frozen_rates(cfg, rows, lifetimes):
+def _is_fold(name: str) -> bool:
+    """A pre-norm kernel instantiated to absorb a frozen run (norm_kernel<..., true>)."""
+    return "norm_kernel" in name and "true>" in name
+
+
+def frozen_rates(cfg, rows, lifetimes, folded=False):
+    """Timed launches carrying frozen units per budget: standalone frozen-run kernels, or (with
+    ``folded``) the pre-norms that absorbed a run, matched to the schedule in dispatch order."""
     import numpy as np
 
     import bench
 
     T, L = cfg.T, cfg.L
     W, K = T, 3 * T  # bench.py's defaults: T warm-up steps, three whole trajectories
-    fr = sorted((r for r in rows if "frozen_run_kernel" in r["Kernel_Name"]), key=lambda r: int(r["Start_Timestamp"]))
+    match = _is_fold if folded else (lambda name: "frozen_run_kernel" in name)
+    fr = sorted((r for r in rows if match(r["Kernel_Name"])), key=lambda r: int(r["Start_Timestamp"]))
     i, out = 0, []
-    # the budgets in increasing order, then the headline (smallest) budget once more: the run
-    # in which bench.py records HIP events around every frozen-run launch (not reported here)
+    # the budgets in increasing order, then the headline (smallest) budget twice more: the runs
+    # in which bench.py records HIP events around the frozen-run and the folding pre-norm
+    # launches (not reported here)
     runs = sorted(cfg.budgets)
-    for k, pct in enumerate(runs + [runs[0]]):
+    for k, pct in enumerate(runs + [runs[0], runs[0]]):
         life = np.asarray(lifetimes[str(pct)])
         act = np.arange(1, T + 1)[:, None] <= life[None, :]
         nbytes, secs, n = 0, 0.0, 0
         for phase, steps in (("warmup", W), ("timed", K)):
             for j in range(steps):
-                for b in bench.frozen_launch_bytes(cfg, act[j % T]):
+                for b in bench.frozen_launches(cfg, act[j % T])[1 if folded else 0]:
                     r = fr[i]
                     i += 1
                     if phase == "timed":
@@ -75,7 +84,7 @@ def frozen_rates(cfg, rows, lifetimes):
         if k < len(runs):
             out.append((pct, n, nbytes, secs))
     if i != len(fr):
-        raise SystemExit(f"trace has {len(fr)} frozen-run dispatches, the schedules predict {i}")
+        raise SystemExit(f"trace has {len(fr)} matching dispatches, the schedules predict {i}")
     return out
 
 
@@ -93,10 +102,16 @@ def main() -> int:
     print("| kernel | grid (work-items) | calls | total ms | avg us | % |\n|---|---:|---:|---:|---:|---:|")
     for name, grid, n, t, avg, pc in kernel_stats(rows)[:14]:
         print(f"| `{name[:110]}` | {grid} | {n} | {t / 1e3:.1f} | {avg:.2f} | {pc:.2f} |")
-    print("\n| budget | timed frozen-run launches | GB | ms | GB/s | of 8 TB/s |\n|---:|---:|---:|---:|---:|---:|")
-    for pct, n, nbytes, secs in frozen_rates(cfg, rows, json.load(open(args.lifetimes))):
-        print(f"| {pct}% | {n} | {nbytes / 1e9:.2f} | {secs * 1e3:.2f} | {nbytes / secs / 1e9:.0f} | "
-              f"{nbytes / secs / 8e12:.3f} |")
+    lt = json.load(open(args.lifetimes))
+    print("\n| budget | launches | kind | GB | ms | GB/s | of 8 TB/s |\n|---:|---:|---|---:|---:|---:|---:|")
+    alone = frozen_rates(cfg, rows, lt)
+    fold = frozen_rates(cfg, rows, lt, folded=True)
+    for (pct, n, nb, sc), (_, n2, nb2, sc2) in zip(alone, fold):
+        for kind, cnt, byt, sec in (("standalone frozen runs", n, nb, sc), ("pre-norms absorbing a run", n2, nb2, sc2),
+                                    ("all launches with frozen units", n + n2, nb + nb2, sc + sc2)):
+            if cnt:
+                print(f"| {pct}% | {cnt} | {kind} | {byt / 1e9:.2f} | {sec * 1e3:.2f} | {byt / sec / 1e9:.0f} | "
+                      f"{byt / sec / 8e12:.3f} |")
     return 0
 
 

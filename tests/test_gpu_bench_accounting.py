@@ -1,6 +1,7 @@
 """bench.py's frozen-path accounting against the launches the library actually makes.
 
-`frozen_launch_bytes` predicts, from a schedule's active mask, every frozen-run launch of a
+`frozen_launches` predicts, from a schedule's active mask, every frozen-run launch and every
+pre-norm that absorbs a frozen run, of a
 step (maximal runs of frozen units, at most 32, ended by U-ViT out-blocks); the library's
 own profiler counts the frozen-run launches of the same steps.
 """
@@ -29,7 +30,7 @@ def P():
     return P
 
 
-@pytest.mark.parametrize("name", ["llada_mini", "uvit_mini"])
+@pytest.mark.parametrize("name", ["llada_mini", "uvit_mini", "dit_mini", "sdxl_unet_mini"])
 def test_frozen_launch_count(P, name):
     import torch
 
@@ -45,13 +46,18 @@ def test_frozen_launch_count(P, name):
     sched = P.schedule_from_lifetimes(lifetimes, cfg.T)
     z = torch.from_numpy(x["z"].copy()).cuda()
     cache = P.Cache(dm)
-    dm.profile_begin("frozen", 4096)
-    for s in range(1, cfg.T + 1):
-        dm.step(z, s, sched, cache)
-    torch.cuda.synchronize()
-    _, n = dm.profile_end()
+    counts = {}
+    for kclass in ("frozen", "fold"):
+        cache.reset()
+        z.copy_(torch.from_numpy(x["z"]))
+        dm.profile_begin(kclass, 4096)
+        for s in range(1, cfg.T + 1):
+            dm.step(z, s, sched, cache)
+        torch.cuda.synchronize()
+        counts[kclass] = dm.profile_end()[1]
     act = np.asarray(sched.active, bool)
-    want = sum(len(bench.frozen_launch_bytes(cfg, act[s])) for s in range(cfg.T))
-    assert want > 0
-    assert n == want
+    launches = [bench.frozen_launches(cfg, act[s]) for s in range(cfg.T)]
+    assert counts["frozen"] == sum(len(a) for a, _ in launches)
+    assert counts["fold"] == sum(len(f) for _, f in launches)
+    assert counts["frozen"] + counts["fold"] > 0
     dm.close()

@@ -89,13 +89,13 @@ def test_traffic_record_groups_split_launches(tmp_path):
 
 def _trace_rows(cfg, lifetimes, extra=0):
     """Frozen-run dispatches in bench.py's order: every budget (T warm-up + 3T timed steps), then
-    the headline budget once more; launch i lasts 1 + i ns."""
+    the headline budget twice more; launch i lasts 1 + i ns."""
     import bench
 
     T = cfg.T
     runs = sorted(cfg.budgets)
     rows, t = [], 0
-    for pct in runs + [runs[0]]:
+    for pct in runs + [runs[0], runs[0]]:
         act = np.arange(1, T + 1)[:, None] <= np.asarray(lifetimes[str(pct)])[None, :]
         for j in range(4 * T):
             for _ in bench.frozen_launch_bytes(cfg, act[j % T]):
