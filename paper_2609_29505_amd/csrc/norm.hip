@@ -159,9 +159,11 @@ hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t st) {
 // [B, N, C] (the fp32 stream or a bf16 convolution output), in three launches with coalesced
 // rows: (1) per block of kGnRows positions, a workgroup of C / 4 threads (thread t owns
 // channels 4t .. 4t+3, all in one group) sums x and x^2 over its rows and combines the
-// threads of each group in a fixed order into fp64 partials; (2) one thread per (sample,
-// group) adds the partials in order and forms the mean and 1 / sqrt(biased variance + eps);
-// (3) the same row blocks normalise, apply the gain and shift, SiLU, and store bf16.
+// threads of each group in a fixed order into fp64 partials; (2) one wave per (sample, group)
+// adds the partials (lane j takes blocks j, j + 64, ... in order, then a fixed butterfly over
+// the lanes) and forms the mean and 1 / sqrt(biased variance + eps); (3) the same row blocks
+// normalise, apply the gain and shift, SiLU, and store bf16.  Full row blocks unroll their
+// row loop, so every row's load is in flight at once.
 template <typename TI>
 __device__ __forceinline__ float4 ld4_any(const TI* p);
 template <>
@@ -182,10 +184,16 @@ __global__ __launch_bounds__(1024) void gn_partial_kernel(GroupNormArgs a, doubl
     const TI* x = (const TI*)a.x + ((long)b * a.N + (long)blk * kGnRows) * a.C + 4 * t;
     const int rows = min(kGnRows, a.N - blk * kGnRows);
     float s = 0.f, ss = 0.f;
-    for (int r = 0; r < rows; ++r) {
+    auto add = [&](int r) {
         const float4 v = ld4_any<TI>(x + (long)r * a.C);
         s += (v.x + v.y) + (v.z + v.w);
         ss += (v.x * v.x + v.y * v.y) + (v.z * v.z + v.w * v.w);
+    };
+    if (rows == kGnRows) {
+#pragma unroll
+        for (int r = 0; r < kGnRows; ++r) add(r);
+    } else {
+        for (int r = 0; r < rows; ++r) add(r);
     }
     extern __shared__ double red[];  // [C / 4][2]
     red[2 * t] = s;
@@ -204,16 +212,23 @@ __global__ __launch_bounds__(1024) void gn_partial_kernel(GroupNormArgs a, doubl
 }
 
 __global__ __launch_bounds__(256) void gn_stats_kernel(GroupNormArgs a, const double* partial, float* stats) {
-    const int i = blockIdx.x * 256 + threadIdx.x;  // sample * groups + group
-    if (i >= a.B * a.groups) return;
+    const int i = blockIdx.x * 4 + (threadIdx.x >> 6);  // sample * groups + group: one wave each
+    const int lane = threadIdx.x & 63;
+    if (i >= a.B * a.groups) return;  // whole waves
     const int b = i / a.groups, g = i - b * a.groups;
     const int nblk = (a.N + kGnRows - 1) / kGnRows;
     double s = 0.0, ss = 0.0;
-    for (int blk = 0; blk < nblk; ++blk) {
+    for (int blk = lane; blk < nblk; blk += 64) {
         const double* p = partial + (((long)b * nblk + blk) * a.groups + g) * 2;
         s += p[0];
         ss += p[1];
     }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        s += __shfl_xor(s, off);
+        ss += __shfl_xor(ss, off);
+    }
+    if (lane != 0) return;
     const double cnt = (double)a.N * (a.C / a.groups);
     const double mean = s / cnt;
     const double var = fmax(ss / cnt - mean * mean, 0.0);
@@ -232,7 +247,7 @@ __global__ __launch_bounds__(1024) void gn_apply_kernel(GroupNormArgs a, const f
     const TI* x = (const TI*)a.x + off;
     bf16* y = (bf16*)a.y + off;
     const int rows = min(kGnRows, a.N - blk * kGnRows);
-    for (int r = 0; r < rows; ++r) {
+    auto apply = [&](int r) {
         const float4 v = ld4_any<TI>(x + (long)r * a.C);
         bf16x4 o;
         o[0] = f2bf(silu((v.x - mean) * rstd * ww.x + bv.x));
@@ -240,6 +255,12 @@ __global__ __launch_bounds__(1024) void gn_apply_kernel(GroupNormArgs a, const f
         o[2] = f2bf(silu((v.z - mean) * rstd * ww.z + bv.z));
         o[3] = f2bf(silu((v.w - mean) * rstd * ww.w + bv.w));
         *(bf16x4*)(y + (long)r * a.C) = o;
+    };
+    if (rows == kGnRows) {
+#pragma unroll
+        for (int r = 0; r < kGnRows; ++r) apply(r);
+    } else {
+        for (int r = 0; r < rows; ++r) apply(r);
     }
 }
 
@@ -256,7 +277,7 @@ hipError_t launch_group_norm_silu(int in_bf16, const GroupNormArgs& a, void* scr
     const size_t lds = (size_t)(a.C / 4) * 2 * sizeof(double);
     if (in_bf16) hipLaunchKernelGGL(gn_partial_kernel<bf16>, rows, threads, lds, st, a, partial);
     else hipLaunchKernelGGL(gn_partial_kernel<float>, rows, threads, lds, st, a, partial);
-    hipLaunchKernelGGL(gn_stats_kernel, dim3((a.B * a.groups + 255) / 256), dim3(256), 0, st, a,
+    hipLaunchKernelGGL(gn_stats_kernel, dim3((a.B * a.groups + 3) / 4), dim3(256), 0, st, a,
                        (const double*)partial, stats);
     if (in_bf16) hipLaunchKernelGGL(gn_apply_kernel<bf16>, rows, threads, 0, st, a, (const float*)stats);
     else hipLaunchKernelGGL(gn_apply_kernel<float>, rows, threads, 0, st, a, (const float*)stats);

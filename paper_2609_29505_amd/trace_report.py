@@ -48,8 +48,9 @@ def kernel_stats(rows):
 
 
 def _is_fold(name: str) -> bool:
-    """A pre-norm kernel instantiated to absorb a frozen run (norm_kernel<..., true>)."""
-    return "norm_kernel" in name and "true>" in name
+    """A pre-norm kernel instantiated to absorb a frozen run (norm_kernel<..., true>; rocprofv3
+    leaves the bf16 instances mangled, where the flag reads Lb1E)."""
+    return "norm_kernel" in name and ("true>" in name or "Lb1E" in name)
 
 
 def frozen_rates(cfg, rows, lifetimes, folded=False):

@@ -176,6 +176,30 @@ def test_attention(P, dtype, B, H, nq, nk, dh):
     assert relmax(got, ref) <= tol
 
 
+@pytest.mark.parametrize("B,H,nq,nk,dh", [(1, 2, 300, 1000, 128), (2, 2, 130, 700, 72), (32, 16, 256, 256, 72),
+                                          (2, 2, 96, 77, 64), (16, 64, 300, 300, 64)])
+def test_attention_rising_scores(P, B, H, nq, nk, dh):
+    """Key norms growing along the sequence: later key blocks keep exceeding the running maximum
+    by many binades, so the online softmax raises its reference block after block instead of
+    keeping it."""
+    rng = np.random.default_rng(nq + 3 * nk + dh)
+    npq, npk = -(-nq // 64) * 64, -(-nk // 64) * 64
+    q = rng.standard_normal((B * H, npq, dh)) * 1.5
+    k = rng.standard_normal((B * H, npk, dh)) * np.linspace(0.1, 8.0, npk)[None, :, None]
+    v = rng.standard_normal((B * H, npk, dh))
+    qs, ks, vs = synth.store(q, "bf16"), synth.store(k, "bf16"), synth.store(v, "bf16")
+    vts = np.ascontiguousarray(vs.transpose(0, 2, 1))
+    o = empty((B, nq, H * dh), "bf16")
+    P.op_attention(dev(qs), dev(ks), dev(vts), o, B, H, dh, nq, nk)
+    qd = decode(qs, "bf16")[:, :nq].reshape(B, H, nq, dh)
+    kd = decode(ks, "bf16")[:, :nk].reshape(B, H, nk, dh)
+    vd = decode(vs, "bf16")[:, :nk].reshape(B, H, nk, dh)
+    ref = om.merge_heads(om.attention(qd, kd, vd))
+    got = host(o)
+    assert np.isfinite(got).all()
+    assert relmax(got, ref) <= 1.5e-2
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("kind,d,M", [(0, 256, 70), (0, 4096, 70), (1, 1024, 70), (1, 1280, 70), (2, 1152, 70),
                                       # many rows: one wave per row, ragged last workgroup

@@ -147,3 +147,34 @@ def test_trace_report_separates_grids():
     st = trace_report.kernel_stats(rows)
     assert [(g, n) for _, g, n, _, _, _ in st] == [(262144, 2), (131072, 1)]
     assert st[0][4] == pytest.approx(179.0) and st[1][4] == pytest.approx(96.0)
+
+
+def test_trace_report_recognises_folding_pre_norms():
+    """rocprofv3 demangles the fp32 pre-norms but leaves the bf16 ones mangled (__bf16 is DF16b):
+    the folding instance must be recognised in both spellings, and matched in dispatch order."""
+    from paper_2609_29505_amd import trace_report
+
+    import bench
+
+    fold_names = ["_ZN3sgd11norm_kernelIDF16bLi4ELi4ELb1EEEvNS_8NormArgsE",
+                  "void sgd::norm_kernel<float, 4, 4, true>(sgd::NormArgs)"]
+    plain_names = ["_ZN3sgd11norm_kernelIDF16bLi4ELi4ELb0EEEvNS_8NormArgsE",
+                   "void sgd::norm_kernel<float, 4, 4, false>(sgd::NormArgs)"]
+    assert all(trace_report._is_fold(n) for n in fold_names)
+    assert not any(trace_report._is_fold(n) for n in plain_names)
+
+    cfg = synth.get_config("tiny")
+    lifetimes = {"50": [3, 10, 1, 6]}
+    runs = sorted(cfg.budgets)
+    rows, t = [], 0
+    for pct in runs + [runs[0], runs[0]]:
+        act = np.arange(1, cfg.T + 1)[:, None] <= np.asarray(lifetimes[str(pct)])[None, :]
+        for j in range(4 * cfg.T):
+            for _ in bench.frozen_launches(cfg, act[j % cfg.T])[1]:
+                rows.append({"Kernel_Name": fold_names[0], "Start_Timestamp": str(t), "End_Timestamp": str(t + 5)})
+                rows.append({"Kernel_Name": plain_names[0], "Start_Timestamp": str(t + 10), "End_Timestamp": str(t + 15)})
+                t += 1000
+    out = trace_report.frozen_rates(cfg, rows, lifetimes, folded=True)
+    act = np.arange(1, cfg.T + 1)[:, None] <= np.asarray(lifetimes["50"])[None, :]
+    n = sum(len(bench.frozen_launches(cfg, act[j % cfg.T])[1]) for j in range(3 * cfg.T))
+    assert n > 0 and out[0][1] == n
