@@ -75,11 +75,12 @@ def trajectory(model: om.Model, z0: np.ndarray, static_mask: np.ndarray, steps: 
     out = DriftTrajectory()
     for s in range(1, steps + 1):
         m = int(np.asarray(static_mask[s - 1]).sum())
+        U = model.n_units
         if prev is not None and prev2 is not None:
-            d = np.array([drift(prev[l], prev2[l]) for l in range(cfg.L)])
+            d = np.array([drift(prev[l], prev2[l]) for l in range(U)])
         else:
-            d = np.zeros(cfg.L)
-        row = np.ones(cfg.L, np.uint8) if s == 1 else select(d, m)
+            d = np.zeros(U)
+        row = np.ones(U, np.uint8) if s == 1 else select(d, m)
         if forced_rows is not None:
             row = np.asarray(forced_rows[s - 1], np.uint8)
         inputs: Dict[int, np.ndarray] = {}

@@ -27,6 +27,13 @@ A multi-branch unit's update Delta is the sum of its branch updates in
 execution order (ResNet block, attention, cross-attention, MLP), and the
 active path adds each branch to the stream as it is produced, exactly as
 the unscheduled forward does.
+
+Unit granularity.  The scheduled unit is one block by default (its branches
+share a lifetime and one cached update).  With ``granularity="branch"`` every
+pre-norm residual branch of a block is a unit of its own (the residual units
+of Sec. 3.1 taken at branch level): block l's branches are units
+l * nb, ..., l * nb + nb - 1 in execution order, each with its own lifetime
+and cached update (its branch output), nb = len(branches(arch)).
 """
 from __future__ import annotations
 
@@ -45,6 +52,16 @@ LN_EPS = 1e-5
 GN_EPS = 1e-5
 ROPE_THETA = 10000.0
 CROSS_ARCHS = ("sdxl", "sdxl_unet")  # architectures with a cross-attention branch
+GRANULARITIES = ("block", "branch")
+
+
+def branches(arch: str):
+    """The residual branches of one block, in execution order."""
+    out = ("resnet",) if arch == "sdxl_unet" else ()
+    out += ("attn",)
+    if arch in CROSS_ARCHS:
+        out += ("xattn",)
+    return out + ("mlp",)
 
 
 # --------------------------------------------------------------------------
@@ -182,11 +199,18 @@ class Model:
     """One workload's weights decoded to float64, plus its architecture rules."""
 
     def __init__(self, cfg, weights: List[Dict[str, np.ndarray]], inputs: Dict[str, np.ndarray],
-                 lazy: bool = False):
+                 lazy: bool = False, granularity: str = "block"):
         """``lazy`` decodes a unit's weights each time the unit runs instead of keeping every
-        unit in float64 (for the full-size workloads)."""
+        unit in float64 (for the full-size workloads).  ``granularity``: "block" (one scheduled
+        unit per block) or "branch" (one per residual branch)."""
+        if granularity not in GRANULARITIES:
+            raise ValueError(f"granularity {granularity!r}")
         self.cfg = cfg
         self.arch = cfg.arch
+        self.granularity = granularity
+        self.branch_names = branches(cfg.arch)
+        self.nb = len(self.branch_names) if granularity == "branch" else 1
+        self.n_units = cfg.L * self.nb
         self.prec = Precision(cfg.dtype == "bf16")
         self._raw = weights
         self.units = _LazyUnits(weights, cfg.dtype) if lazy else [_decode_unit(w, cfg.dtype) for w in weights]
@@ -300,6 +324,16 @@ class Model:
         x2 = q(silu(group_norm(u1, cfg.groups, u["gn2_w"], u["gn2_b"])))
         return conv3x3(x2, u["w_conv2"], cfg.grid) + u["b_conv2"]
 
+    def branch(self, name: str, u, h: np.ndarray, t: float, mod=None, cross=None) -> np.ndarray:
+        """The update of one residual branch of a block on the current stream."""
+        if name == "resnet":
+            return self.resnet_branch(u, h, t)
+        if name == "attn":
+            return self.attn_branch(u, h, mod)
+        if name == "xattn":
+            return self.xattn_branch(u, h, *cross)
+        return self.mlp_branch(u, h, mod)
+
     def unit_active(self, l: int, h: np.ndarray, t: float, cross=None):
         """Run unit l's branches on the current stream.  Returns (h_out, Delta_l)."""
         u = self.units[l]
@@ -351,26 +385,50 @@ def denoise_step(model: Model, z: np.ndarray, s: int, active: Optional[Sequence[
     active step; the entry read later is the one from the last active step, S_l for a
     static schedule).  The active set need not be nested in s (the input-aware baselines).
     ``unit_inputs``, if given, receives each unit's input h_{l-1,s}: the residual stream
-    arriving at unit l (for a U-ViT out-block, before its skip linear).
+    arriving at unit l (for a U-ViT out-block, before its skip linear; with branch units, the
+    first branch of an out-block likewise).  Units are blocks or branches as
+    ``model.granularity`` says; ``active`` and ``cache`` are indexed by unit.
     """
     cfg = model.cfg
     t = timestep_value(s, cfg.T)
     h = initial_stream(model, z, s)
     skips: Dict[int, np.ndarray] = {}
+    nb = model.nb
     for l in range(cfg.L):
         if unit_inputs is not None:
-            unit_inputs[l] = h.copy()
+            unit_inputs[l * nb] = h.copy()
         src = model.skip_source(l)
         if src >= 0:
             h = model.skip_linear(model.units[l], h, skips[src])
-        if active is None or active[l]:
-            h, delta = model.unit_active(l, h, t, None if cross is None else cross[l])
-            if active is not None:
-                cache[l] = delta
+        if nb == 1:
+            if active is None or active[l]:
+                h, delta = model.unit_active(l, h, t, None if cross is None else cross[l])
+                if active is not None:
+                    cache[l] = delta
+            else:
+                if l not in cache:
+                    raise RuntimeError(f"unit {l} frozen before its cache was written")
+                h = h + cache[l]
         else:
-            if l not in cache:
-                raise RuntimeError(f"unit {l} frozen before its cache was written")
-            h = h + cache[l]
+            # branch units: each branch computes or adds its own cached update; a DiT block's
+            # modulation is computed when one of its branches computes
+            u, mod = None, None
+            for k, name in enumerate(model.branch_names):
+                j = l * nb + k
+                if unit_inputs is not None and k > 0:
+                    unit_inputs[j] = h.copy()
+                if active is None or active[j]:
+                    if u is None:
+                        u = model.units[l]
+                        mod = model.adaln(u, t) if model.arch == "dit" else None
+                    o = model.branch(name, u, h, t, mod, None if cross is None else cross[l])
+                    h = h + o
+                    if active is not None:
+                        cache[j] = o
+                else:
+                    if j not in cache:
+                        raise RuntimeError(f"unit {j} frozen before its cache was written")
+                    h = h + cache[j]
         if model.saves_skip(l):
             skips[l] = h
     return h
@@ -390,7 +448,7 @@ def sampler_update(cfg, z: np.ndarray, eps: np.ndarray, s: int) -> np.ndarray:
 
 def trajectory(model: Model, z0: np.ndarray, active_mask: Optional[np.ndarray],
                steps: Optional[int] = None) -> Trajectory:
-    """Run steps 1..steps (default T).  ``active_mask[s-1, l]`` or None for unscheduled."""
+    """Run steps 1..steps (default T).  ``active_mask[s-1, unit]`` or None for unscheduled."""
     cfg = model.cfg
     steps = cfg.T if steps is None else steps
     cross = None

@@ -58,7 +58,7 @@ class ReplayResult:
 def search(model: om.Model, z0: np.ndarray, tau_agree: float = 5e-3,
            max_layer_steps: Optional[int] = None) -> ReplayResult:
     cfg = model.cfg
-    L, T = cfg.L, cfg.T
+    L, T = model.n_units, cfg.T  # scheduled units: blocks or branches
     ceiling = max_layer_steps if max_layer_steps and max_layer_steps > 0 else L * T
     cross = [model.cross_kv(u) for u in model.units] if model.arch in om.CROSS_ARCHS else None
     z = np.array(z0, dtype=np.float64)

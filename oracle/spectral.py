@@ -129,6 +129,14 @@ def normalise(raw: Sequence[float]) -> np.ndarray:
 ATTN_ROLES = ("q", "k", "v", "o")
 XATTN_ROLES = ("xq", "xk", "xv", "xo")
 MLP_ROLES = ("w1", "w2")
+CONV_ROLES = ("conv1", "conv2")
+BRANCH_ROLES = {"resnet": CONV_ROLES, "attn": ATTN_ROLES, "xattn": XATTN_ROLES, "mlp": MLP_ROLES}
+
+
+def branch_matrices(mats: Dict[str, np.ndarray], branch: str) -> Dict[str, np.ndarray]:
+    """The scored matrices of one residual branch of a block (a unit at branch granularity):
+    its score is that branch's component of Eq. app-block-score alone."""
+    return {r: mats[r] for r in BRANCH_ROLES[branch]}
 
 
 def unit_matrices(weights: Dict[str, np.ndarray], d: int, dtype: str) -> Dict[str, np.ndarray]:
