@@ -118,6 +118,8 @@ def main() -> int:
     ap.add_argument("--no-input-aware", action="store_true",
                     help="skip the activation-drift policy and the oracle-replay search")
     ap.add_argument("--tau-agree", type=float, default=5e-3, help="oracle-replay tolerance")
+    ap.add_argument("--no-branch-units", action="store_true",
+                    help="skip the branch-granular schedule (every residual branch a unit of its own)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the library has no multi-GPU path (batches would shard by "
@@ -319,6 +321,30 @@ def main() -> int:
         log(f"oracle replay: search {t_search:.1f}s ({evals} evaluations), lifetimes {life.tolist()} -> "
             f"{rate(times):.2f} steps/s, deviation {r_dev['rel_l2']:.3e}")
 
+    branch_units = None
+    if not args.no_branch_units and not args.lifetimes:
+        # the same budget over branch units (each residual branch its own lifetime and cached
+        # update), on the same device weights; spectra rebuilt per branch (offline, not timed)
+        dmb = P.DeviceModel(cfg, weights, inputs, granularity="branch", share=dm)
+        U = dmb.n_units
+        bsch = P.schedule_build(dmb.scored_units(), [cfg.dh] * U, T, budget_pct=head)
+        cache_b = P.Cache(dmb)
+
+        def branch_step(s):
+            if s == 1:
+                cache_b.reset()
+            dmb.step(z, s, bsch, cache_b)
+
+        times, _ = timed(None, stepper=branch_step)
+        b_dev = deviation()
+        branch_units = {"units": U, "steps_per_s": round(rate(times), 3), "speedup": round(rate(times) / all_rate, 4),
+                        "unit_steps": bsch.layer_steps, "of": U * T, "deviation": b_dev,
+                        "lifetimes": bsch.lifetimes.tolist()}
+        log(f"branch units ({U}): {bsch.layer_steps} unit-steps -> {rate(times):.2f} steps/s, "
+            f"deviation {b_dev['rel_l2']:.3e}")
+        del cache_b
+        dmb.close()
+
     value = rate(results[head])
     head_ms = float(np.median(results[head]))
 
@@ -412,6 +438,7 @@ def main() -> int:
                          "layer_steps": rule_scheds[r].layer_steps, "deviation": dv}
                      for r, (tm, dv) in rule_res.items()}},
         "input_aware": input_aware,
+        "branch_units": branch_units,
         "roofline": roofline,
         "kernels": kernels,
         "frozen_path": frozen,

@@ -66,6 +66,17 @@ enum sgd_arch {
                             * convolution) followed by the SDXL transformer block        */
 };
 
+/* What one scheduled unit is (the residual units h_l = h_{l-1} + F_l of Sec. 3.1).
+ * SGD_UNIT_BLOCK: one unit per block; its branches share one lifetime and one cached update,
+ *   the sum of its branch updates in execution order.
+ * SGD_UNIT_BRANCH: every residual branch of a block is a unit of its own, with its own lifetime
+ *   and cached update (its branch output).  Block l's branches are units l nb .. l nb + nb - 1
+ *   in execution order: [ResNet block (SDXL UNet)], self-attention, [cross-attention (SDXL,
+ *   SDXL UNet)], MLP; nb = 2, 3 or 4.  Its score is that branch's component of
+ *   Eq. app-block-score (build the schedule from one sgd_unit per branch).
+ * Schedules, active rows, cache slots, drift and replay count units: U = L (blocks) or L nb. */
+enum sgd_granularity { SGD_UNIT_BLOCK = 0, SGD_UNIT_BRANCH = 1 };
+
 /* Role of a scored matrix inside its unit (appendix "Exact Block-Level Scores"). */
 enum sgd_role {
     SGD_ROLE_Q = 0, SGD_ROLE_K = 1, SGD_ROLE_V = 2, SGD_ROLE_O = 3,
@@ -259,6 +270,7 @@ typedef struct {
     const void* ctx;
     const sgd_unit_weights* units; /* [L], copied by sgd_model_create */
     int32_t grid, groups;          /* SDXL UNet units only */
+    int32_t granularity;           /* sgd_granularity: SGD_UNIT_BLOCK (0) or SGD_UNIT_BRANCH */
 } sgd_model_desc;
 
 typedef struct sgd_model sgd_model;
@@ -266,10 +278,14 @@ typedef struct sgd_cache sgd_cache;
 
 int sgd_model_create(const sgd_model_desc* desc, sgd_model** out);
 int sgd_model_destroy(sgd_model* model);
+/* The number U of scheduled units (L, or L times the branches of a block; see sgd_granularity):
+ * the L of every schedule, active row, drift record and replay result of this model. */
+int sgd_model_units(const sgd_model* model, int32_t* units);
 
 /* Bytes of scratch one sgd_denoise_step needs (device, 256-byte aligned). */
 int sgd_workspace_bytes(const sgd_model* model, size_t* bytes);
-/* Bytes of the per-trajectory delta cache: L fp32 [B x N x d] slots (+ SDXL context K/V). */
+/* Bytes of the per-trajectory delta cache: U fp32 [B x N x d] slots (one per scheduled unit)
+ * (+ SDXL context K/V, one per block). */
 int sgd_cache_bytes(const sgd_model* model, size_t* bytes);
 /* Wrap a caller-owned device buffer of sgd_cache_bytes as the cache of one trajectory. */
 int sgd_cache_bind(sgd_model* model, void* device_buffer, size_t bytes, sgd_cache** out);
@@ -287,7 +303,8 @@ typedef struct {
  *   state  device fp32 [B x N x d] (z_s on entry, z_{s+1} on return; updated in place)
  *   step   s in 1..T
  *   sched  NULL runs the unscheduled forward (every unit active, cache untouched, cache
- *          may be NULL); otherwise a schedule with sched->L == L and sched->T == T
+ *          may be NULL); otherwise a schedule of the model's U units (sched->L == U, see
+ *          sgd_model_units) and sched->T == T
  *   cache  the trajectory's cache; steps must arrive in order 1, 2, ..., T
  * A frozen unit's slot must have been written by an earlier step of this trajectory
  * (SGD_E_CACHE).  Returns after enqueueing on hip_stream.                           */
@@ -315,7 +332,7 @@ int sgd_denoise_step_noalloc(sgd_model* model, void* state, int32_t step, const 
 /* -------------------------------------------------- input-aware baselines */
 
 /* One step with an arbitrary set of active units (Alg. 2 with a per-step active set that
- * need not be nested in s).  active: host [L], nonzero = the unit computes its branches.
+ * need not be nested in s).  active: host [U], nonzero = the unit computes its branch(es).
  * An active unit refreshes its cached update at every active step (except at step T, which
  * no later step reads); a frozen unit adds the update of its latest active step, which must
  * exist (SGD_E_CACHE otherwise).  Steps arrive in order 1..T on the cache, as for
@@ -324,23 +341,24 @@ int sgd_denoise_step_masked(sgd_model* model, void* state, int32_t step, const u
                             const sgd_step_args* args, void* hip_stream);
 
 /* Device bytes of the drift record of sgd_drift_step (caller-allocated, 256-byte aligned).
- * Layout: L slots of align256(B N d 4) bytes holding each unit's fp32 input [B, N, d] of
- * the last recorded step, then L x 256 x 2 fp64 partial sums (256-byte aligned), then L x 2
- * fp64 sums: sum over the input's elements of (h_s - h_{s-1})^2 and of h_s^2 per unit. */
+ * Layout: U slots of align256(B N d 4) bytes holding each unit's fp32 input [B, N, d] of
+ * the last recorded step, then U x 256 x 2 fp64 partial sums (256-byte aligned), then U x 2
+ * fp64 sums: sum over the input's elements of (h_s - h_{s-1})^2 and of h_s^2 per unit
+ * (U = sgd_model_units). */
 int sgd_drift_bytes(const sgd_model* model, size_t* bytes);
 
 /* One step of the causal activation-drift policy (appendix "Protocol Details", "Dynamic
  * baselines", "Causal activation drift"; Table "Static versus input-aware scheduling at
  * matched per-step active counts").  After step s-1 the policy holds, for every unit l,
  *   d_{l,s-1} = ||h_{l-1,s-1} - h_{l-1,s-2}||_2 / (||h_{l-1,s-1}||_2 + 1e-8)
- * of the unit's input h_{l-1} (the residual stream arriving at the unit; norms over the whole
- * [B, N, d] tensor).  Step s activates the m_s units of largest lagged drift, m_s being the
+ * of the unit's input h_{l-1} (the residual stream arriving at the unit, for the first unit of
+ * a U-ViT out-block before its skip linear; norms over the whole [B, N, d] tensor).  Step s activates the m_s units of largest lagged drift, m_s being the
  * active count of `sched` at step s, ties to the lower unit index; step 1 is full, and at
  * step 2 no lagged drift exists (every drift counts as 0).  The step then runs as
  * sgd_denoise_step_masked and records this step's unit inputs for the next one.
  *   drift_buf   device buffer of sgd_drift_bytes, the same for a whole trajectory
- *   active_out  host [L] or NULL: the active set this step used
- *   drift_out   host [L] or NULL: the lagged drift d_{l,s-1} the choice used
+ *   active_out  host [U] or NULL: the active set this step used
+ *   drift_out   host [U] or NULL: the lagged drift d_{l,s-1} the choice used
  * Steps s >= 3 synchronise hip_stream first, to read the drift step s-1 recorded. */
 int sgd_drift_step(sgd_model* model, void* state, int32_t step, const sgd_schedule* sched, sgd_cache* cache,
                    const sgd_step_args* args, void* drift_buf, size_t drift_bytes, uint8_t* active_out,
@@ -349,14 +367,14 @@ int sgd_drift_step(sgd_model* model, void* state, int32_t step, const sgd_schedu
 /* Oracle replay (appendix "Protocol Details", "Dynamic baselines", "Oracle replay"): a
  * non-deployable headroom search.  Parameters:
  *   tau_agree        tolerance on the relative output deviation (the paper uses 5e-3)
- *   max_layer_steps  ceiling on the active layer-steps of the whole trajectory (<= 0: L T) */
+ *   max_layer_steps  ceiling on the active unit-steps of the whole trajectory (<= 0: U T) */
 typedef struct {
     double tau_agree;
     int64_t max_layer_steps;
 } sgd_replay_params;
 
 /* Device bytes of the search's buffer (caller-allocated, 256-byte aligned): the state, two
- * output buffers and 2 L cached-update slots of B N d fp32 values each, plus the SDXL
+ * output buffers and 2 U cached-update slots of B N d fp32 values each, plus the SDXL
  * context projections and reduction scratch. */
 int sgd_replay_bytes(const sgd_model* model, size_t* bytes);
 
@@ -370,11 +388,11 @@ int sgd_replay_bytes(const sgd_model* model, size_t* bytes);
  *   deviation (ties to the lower index) joins F while delta <= tau_agree, or, ignoring the
  *   tolerance, while keeping the current active count for the remaining steps would exceed
  *   the ceiling.  Step 1 is full (no update exists yet).
- *   lifetimes   host [L]: S_l = the last step before unit l joined F (T if it never did), a
+ *   lifetimes   host [U]: S_l = the last step before unit l joined F (T if it never did), a
  *               nested schedule for sgd_schedule_from_lifetimes
  *   evaluations host, optional: network evaluations the search ran
- *   delta_log   host [T L L] or NULL: delta of candidate j in round r of step s at
- *               [((s-1) L + r) L + j], NaN where nothing was evaluated
+ *   delta_log   host [T U U] or NULL: delta of candidate j in round r of step s at
+ *               [((s-1) U + r) U + j], NaN where nothing was evaluated
  * args supplies alpha, beta and the step workspace.  Synchronises hip_stream. */
 int sgd_replay_search(sgd_model* model, const void* z1, const sgd_replay_params* params, const sgd_step_args* args,
                       void* replay_buf, size_t replay_bytes, int32_t* lifetimes, int64_t* evaluations,

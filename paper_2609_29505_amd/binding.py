@@ -16,6 +16,7 @@ lib_path = os.path.join(_PKG, "lib", "libsgd.so")
 
 SGD_F32, SGD_BF16 = 0, 1
 SGD_ARCH = {"tiny": 0, "llada": 1, "dit": 2, "uvit": 3, "sdxl": 4, "sdxl_unet": 5}
+SGD_UNIT = {"block": 0, "branch": 1}
 SGD_RULE = {"scr_frob": 0, "random": 1, "depth": 2, "frob": 3, "spectral": 4, "stable_rank": 5,
             "frob_srank": 6, "raw_scr": 7}
 SGD_ROLE = {"q": 0, "k": 1, "v": 2, "o": 3, "xq": 4, "xk": 5, "xv": 6, "xo": 7, "w1": 8, "w2": 9, "conv": 10}
@@ -69,7 +70,8 @@ class sgd_model_desc(C.Structure):
                 ("H", C.c_int32), ("head_dim", C.c_int32), ("F", C.c_int32), ("L", C.c_int32), ("T", C.c_int32),
                 ("ctx_len", C.c_int32), ("ctx_dim", C.c_int32), ("update_row_begin", C.c_int32),
                 ("update_row_end", C.c_int32), ("class_emb", C.c_void_p), ("ctx", C.c_void_p),
-                ("units", C.POINTER(sgd_unit_weights)), ("grid", C.c_int32), ("groups", C.c_int32)]
+                ("units", C.POINTER(sgd_unit_weights)), ("grid", C.c_int32), ("groups", C.c_int32),
+                ("granularity", C.c_int32)]
 
 
 class sgd_replay_params(C.Structure):
@@ -88,7 +90,7 @@ _lib = None
 EXPORTS = ["sgd_last_error", "sgd_version", "sgd_s_min_default", "sgd_budget_layer_steps",
            "sgd_schedule_workspace_bytes", "sgd_schedule_build", "sgd_matrix_stats", "sgd_schedule_from_scores",
            "sgd_schedule_from_stats",
-           "sgd_schedule_from_lifetimes", "sgd_model_create", "sgd_model_destroy", "sgd_workspace_bytes",
+           "sgd_schedule_from_lifetimes", "sgd_model_create", "sgd_model_destroy", "sgd_model_units", "sgd_workspace_bytes",
            "sgd_cache_bytes", "sgd_cache_bind", "sgd_cache_reset", "sgd_cache_destroy", "sgd_denoise_step",
            "sgd_denoise_step_noalloc", "sgd_denoise_step_masked", "sgd_drift_bytes", "sgd_drift_step", "sgd_replay_bytes", "sgd_replay_search",
            "sgd_profile_begin", "sgd_profile_end", "sgd_op_linear", "sgd_op_attention", "sgd_op_norm",
@@ -118,6 +120,7 @@ def lib() -> C.CDLL:
             "sgd_schedule_from_lifetimes": [i32, i32, C.POINTER(C.c_int32), C.POINTER(sgd_schedule)],
             "sgd_model_create": [C.POINTER(sgd_model_desc), C.POINTER(vp)],
             "sgd_model_destroy": [vp],
+            "sgd_model_units": [vp, C.POINTER(C.c_int32)],
             "sgd_workspace_bytes": [vp, C.POINTER(C.c_size_t)],
             "sgd_cache_bytes": [vp, C.POINTER(C.c_size_t)],
             "sgd_cache_bind": [vp, vp, C.c_size_t, C.POINTER(vp)],
@@ -424,21 +427,32 @@ def _to_device(arr: np.ndarray, dtype: str):
 class DeviceModel:
     """Uploads one workload's weights and inputs and owns the ``sgd_model`` handle."""
 
-    def __init__(self, cfg, weights: List[Dict[str, np.ndarray]], inputs: Dict[str, np.ndarray]):
+    def __init__(self, cfg, weights: List[Dict[str, np.ndarray]], inputs: Dict[str, np.ndarray],
+                 granularity: str = "block", share: Optional["DeviceModel"] = None):
+        """``granularity``: "block" (one scheduled unit per block) or "branch" (one per residual
+        branch; see sgd_granularity).  ``share``: a model of the same workload whose device
+        weights and inputs this one uses instead of uploading its own."""
         import torch
         self.cfg = cfg
+        self.granularity = granularity
         self.dtype = SGD_BF16 if cfg.dtype == "bf16" else SGD_F32
         self.tensors: List[Dict[str, "torch.Tensor"]] = []
         cw = (sgd_unit_weights * cfg.L)()
-        for l, w in enumerate(weights):
-            dev = {k: _to_device(v, cfg.dtype) for k, v in w.items() if not k.startswith("_")}
+        for l in range(cfg.L):
+            if share is not None:
+                dev = share.tensors[l]
+            else:
+                dev = {k: _to_device(v, cfg.dtype) for k, v in weights[l].items() if not k.startswith("_")}
             self.tensors.append(dev)
             for name in _W_FIELDS:
                 if name in dev:
                     setattr(cw[l], name, dev[name].data_ptr())
         self._cw = cw
-        self.class_emb = _to_device(inputs["class_emb"], "f32") if "class_emb" in inputs else None
-        self.ctx = _to_device(inputs["ctx"], cfg.dtype) if "ctx" in inputs else None
+        if share is not None:
+            self.class_emb, self.ctx = share.class_emb, share.ctx
+        else:
+            self.class_emb = _to_device(inputs["class_emb"], "f32") if "class_emb" in inputs else None
+            self.ctx = _to_device(inputs["ctx"], cfg.dtype) if "ctx" in inputs else None
         d = sgd_model_desc()
         d.arch, d.dtype = SGD_ARCH[cfg.arch], self.dtype
         d.B, d.N, d.d, d.H, d.head_dim, d.F, d.L, d.T = cfg.B, cfg.N, cfg.d, cfg.H, cfg.dh, cfg.F, cfg.L, cfg.T
@@ -448,9 +462,13 @@ class DeviceModel:
         d.ctx = self.ctx.data_ptr() if self.ctx is not None else None
         d.units = C.cast(cw, C.POINTER(sgd_unit_weights))
         d.grid, d.groups = cfg.grid, cfg.groups
+        d.granularity = SGD_UNIT[granularity]
         h = C.c_void_p()
         _check(lib().sgd_model_create(C.byref(d), C.byref(h)))
         self.h = h
+        nu = C.c_int32()
+        _check(lib().sgd_model_units(h, C.byref(nu)))
+        self.n_units = int(nu.value)
         ws = C.c_size_t()
         _check(lib().sgd_workspace_bytes(h, C.byref(ws)))
         self.workspace_bytes = int(ws.value)
@@ -460,19 +478,26 @@ class DeviceModel:
         self.workspace = torch.empty(max(self.workspace_bytes, 256), dtype=torch.uint8, device="cuda")
 
     def scored_units(self):
-        """Per unit, the (role, device tensor) pairs the schedule scores (views of fused storage)."""
+        """Per scheduled unit, the (role, device tensor) pairs the schedule scores (views of fused
+        storage): a block's matrices, or with branch units one branch's, in execution order."""
         cfg, d = self.cfg, self.cfg.d
         out = []
         for dev in self.tensors:
             qkv = dev["w_qkv"]
-            mats = [("q", qkv[:d]), ("k", qkv[d:2 * d]), ("v", qkv[2 * d:]), ("o", dev["w_o"])]
+            parts = []
             if "w_conv1" in dev:
-                mats += [("conv", dev["w_conv1"]), ("conv", dev["w_conv2"])]
+                parts.append([("conv", dev["w_conv1"]), ("conv", dev["w_conv2"])])
+            parts.append([("q", qkv[:d]), ("k", qkv[d:2 * d]), ("v", qkv[2 * d:]), ("o", dev["w_o"])])
             if "w_xq" in dev:
                 xkv = dev["w_xkv"]
-                mats += [("xq", dev["w_xq"]), ("xk", xkv[:d]), ("xv", xkv[d:]), ("xo", dev["w_xo"])]
-            mats += [("w1", dev["w1"]), ("w2", dev["w2"])]
-            out.append(mats)
+                parts.append([("xq", dev["w_xq"]), ("xk", xkv[:d]), ("xv", xkv[d:]), ("xo", dev["w_xo"])])
+            parts.append([("w1", dev["w1"]), ("w2", dev["w2"])])
+            if self.granularity == "branch":
+                out.extend(parts)
+            else:
+                # a block lists its attention matrices first (the order of mat_stats)
+                order = [1, 0] + list(range(2, len(parts))) if "w_conv1" in dev else range(len(parts))
+                out.append([m for i in order for m in parts[i]])
         return out
 
     def step(self, state, s: int, sched: Optional[Schedule], cache: Optional["Cache"], alpha=1.0, beta=None,
@@ -501,7 +526,7 @@ class DeviceModel:
                                               C.c_void_p(_stream_ptr(stream))))
 
     def step_masked(self, state, s: int, active_row, cache: "Cache", alpha=1.0, beta=None, stream=None) -> None:
-        """One step with an arbitrary active set (``active_row``: L flags)."""
+        """One step with an arbitrary active set (``active_row``: one flag per scheduled unit)."""
         row = np.ascontiguousarray(active_row, dtype=np.uint8)
         a = self._args(alpha, beta)
         _check(lib().sgd_denoise_step_masked(self.h, C.c_void_p(state.data_ptr()), s,
@@ -517,7 +542,7 @@ class DeviceModel:
     def drift_step(self, state, s: int, sched: Schedule, cache: "Cache", drift_buf, alpha=1.0, beta=None,
                    stream=None):
         """One step of the causal activation-drift policy; returns (active row, lagged drift)."""
-        L = self.cfg.L
+        L = self.n_units
         row = np.zeros(L, np.uint8)
         dr = np.zeros(L, np.float64)
         a = self._args(alpha, beta)
@@ -529,7 +554,7 @@ class DeviceModel:
 
     def replay_search(self, z1, tau_agree=5e-3, max_layer_steps=0, alpha=1.0, beta=None, log=False, stream=None):
         """Oracle-replay search from z1; returns (lifetimes, evaluations, delta log or None)."""
-        L, T = self.cfg.L, self.cfg.T
+        L, T = self.n_units, self.cfg.T
         nb = C.c_size_t()
         _check(lib().sgd_replay_bytes(self.h, C.byref(nb)))
         buf = _workspace(nb.value)

@@ -42,6 +42,13 @@ extern "C" int sgd_version(void) { return 1; }
 namespace sgd {
 bool arch_gated(int a) { return a == SGD_ARCH_LLADA || a == SGD_ARCH_SDXL || a == SGD_ARCH_SDXL_UNET; }
 bool arch_cross(int a) { return a == SGD_ARCH_SDXL || a == SGD_ARCH_SDXL_UNET; }
+int block_branch(int arch, int i) {
+    const int first = arch == SGD_ARCH_SDXL_UNET ? BR_RESNET : BR_ATTN;
+    int b = first + i;
+    if (b >= BR_XATTN && !arch_cross(arch)) ++b;  // no cross-attention branch
+    return b;
+}
+int block_branches(int arch) { return 2 + (arch == SGD_ARCH_SDXL_UNET) + arch_cross(arch); }
 }  // namespace sgd
 
 namespace {
@@ -127,6 +134,8 @@ extern "C" int sgd_model_create(const sgd_model_desc* desc, sgd_model** out) {
         if (d.ctx_len < 1 || d.ctx_dim < 64 || d.ctx_dim % 64) return fail(SGD_E_SHAPE, "ctx_len >= 1, ctx_dim % 64 == 0");
     }
     if ((long)d.B * d.N * d.d >= (1L << 31)) return fail(SGD_E_SHAPE, "B * N * d must stay below 2^31");
+    if (d.granularity != SGD_UNIT_BLOCK && d.granularity != SGD_UNIT_BRANCH)
+        return fail(SGD_E_ARG, "granularity must be SGD_UNIT_BLOCK or SGD_UNIT_BRANCH");
     for (int l = 0; l < d.L; ++l) {
         int rc = check_unit(d, d.units[l], l);
         if (rc) return rc;
@@ -140,6 +149,8 @@ extern "C" int sgd_model_create(const sgd_model_desc* desc, sgd_model** out) {
     m->np = (d.N + 63) / 64 * 64;
     m->npc = arch_cross(d.arch) ? (d.ctx_len + 63) / 64 * 64 : 64;
     m->M = (long)d.B * d.N;
+    m->nb = d.granularity == SGD_UNIT_BRANCH ? block_branches(d.arch) : 1;
+    m->nu = d.L * m->nb;
     const size_t Md = (size_t)m->M * d.d;
     const size_t heads = (size_t)d.B * d.H * m->np * d.head_dim;
     const size_t cheads = (size_t)d.B * d.H * m->npc * d.head_dim;
@@ -162,7 +173,7 @@ extern "C" int sgd_model_create(const sgd_model_desc* desc, sgd_model** out) {
     m->w_gn = take(d.arch == SGD_ARCH_SDXL_UNET ? group_norm_scratch_bytes(d.B, d.N, d.groups) : 0);
     m->w_total = o;
     o = 0;
-    m->c_delta = take((size_t)d.L * align256(Md * 4));
+    m->c_delta = take((size_t)m->nu * align256(Md * 4));
     m->c_ctx = take(arch_cross(d.arch) ? (size_t)d.L * m->ckv_unit : 0);
     m->c_total = o;
     *out = m;
@@ -173,6 +184,12 @@ extern "C" int sgd_model_destroy(sgd_model* m) {
     if (!m) return fail(SGD_E_ARG, "NULL model");
     for (hipEvent_t e : m->prof_ev) (void)hipEventDestroy(e);
     delete m;
+    return SGD_OK;
+}
+
+extern "C" int sgd_model_units(const sgd_model* m, int32_t* units) {
+    if (!m || !units) return fail(SGD_E_ARG, "NULL argument");
+    *units = m->nu;
     return SGD_OK;
 }
 
@@ -197,7 +214,7 @@ extern "C" int sgd_cache_bind(sgd_model* m, void* buf, size_t bytes, sgd_cache**
     c->base = (char*)buf;
     c->bytes = bytes;
     c->last_step = 0;
-    c->written.assign(m->d.L, 0);
+    c->written.assign(m->nu, 0);
     c->ctx_valid = false;
     *out = c;
     return SGD_OK;
@@ -386,7 +403,7 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
     };
 
     int hb_cur = 0;
-    // where unit l's output copy (for a long skip or the next out-block) goes, or NULL
+    // where block l's output copy (for a long skip or the next out-block) goes, or NULL
     auto out_copy = [&](int l) -> void* {
         if (!uvit) return nullptr;
         if (l < half) return skipbuf(l);
@@ -394,61 +411,84 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
         return nullptr;
     };
 
-    int l = 0;
-    while (l < L && S.err == hipSuccess) {
+    // scheduled units: blocks (nb = 1: a unit runs every branch of its block) or single
+    // branches (nb = the block's branch count: unit u is branch u % nb of block u / nb)
+    const int nb = m->nb, nu = m->nu;
+    auto branch_of = [&](int u) { return nb == 1 ? -1 : block_branch(d.arch, u % nb); };
+    auto last_of_block = [&](int u) { return u % nb == nb - 1; };
+    // a U-ViT out-block's first unit: its skip linear reads h before anything else
+    auto out_start = [&](int u) { return uvit && u / nb > half && u % nb == 0; };
+    int mod_block = -1;  // DiT: the block whose modulation `mod` holds
+
+    int u = 0;
+    while (u < nu && S.err == hipSuccess) {
+        const int l = u / nb;
         const sgd_unit_weights& w = m->u[l];
-        const bool out_block = uvit && l > half;
-        if (!act[l] && !out_block) {
-            // maximal run of frozen units that need no skip linear in between (single units
-            // while drift is recorded: each unit's input is measured before its update)
-            FrozenRun fr{};
-            fr.h = h; fr.n = (long)Md; fr.r = 0; fr.snap_bf16 = dt;
-            const int cap = dr ? 1 : kMaxRun;
-            if (dr) record_drift(l);
-            bool snaps = false;
-            while (l < L && !act[l] && !(uvit && l > half) && fr.r < cap) {
-                fr.delta[fr.r] = plan.dread[l];
-                fr.snap[fr.r] = out_copy(l);
-                snaps = snaps || fr.snap[fr.r];
-                fr.r++;
-                ++l;
-            }
-            // handed to the next unit's first norm when that unit computes and starts with one
-            // (not a U-ViT out-block, whose skip linear reads h first; not a UNet unit, whose
-            // ResNet block starts with GroupNorm), and no unit of the run copies h out
-            if (!dr && !snaps && l < L && act[l] && !(uvit && l > half) && !unet) {
-                fold.assign(fr.delta, fr.delta + fr.r);
-                continue;
-            }
-            S.run(SGD_K_FROZEN, [&] { return launch_frozen_run(fr, S.st); });
-            continue;
-        }
-        record_drift(l);
-        if (out_block) {
-            // U-ViT skip linear (always executed): h <- [h ; skip] W_skip^T + b (+ Delta if frozen)
+        if (out_start(u)) {
+            // U-ViT skip linear (always executed): h <- [h ; skip] W_skip^T + b; a frozen block
+            // unit's cached update is added in the same epilogue
+            record_drift(u);
+            const bool frozen_block = nb == 1 && !act[u];
             GemmArgs g;
             g.A0 = hb(hb_cur); g.lda0 = dd; g.A1 = skipbuf(L - 1 - l); g.lda1 = dd; g.K0 = dd;
             g.B = w.w_skip; g.ldb = 2L * dd; g.M = (int)M; g.N = dd; g.K = 2 * dd;
             hb_cur ^= 1;
             EpiParams e;
             e.kind = EP_SKIP; e.bias = (const float*)w.b_skip; e.h = h; e.d = dd;
-            if (!act[l]) { e.delta = (float*)plan.dread[l]; e.delta_mode = 1; e.hcopy = out_copy(l); }
+            if (frozen_block) { e.delta = (float*)plan.dread[u]; e.delta_mode = 1; e.hcopy = out_copy(l); }
             S.run(SGD_K_GEMM_SKIP, [&] { return launch_gemm(dt, g, e, S.st); });
-            if (!act[l]) { ++l; continue; }
+            if (frozen_block) { ++u; continue; }
+        } else if (act[u]) {
+            record_drift(u);
         }
-        // ---- active unit: every branch, in order
-        float* dl = plan.dwrite ? plan.dwrite[l] : nullptr;
+        if (!act[u]) {
+            // maximal run of frozen units that crosses no skip linear (single units while drift
+            // is recorded: each unit's input is measured before its update)
+            FrozenRun fr{};
+            fr.h = h; fr.n = (long)Md; fr.r = 0; fr.snap_bf16 = dt;
+            const int cap = dr ? 1 : kMaxRun;
+            if (dr && !out_start(u)) record_drift(u);
+            bool snaps = false;
+            do {
+                fr.delta[fr.r] = plan.dread[u];
+                fr.snap[fr.r] = last_of_block(u) ? out_copy(u / nb) : nullptr;
+                snaps = snaps || fr.snap[fr.r];
+                fr.r++;
+                ++u;
+            } while (u < nu && !act[u] && !out_start(u) && fr.r < cap);
+            // handed to the next unit's first norm when that unit computes and starts with one
+            // (not a U-ViT out-block, whose skip linear reads h first; not a UNet ResNet
+            // branch, which starts with GroupNorm), and no unit of the run copies h out
+            const bool next_norm = u < nu && act[u] && !out_start(u) &&
+                                   !(unet && (nb == 1 || branch_of(u) == BR_RESNET));
+            if (!dr && !snaps && next_norm) {
+                fold.assign(fr.delta, fr.delta + fr.r);
+                continue;
+            }
+            S.run(SGD_K_FROZEN, [&] { return launch_frozen_run(fr, S.st); });
+            continue;
+        }
+        // ---- active unit: its branch, or every branch of its block, in order
+        float* dl = plan.dwrite ? plan.dwrite[u] : nullptr;
+        // cached-update mode of a branch's residual epilogue: a block unit stores its first
+        // branch's update and adds the later ones; a branch unit stores its own
+        bool first = true;
+        auto dmode = [&]() { const int r = dl ? (first || nb > 1 ? 1 : 2) : 0; first = false; return r; };
         const float* mod_l = nullptr;
         if (dit) {
-            S.run(SGD_K_COND, [&] {
-                return launch_adaln_mod(dt, siluc, w.w_ada, (const float*)w.b_ada, mod, d.B, dd, 6 * dd, S.st);
-            });
+            if (mod_block != l) {
+                S.run(SGD_K_COND, [&] {
+                    return launch_adaln_mod(dt, siluc, w.w_ada, (const float*)w.b_ada, mod, d.B, dd, 6 * dd, S.st);
+                });
+                mod_block = l;
+            }
             mod_l = mod;
         }
-        if (unet) {
+        const int br = branch_of(u);
+        if (unet && (br < 0 || br == BR_RESNET)) {
             // ResNet block: the unit's time projection, GroupNorm + SiLU, 3x3 convolution (+ bias
             // + time projection) into the hidden buffer, GroupNorm + SiLU, 3x3 convolution added
-            // to the stream (the first branch: it stores the cached update)
+            // to the stream
             S.run(SGD_K_COND, [&] {
                 return launch_adaln_mod(dt, siluc, w.w_temb, (const float*)w.b_temb, mod, d.B, dd, dd, S.st);
             });
@@ -467,12 +507,11 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
             g2.B = w.w_conv2;
             EpiParams e2;
             e2.kind = EP_RESID; e2.bias = (const float*)w.b_conv2; e2.h = h; e2.d = dd; e2.delta = dl;
-            e2.delta_mode = dl ? 1 : 0; e2.ntok = N;
+            e2.delta_mode = dmode(); e2.ntok = N;
             S.run(SGD_K_GEMM_CONV, [&] { return launch_gemm(dt, g2, e2, S.st); });
         }
-        // attention branch
-        norm((const float*)w.norm1_w, (const float*)w.norm1_b, mod_l, mod_l ? mod_l + dd : nullptr);
-        {
+        if (br < 0 || br == BR_ATTN) {
+            norm((const float*)w.norm1_w, (const float*)w.norm1_b, mod_l, mod_l ? mod_l + dd : nullptr);
             GemmArgs g;
             g.A0 = xb; g.lda0 = dd; g.B = w.w_qkv; g.ldb = dd; g.M = (int)M; g.N = 3 * dd; g.K = dd;
             EpiParams e;
@@ -480,12 +519,10 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
             e.ntok = N; e.np = m->np; e.H = H; e.dh = dh; e.d = dd;
             e.rope = d.arch == SGD_ARCH_LLADA; e.rope_log2_theta = (float)std::log2(10000.0);
             S.run(SGD_K_GEMM_QKV, [&] { return launch_gemm(dt, g, e, S.st); });
+            attention(qb, kb, vtb, N, m->np, SGD_K_ATTN);
+            resid(SGD_K_GEMM_O, ob, dd, dd, w.w_o, w.b_o, mod_l ? mod_l + 2 * dd : nullptr, dl, dmode(), nullptr);
         }
-        attention(qb, kb, vtb, N, m->np, SGD_K_ATTN);
-        resid(SGD_K_GEMM_O, ob, dd, dd, w.w_o, w.b_o, mod_l ? mod_l + 2 * dd : nullptr, dl, dl ? (unet ? 2 : 1) : 0,
-              nullptr);
-        // cross-attention branch (SDXL)
-        if (sdxl) {
+        if (sdxl && (br < 0 || br == BR_XATTN)) {
             char* ckv = plan.ckv ? plan.ckv + (size_t)l * m->ckv_unit : S.ws + m->w_ckv;
             if (!plan.ckv) ctx_kv(l, ckv);
             norm((const float*)w.normx_w, (const float*)w.normx_b, nullptr, nullptr);
@@ -495,23 +532,23 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
             e.kind = EP_HEADS; e.q = qb; e.ntok = N; e.np = m->np; e.H = H; e.dh = dh; e.d = dd;
             S.run(SGD_K_GEMM_X, [&] { return launch_gemm(dt, g, e, S.st); });
             attention(qb, ckv, ckv + cheads * m->es, d.ctx_len, m->npc, SGD_K_ATTN_X);
-            resid(SGD_K_GEMM_X, ob, dd, dd, w.w_xo, w.b_xo, nullptr, dl, dl ? 2 : 0, nullptr);
+            resid(SGD_K_GEMM_X, ob, dd, dd, w.w_xo, w.b_xo, nullptr, dl, dmode(), nullptr);
         }
-        // MLP branch
-        norm((const float*)w.norm2_w, (const float*)w.norm2_b, mod_l ? mod_l + 3 * dd : nullptr,
-             mod_l ? mod_l + 4 * dd : nullptr);
-        {
+        if (br < 0 || br == BR_MLP) {
+            norm((const float*)w.norm2_w, (const float*)w.norm2_b, mod_l ? mod_l + 3 * dd : nullptr,
+                 mod_l ? mod_l + 4 * dd : nullptr);
             GemmArgs g;
             g.A0 = xb; g.lda0 = dd; g.B = w.w1; g.ldb = dd; g.M = (int)M; g.N = gated ? 2 * F : F; g.K = dd;
             EpiParams e;
             e.kind = gated ? EP_GATED : EP_ACT; e.bias = (const float*)w.b1; e.out = hid; e.ldo = F; e.act = mlp_act;
             e.F = F;
             S.run(SGD_K_GEMM_W1, [&] { return launch_gemm(dt, g, e, S.st); });
+            // the MLP is a block's last branch: the block's output copy goes with it
+            resid(SGD_K_GEMM_W2, hid, F, F, w.w2, w.b2, mod_l ? mod_l + 5 * dd : nullptr, dl, dmode(), out_copy(l));
         }
-        resid(SGD_K_GEMM_W2, hid, F, F, w.w2, w.b2, mod_l ? mod_l + 5 * dd : nullptr, dl, dl ? 2 : 0, out_copy(l));
-        ++l;
+        ++u;
     }
-    if (dr && dr->have_prev) S.run(SGD_K_DRIFT, [&] { return launch_sumsq_finish(dr->partial, L, dr->sums, S.st); });
+    if (dr && dr->have_prev) S.run(SGD_K_DRIFT, [&] { return launch_sumsq_finish(dr->partial, nu, dr->sums, S.st); });
     if (plan.sampler)
         S.run(SGD_K_STATE, [&] {
             return launch_state_update((float*)state, h, d.B, N, dd, d.update_row_begin, d.update_row_end, args->alpha,
@@ -545,7 +582,7 @@ float* cache_delta(const sgd_model* m, const sgd_cache* c, int l) {
 // refresh their cached update (except at the last step, which no later step reads).
 int masked_step(sgd_model* m, void* state, int32_t step, const uint8_t* row, sgd_cache* cache,
                 const sgd_step_args* args, const DriftRec* drift, hipStream_t st) {
-    const int L = m->d.L;
+    const int L = m->nu;  // scheduled units
     std::vector<const float*> dread(L, nullptr);
     std::vector<float*> dwrite(L, nullptr);
     std::vector<uint8_t> act(L);
@@ -579,7 +616,7 @@ extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const s
     int rc = check_step_args(m, state, step, args);
     if (rc) return rc;
     const sgd_model_desc& d = m->d;
-    const int L = d.L;
+    const int L = m->nu;  // scheduled units
     std::vector<uint8_t> act(L, 1);
     std::vector<int> life(L, d.T);
     std::vector<const float*> dread(L, nullptr);

@@ -25,13 +25,13 @@ namespace {
 
 size_t slot_bytes(const sgd_model* m) { return align256((size_t)m->M * m->d.d * 4); }
 
-// drift buffer: [L] unit-input slots, [L][kSumBlocks][2] partial sums, [L][2] sums
+// drift buffer: [U] unit-input slots, [U][kSumBlocks][2] partial sums, [U][2] sums (U scheduled units)
 struct DriftLayout {
     size_t prev, partial, sums, total;
 };
 DriftLayout drift_layout(const sgd_model* m) {
     DriftLayout o;
-    const int L = m->d.L;
+    const int L = m->nu;
     o.prev = 0;
     o.partial = (size_t)L * slot_bytes(m);
     o.sums = o.partial + align256((size_t)L * kSumBlocks * 2 * sizeof(double));
@@ -63,7 +63,7 @@ extern "C" int sgd_drift_step(sgd_model* m, void* state, int32_t step, const sgd
     int rc = check_step_args(m, state, step, args);
     if (rc) return rc;
     if ((rc = check_cache(m, cache, step))) return rc;
-    const int L = m->d.L, T = m->d.T;
+    const int L = m->nu, T = m->d.T;  // scheduled units
     if (!sched || sched->L != L || sched->T != T || !sched->active)
         return fail(SGD_E_ARG, "schedule does not match the model");
     const DriftLayout lay = drift_layout(m);
@@ -100,21 +100,21 @@ extern "C" int sgd_drift_step(sgd_model* m, void* state, int32_t step, const sgd
 
 namespace {
 
-// replay buffer: z, h of the unscheduled evaluation, h of a candidate, 2 L update slots,
-// SDXL context K/V, [L][kSumBlocks][2] partial sums, [L][2] sums
+// replay buffer: z, h of the unscheduled evaluation, h of a candidate, 2 U update slots (U
+// scheduled units), SDXL context K/V (one per block), [U][kSumBlocks][2] partial sums, [U][2] sums
 struct ReplayLayout {
     size_t z, href, hcand, slots, ckv, partial, sums, total;
 };
 ReplayLayout replay_layout(const sgd_model* m) {
     ReplayLayout o;
-    const int L = m->d.L;
+    const int L = m->nu;
     const size_t sb = slot_bytes(m);
     o.z = 0;
     o.href = sb;
     o.hcand = 2 * sb;
     o.slots = 3 * sb;
     o.ckv = o.slots + 2 * (size_t)L * sb;
-    o.partial = o.ckv + (arch_cross(m->d.arch) ? (size_t)L * m->ckv_unit : 0);
+    o.partial = o.ckv + (arch_cross(m->d.arch) ? (size_t)m->d.L * m->ckv_unit : 0);
     o.sums = o.partial + align256((size_t)L * kSumBlocks * 2 * sizeof(double));
     o.total = o.sums + align256((size_t)L * 2 * sizeof(double));
     return o;
@@ -140,7 +140,7 @@ extern "C" int sgd_replay_search(sgd_model* m, const void* z1, const sgd_replay_
     int rc = check_step_args(m, base + lay.z, 1, args);
     if (rc) return rc;
     const sgd_model_desc& d = m->d;
-    const int L = d.L, T = d.T;
+    const int L = m->nu, T = d.T;  // scheduled units
     const int64_t ceiling = p->max_layer_steps > 0 ? p->max_layer_steps : (int64_t)L * T;
     if (ceiling < L) return fail(SGD_E_BUDGET, "the ceiling is below one full first step");
     hipStream_t st = (hipStream_t)hip_stream;

@@ -15,6 +15,8 @@ struct sgd_model {
     int np = 64;      // tokens padded to 64
     int npc = 64;     // context tokens padded to 64
     long M = 0;
+    int nb = 1;       // scheduled units per block (1, or the block's branches)
+    int nu = 0;       // scheduled units: L nb
     // workspace layout
     size_t w_h, w_xb, w_q, w_k, w_vt, w_ob, w_hid, w_siluc, w_mod, w_hb, w_skip, w_ckv, w_gn, w_total;
     // cache layout
@@ -41,6 +43,10 @@ namespace sgd {
 size_t align256(size_t x);
 bool arch_gated(int arch);
 bool arch_cross(int arch);  // SDXL-style units with a cross-attention branch
+// residual branches of a block, in execution order
+enum Branch { BR_RESNET = 0, BR_ATTN = 1, BR_XATTN = 2, BR_MLP = 3 };
+int block_branches(int arch);         // branches per block: 2, 3 or 4
+int block_branch(int arch, int i);    // the i-th branch of a block (Branch)
 
 // Drift recording of one step (the input-aware baseline): for every unit, the squared norm
 // of the change of its input since the previous recorded step and the squared norm of the

@@ -46,16 +46,28 @@ def rel_err(x: np.ndarray, ref: np.ndarray) -> float:
     return float(np.max(np.abs(np.asarray(x, np.float64) - ref)) / max(np.max(np.abs(ref)), 1e-30))
 
 
-def oracle_schedule(cfg, weights, pct):
-    raw = [osp.unit_score(osp.unit_matrices(u, cfg.d, cfg.dtype), cfg.dh).raw for u in weights]
+def unit_raw_scores(cfg, weights, granularity="block"):
+    """The oracle's raw score q~ of every scheduled unit: per block, or per residual branch."""
+    raw = []
+    for u in weights:
+        mats = osp.unit_matrices(u, cfg.d, cfg.dtype)
+        if granularity == "branch":
+            raw += [osp.unit_score(osp.branch_matrices(mats, b), cfg.dh).raw for b in om.branches(cfg.arch)]
+        else:
+            raw.append(osp.unit_score(mats, cfg.dh).raw)
+    return np.array(raw)
+
+
+def oracle_schedule(cfg, weights, pct, granularity="block"):
+    raw = unit_raw_scores(cfg, weights, granularity)
     lam = osp.normalise(raw)
-    n = osch.budget_layer_steps(pct, cfg.L, cfg.T)
+    n = osch.budget_layer_steps(pct, len(raw), cfg.T)
     bs = osch.lifetimes_budget(lam, cfg.T, n, osch.s_min_default(cfg.T))
-    return np.array(raw), lam, bs
+    return raw, lam, bs
 
 
-def oracle_trajectory(cfg, weights, inputs, mask, steps=None):
-    m = om.Model(cfg, weights, inputs)
+def oracle_trajectory(cfg, weights, inputs, mask, steps=None, granularity="block"):
+    m = om.Model(cfg, weights, inputs, granularity=granularity)
     return om.trajectory(m, inputs["z"], mask, steps)
 
 
@@ -98,17 +110,17 @@ def gpu_teacher_forced(dm, cfg, oracle_z, z0, sched):
     return out
 
 
-def chaos_floor(cfg, weights, inputs, mask, rels=(1e-7, 1e-5), seeds=(1, 2)):
+def chaos_floor(cfg, weights, inputs, mask, rels=(1e-7, 1e-5), seeds=(1, 2), granularity="block"):
     """Divergence of the oracle from itself when its initial state is perturbed (relative
     perturbations `rels`, seeded): the sensitivity of the bf16-quantised trajectory map.
     Returns the unperturbed trajectory and, per step, the largest divergence observed."""
-    a = oracle_trajectory(cfg, weights, inputs, mask)
+    a = oracle_trajectory(cfg, weights, inputs, mask, granularity=granularity)
     floor = [0.0] * len(a.z)
     for rel in rels:
         for seed in seeds:
             x2 = dict(inputs)
             rng = np.random.default_rng(seed)
             x2["z"] = (inputs["z"] * (1 + rel * rng.standard_normal(inputs["z"].shape))).astype(np.float32)
-            b = oracle_trajectory(cfg, weights, x2, mask)
+            b = oracle_trajectory(cfg, weights, x2, mask, granularity=granularity)
             floor = [max(f, rel_err(p, q)) for f, p, q in zip(floor, b.z, a.z)]
     return a, floor

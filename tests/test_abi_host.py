@@ -163,3 +163,47 @@ def test_rule_schedules_from_stats_match_oracle(rule):
         got = P.schedule_from_stats(roles, [dh] * L, np.array(rows), T, budget_pct=pct, rule=rule)
         assert np.array_equal(got.unit_raw, ru.raw_scores(rule, stats, dh))
         assert np.array_equal(got.lifetimes, ref.lifetimes)
+
+
+@pytest.mark.parametrize("arch,nb", [("tiny", 2), ("llada", 2), ("dit", 2), ("uvit", 2), ("sdxl", 3), ("sdxl_unet", 4)])
+def test_model_units_by_granularity(arch, nb):
+    """sgd_model_create validates and lays out without touching device memory, so the unit count
+    and the cache size of both granularities are checked here with stand-in pointers (never
+    dereferenced): L block units, or L nb branch units with one cache slot each."""
+    import ctypes as C
+    lib = _lib_or_skip()
+    b = P.binding
+    L, B, N, d, H, dh, F = (3 if arch == "uvit" else 2), 1, 64, 256, 2, 128, 512
+    fake = 1 << 20  # 1 MiB-aligned stand-in address
+    cw = (b.sgd_unit_weights * L)()
+    for l in range(L):
+        for name in b._W_FIELDS:
+            setattr(cw[l], name, fake)
+
+    def create(granularity):
+        dsc = b.sgd_model_desc()
+        dsc.arch, dsc.dtype = b.SGD_ARCH[arch], b.SGD_BF16
+        dsc.B, dsc.N, dsc.d, dsc.H, dsc.head_dim, dsc.F, dsc.L, dsc.T = B, N, d, H, dh, F, L, 10
+        dsc.ctx_len, dsc.ctx_dim = 77, 256
+        dsc.update_row_begin, dsc.update_row_end = 0, N
+        dsc.class_emb, dsc.ctx = fake, fake
+        dsc.units = C.cast(cw, C.POINTER(b.sgd_unit_weights))
+        dsc.grid, dsc.groups = 8, 32
+        dsc.granularity = granularity
+        h = C.c_void_p()
+        rc = lib.sgd_model_create(C.byref(dsc), C.byref(h))
+        return rc, h
+
+    sizes = {}
+    for g, units in ((b.SGD_UNIT["block"], L), (b.SGD_UNIT["branch"], L * nb)):
+        rc, h = create(g)
+        assert rc == 0, lib.sgd_last_error()
+        nu, cb = C.c_int32(), C.c_size_t()
+        assert lib.sgd_model_units(h, C.byref(nu)) == 0 and nu.value == units
+        assert lib.sgd_cache_bytes(h, C.byref(cb)) == 0
+        sizes[g] = cb.value
+        assert lib.sgd_model_destroy(h) == 0
+    slot = B * N * d * 4  # one fp32 [B, N, d] update, 256-byte aligned already
+    assert sizes[1] - sizes[0] == (nb - 1) * L * slot
+    rc, _ = create(2)
+    assert rc == -1 and b"granularity" in lib.sgd_last_error()
