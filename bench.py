@@ -118,6 +118,9 @@ def main() -> int:
     ap.add_argument("--no-input-aware", action="store_true",
                     help="skip the activation-drift policy and the oracle-replay search")
     ap.add_argument("--tau-agree", type=float, default=5e-3, help="oracle-replay tolerance")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip timing the headline schedule as a replayed HIP graph (e.g. under a kernel tracer, "
+                         "whose dispatch accounting expects eager launches only)")
     ap.add_argument("--no-branch-units", action="store_true",
                     help="skip the branch-granular schedule (every residual branch a unit of its own)")
     args = ap.parse_args()
@@ -250,6 +253,32 @@ def main() -> int:
             f"-> {rate(times):.2f} steps/s")
     value_head = rate(results[head])
     act_head = np.asarray(scheds[head].active, np.uint8)
+    def graph_timed(sched):
+        """The schedule captured as one HIP graph per trajectory (sgd_graph_capture), one
+        warm-up replay, then n_traj replays bracketed by HIP events on a stream of its own."""
+        gstream = torch.cuda.Stream()
+        torch.cuda.synchronize()
+        evs = []
+        with torch.cuda.stream(gstream):
+            graph = dm.capture(z, sched, cache, gstream)
+            z.copy_(z0)
+            graph.launch(gstream)
+            for _ in range(n_traj):
+                z.copy_(z0)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(gstream)
+                graph.launch(gstream)
+                e1.record(gstream)
+                evs.append((e0, e1))
+        gstream.synchronize()
+        graph.close()
+        return [a.elapsed_time(b) for a, b in evs]
+
+    t_graph = None
+    if not args.no_graph:
+        t_graph = graph_timed(scheds[head])
+        log(f"budget {head}% as one HIP graph per trajectory: median {np.median(t_graph):.2f} ms -> "
+            f"{rate(t_graph):.2f} steps/s (eager launches {value_head:.2f})")
     t_all, _ = timed(all_active)
     z_full = z.clone()  # the all-active trajectory's final state
     log(f"all-active: median {np.median(t_all):.2f} ms per trajectory -> {rate(t_all):.2f} steps/s")
@@ -421,6 +450,7 @@ def main() -> int:
         "config": {"workload": f"{cfg.name}: B={cfg.B} N={cfg.N} d={cfg.d} H={cfg.H} F={cfg.F} L={L} T={T}",
                    "budget_pct": head, "layer_steps": lay[head], "of": L * T,
                    "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "single GPU"},
+        "graph_steps_per_s": round(rate(t_graph), 3) if t_graph else None,
         "all_active_steps_per_s": round(all_rate, 3),
         "speedup_vs_all_active": round(value / all_rate, 4),
         "skipped_layer_step_fraction": round(1 - active_frac, 4),

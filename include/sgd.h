@@ -311,6 +311,31 @@ typedef struct {
 int sgd_denoise_step(sgd_model* model, void* state, int32_t step, const sgd_schedule* sched,
                      sgd_cache* cache, const sgd_step_args* args, void* hip_stream);
 
+/* ---------------------------------------------------------------- graphs */
+
+/* A whole scheduled trajectory captured as one HIP graph: the executor the paper describes
+ * for a static active/frozen pattern (Sec. 4.2: the pattern is known before generation, so
+ * the launch sequence of every step is fixed), one graph launch per trajectory instead of
+ * one launch per kernel. */
+typedef struct sgd_graph sgd_graph;
+
+/* Captures sgd_denoise_step at s = 1..T with `sched` (NULL: the unscheduled forward), each
+ * with its sampler update, on hip_stream (a non-null stream; nothing runs during capture).
+ *   alpha, beta  host [T]: the sampler coefficients of steps 1..T
+ *   state, cache, workspace: the buffers every launch of the graph uses (their addresses are
+ *                recorded); cache may be NULL when sched is NULL
+ * Each sgd_graph_launch runs the T steps on `state` in place (the caller writes z_1 first)
+ * and writes every cache slot before a frozen step reads it, so nothing of an earlier
+ * trajectory is read.  Arguments are validated as for sgd_denoise_step; the cache is left
+ * reset (host bookkeeping) after capture.  Refused (SGD_E_ARG) while kernel-class
+ * profiling is on.  The graph owns no device buffer. */
+int sgd_graph_capture(sgd_model* model, void* state, const sgd_schedule* sched, sgd_cache* cache,
+                      const float* alpha, const float* beta, void* workspace, size_t workspace_bytes,
+                      void* hip_stream, sgd_graph** out);
+/* Enqueues one replay of the captured trajectory on hip_stream. */
+int sgd_graph_launch(sgd_graph* graph, void* hip_stream);
+int sgd_graph_destroy(sgd_graph* graph);
+
 /* ---------------------------------------------------------- no allocation */
 
 /* Size of the library's fixed device scratch: 96 MiB, held by every GPU the library runs on

@@ -92,7 +92,8 @@ EXPORTS = ["sgd_last_error", "sgd_version", "sgd_s_min_default", "sgd_budget_lay
            "sgd_schedule_from_stats",
            "sgd_schedule_from_lifetimes", "sgd_model_create", "sgd_model_destroy", "sgd_model_units", "sgd_workspace_bytes",
            "sgd_cache_bytes", "sgd_cache_bind", "sgd_cache_reset", "sgd_cache_destroy", "sgd_denoise_step",
-           "sgd_denoise_step_noalloc", "sgd_denoise_step_masked", "sgd_drift_bytes", "sgd_drift_step", "sgd_replay_bytes", "sgd_replay_search",
+           "sgd_denoise_step_noalloc", "sgd_graph_capture", "sgd_graph_launch", "sgd_graph_destroy",
+           "sgd_denoise_step_masked", "sgd_drift_bytes", "sgd_drift_step", "sgd_replay_bytes", "sgd_replay_search",
            "sgd_profile_begin", "sgd_profile_end", "sgd_op_linear", "sgd_op_attention", "sgd_op_norm",
            "sgd_op_frozen_run", "sgd_op_heads", "sgd_op_residual", "sgd_op_adaln_mod", "sgd_op_group_norm_silu",
            "sgd_op_group_norm_scratch_bytes", "sgd_op_conv3x3"]
@@ -121,6 +122,10 @@ def lib() -> C.CDLL:
             "sgd_model_create": [C.POINTER(sgd_model_desc), C.POINTER(vp)],
             "sgd_model_destroy": [vp],
             "sgd_model_units": [vp, C.POINTER(C.c_int32)],
+            "sgd_graph_capture": [vp, vp, C.POINTER(sgd_schedule), vp, C.POINTER(C.c_float), C.POINTER(C.c_float),
+                                  vp, C.c_size_t, vp, C.POINTER(vp)],
+            "sgd_graph_launch": [vp, vp],
+            "sgd_graph_destroy": [vp],
             "sgd_workspace_bytes": [vp, C.POINTER(C.c_size_t)],
             "sgd_cache_bytes": [vp, C.POINTER(C.c_size_t)],
             "sgd_cache_bind": [vp, vp, C.c_size_t, C.POINTER(vp)],
@@ -516,6 +521,21 @@ class DeviceModel:
         a.workspace_bytes = self.workspace.numel()
         return a
 
+    def capture(self, state, sched: Optional[Schedule], cache: Optional["Cache"], stream, alpha=1.0, beta=None):
+        """The whole T-step trajectory on ``state`` as one HIP graph (sgd_graph_capture), captured
+        on ``stream`` (a torch.cuda.Stream, not the null stream)."""
+        T = self.cfg.T
+        al = np.full(T, alpha, np.float32)
+        be = np.full(T, (1.0 / T) if beta is None else beta, np.float32)
+        g = C.c_void_p()
+        _check(lib().sgd_graph_capture(self.h, C.c_void_p(state.data_ptr()),
+                                       C.byref(sched.c) if sched is not None else None,
+                                       cache.h if cache is not None else None,
+                                       al.ctypes.data_as(C.POINTER(C.c_float)), be.ctypes.data_as(C.POINTER(C.c_float)),
+                                       C.c_void_p(self.workspace.data_ptr()), self.workspace.numel(),
+                                       C.c_void_p(_stream_ptr(stream)), C.byref(g)))
+        return Graph(g, keep=(state, sched, cache, self))
+
     def step_noalloc(self, state, s: int, sched: Optional[Schedule], cache: Optional["Cache"], alpha=1.0, beta=None,
                      stream=None) -> None:
         """sgd_denoise_step on the library's fixed scratch (no workspace, no allocation)."""
@@ -584,6 +604,27 @@ class DeviceModel:
     def close(self) -> None:
         if getattr(self, "h", None):
             lib().sgd_model_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Graph:
+    """A captured trajectory (sgd_graph); keeps the buffers whose addresses it recorded alive."""
+
+    def __init__(self, h, keep):
+        self.h, self._keep = h, keep
+
+    def launch(self, stream) -> None:
+        _check(lib().sgd_graph_launch(self.h, C.c_void_p(_stream_ptr(stream))))
+
+    def close(self) -> None:
+        if getattr(self, "h", None):
+            lib().sgd_graph_destroy(self.h)
             self.h = None
 
     def __del__(self):

@@ -654,6 +654,64 @@ extern "C" int sgd_denoise_step(sgd_model* m, void* state, int32_t step, const s
     return SGD_OK;
 }
 
+// ---------------------------------------------------------------------------- graphs
+
+struct sgd_graph {
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+};
+
+extern "C" int sgd_graph_capture(sgd_model* m, void* state, const sgd_schedule* sched, sgd_cache* cache,
+                                 const float* alpha, const float* beta, void* workspace, size_t workspace_bytes,
+                                 void* hip_stream, sgd_graph** out) {
+    if (!m || !state || !alpha || !beta || !out) return fail(SGD_E_ARG, "NULL argument");
+    if (!hip_stream) return fail(SGD_E_ARG, "capture needs a non-null stream");
+    if (m->prof_class >= 0) return fail(SGD_E_ARG, "kernel-class profiling is on");
+    if (sched && !cache) return fail(SGD_E_ARG, "a scheduled trajectory needs a cache");
+    if (cache && cache->m != m) return fail(SGD_E_ARG, "cache bound to another model");
+    sgd_step_args a{alpha[0], beta[0], workspace, workspace_bytes};
+    int rc = check_step_args(m, state, 1, &a);  // before capture: nothing to unwind
+    if (rc) return rc;
+    hipStream_t st = (hipStream_t)hip_stream;
+    if (cache) sgd_cache_reset(cache);
+    hipError_t e = hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamBeginCapture");
+    for (int s = 1; s <= m->d.T && rc == SGD_OK; ++s) {
+        a.alpha = alpha[s - 1];
+        a.beta = beta[s - 1];
+        rc = sgd_denoise_step(m, state, s, sched, sched ? cache : nullptr, &a, hip_stream);
+    }
+    hipGraph_t g = nullptr;
+    e = hipStreamEndCapture(st, &g);
+    if (cache) sgd_cache_reset(cache);
+    if (rc != SGD_OK || e != hipSuccess) {
+        if (g) (void)hipGraphDestroy(g);
+        return rc != SGD_OK ? rc : hip_fail(e, "hipStreamEndCapture");
+    }
+    hipGraphExec_t ex = nullptr;
+    e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    if (e != hipSuccess) {
+        (void)hipGraphDestroy(g);
+        return hip_fail(e, "hipGraphInstantiate");
+    }
+    *out = new sgd_graph{g, ex};
+    return SGD_OK;
+}
+
+extern "C" int sgd_graph_launch(sgd_graph* g, void* hip_stream) {
+    if (!g) return fail(SGD_E_ARG, "NULL graph");
+    hipError_t e = hipGraphLaunch(g->exec, (hipStream_t)hip_stream);
+    return e == hipSuccess ? SGD_OK : hip_fail(e, "hipGraphLaunch");
+}
+
+extern "C" int sgd_graph_destroy(sgd_graph* g) {
+    if (!g) return fail(SGD_E_ARG, "NULL graph");
+    if (g->exec) (void)hipGraphExecDestroy(g->exec);
+    if (g->graph) (void)hipGraphDestroy(g->graph);
+    delete g;
+    return SGD_OK;
+}
+
 extern "C" int sgd_denoise_step_masked(sgd_model* m, void* state, int32_t step, const uint8_t* active,
                                        sgd_cache* cache, const sgd_step_args* args, void* hip_stream) {
     int rc = check_step_args(m, state, step, args);

@@ -2,7 +2,7 @@
 
     rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o <w> -- \\
         python3 bench.py --config <w> --no-cpu-baseline --no-kernel-table --taus "" --rules "" \\
-        --lifetimes <lifetimes.json>
+        --no-input-aware --no-graph --lifetimes <lifetimes.json>
     python -m paper_2609_29505_amd.trace_report --workload <w> --trace <dir>/<w>_kernel_trace.csv \\
         --lifetimes <lifetimes.json>
 
@@ -11,7 +11,9 @@ trace's own durations: bench.py launches the budgets in increasing order, each a
 steps and three timed T-step trajectories (then the all-active schedule, and the headline budget twice
 with per-launch events), so the frozen-run dispatches appear in a known order and each
 one's algorithmic bytes follow from the schedule (maximal runs of frozen units, as the
-launcher fuses them).
+launcher fuses them).  The traced run must launch nothing else that carries frozen units:
+no drift policy or replay (--no-input-aware), no graph replays (--no-graph); with
+--lifetimes, bench.py also skips the branch-unit schedule.
 """
 from __future__ import annotations
 
