@@ -44,6 +44,16 @@ int sgd_op_norm(int32_t dtype, int32_t kind, const float* x, void* y, int32_t M,
                 const float* w, const float* b, const float* shift, const float* scale, int64_t mod_ld,
                 int32_t ntok, void* hip_stream);
 
+/* The pre-norm that absorbs a frozen run (what the launcher runs when a run of frozen units
+ * ends at an active unit, Sec. 3.1 frozen rule): x <- x + deltas[0] + ... + deltas[r-1],
+ * added in that order and written back to x (fp32 [M x d], the residual stream), then y = the
+ * pre-norm of the new x exactly as sgd_op_norm computes it.  1 <= r <= 32; deltas: r device
+ * pointers (host array) to fp32 [M x d], 16-byte aligned.  Bitwise the same as
+ * sgd_op_frozen_run followed by sgd_op_norm. */
+int sgd_op_norm_fold(int32_t dtype, int32_t kind, float* x, void* y, int32_t M, int32_t d, float eps,
+                     const float* w, const float* b, const float* shift, const float* scale, int64_t mod_ld,
+                     int32_t ntok, const float* const* deltas, int32_t r, void* hip_stream);
+
 /* Projection into attention heads (the QKV GEMM of a unit): P = A[M x K] W[n_proj*d x K]^T
  * (+ bias), column n of P belongs to projection which0 + n / d (0: q, 1: k, 2: v^T), head
  * (n % d) / dh, dim n % dh; row r is token r % ntok of sample r / ntok.  q, k are

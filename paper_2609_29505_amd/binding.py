@@ -94,7 +94,7 @@ EXPORTS = ["sgd_last_error", "sgd_version", "sgd_s_min_default", "sgd_budget_lay
            "sgd_cache_bytes", "sgd_cache_bind", "sgd_cache_reset", "sgd_cache_destroy", "sgd_denoise_step",
            "sgd_denoise_step_noalloc", "sgd_graph_capture", "sgd_graph_launch", "sgd_graph_destroy",
            "sgd_denoise_step_masked", "sgd_drift_bytes", "sgd_drift_step", "sgd_replay_bytes", "sgd_replay_search",
-           "sgd_profile_begin", "sgd_profile_end", "sgd_op_linear", "sgd_op_attention", "sgd_op_norm",
+           "sgd_profile_begin", "sgd_profile_end", "sgd_op_linear", "sgd_op_attention", "sgd_op_norm", "sgd_op_norm_fold",
            "sgd_op_frozen_run", "sgd_op_heads", "sgd_op_residual", "sgd_op_adaln_mod", "sgd_op_group_norm_silu",
            "sgd_op_group_norm_scratch_bytes", "sgd_op_conv3x3"]
 
@@ -145,6 +145,8 @@ def lib() -> C.CDLL:
             "sgd_op_linear": [i32, vp, i64, vp, i64, vp, vp, i64, i32, i32, i32, i32, i32, i32, vp],
             "sgd_op_attention": [i32, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp],
             "sgd_op_norm": [i32, i32, vp, vp, i32, i32, C.c_float, vp, vp, vp, vp, i64, i32, vp],
+            "sgd_op_norm_fold": [i32, i32, vp, vp, i32, i32, C.c_float, vp, vp, vp, vp, i64, i32,
+                                 C.POINTER(vp), i32, vp],
             "sgd_op_frozen_run": [vp, C.POINTER(vp), i32, i64, vp],
             "sgd_op_heads": [i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, vp],
             "sgd_op_residual": [i32, vp, i64, vp, vp, vp, vp, i32, vp, i64, i32, i32, i32, i32, i32, vp],
@@ -371,6 +373,15 @@ def op_norm(kind, x, y, eps, w=None, b=None, shift=None, scale=None, ntok=1, str
     mod_ld = shift.stride(0) if shift is not None else 0
     _check(lib().sgd_op_norm(_dtype_code(y), kind, _p(x), _p(y), M, d, eps, _p(w), _p(b), _p(shift), _p(scale),
                              mod_ld, ntok, C.c_void_p(_stream_ptr(stream))))
+
+
+def op_norm_fold(kind, x, y, eps, deltas, w=None, b=None, shift=None, scale=None, ntok=1, stream=None) -> None:
+    """x += deltas[0] + ... (in order, written back), then the pre-norm of x into y."""
+    M, d = x.shape
+    mod_ld = shift.stride(0) if shift is not None else 0
+    arr = (C.c_void_p * len(deltas))(*[t.data_ptr() for t in deltas])
+    _check(lib().sgd_op_norm_fold(_dtype_code(y), kind, _p(x), _p(y), M, d, eps, _p(w), _p(b), _p(shift), _p(scale),
+                                  mod_ld, ntok, arr, len(deltas), C.c_void_p(_stream_ptr(stream))))
 
 
 def op_heads(A, W, q, k, vt, n_proj, which0, ntok, H, dh, bias=None, rope=False, tile=0, stream=None) -> None:

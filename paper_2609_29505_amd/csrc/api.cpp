@@ -859,6 +859,28 @@ extern "C" int sgd_op_norm(int32_t dtype, int32_t kind, const float* x, void* y,
     return SGD_OK;
 }
 
+extern "C" int sgd_op_norm_fold(int32_t dtype, int32_t kind, float* x, void* y, int32_t M, int32_t d, float eps,
+                                const float* w, const float* b, const float* shift, const float* scale, int64_t mod_ld,
+                                int32_t ntok, const float* const* deltas, int32_t r, void* hip_stream) {
+    if (!x || !y || !deltas) return fail(SGD_E_ARG, "NULL argument");
+    if (dtype != SGD_F32 && dtype != SGD_BF16) return fail(SGD_E_DTYPE, "dtype must be F32 or BF16");
+    if (kind < 0 || kind > 2 || M < 1 || d < 4 || d % 4 || d > 8192) return fail(SGD_E_SHAPE, "norm shape not supported");
+    if (r < 1 || r > kMaxRun) return fail(SGD_E_ARG, "1 <= r <= 32 cached updates");
+    if ((kind == 0 && !w) || (kind == 1 && (!w || !b)) || (kind == 2 && (!shift || !scale || ntok < 1)))
+        return fail(SGD_E_ARG, "missing norm parameters");
+    if ((uintptr_t)x % 16 || (uintptr_t)w % 16 || (uintptr_t)b % 16 || (uintptr_t)shift % 16 || (uintptr_t)scale % 16 ||
+        mod_ld % 4 || (uintptr_t)y % (dtype == SGD_BF16 ? 8 : 16))
+        return fail(SGD_E_ARG, "norm operands must be 16-byte aligned (bf16 output: 8)");
+    NormArgs a{x, y, M, d, kind, eps, w, b, shift, scale, mod_ld, ntok};
+    a.nfold = r;
+    for (int i = 0; i < r; ++i) {
+        if (!deltas[i] || (uintptr_t)deltas[i] % 16) return fail(SGD_E_ARG, "NULL or misaligned delta");
+        a.fold[i] = deltas[i];
+    }
+    SGD_HIP_TRY(launch_norm(dtype == SGD_BF16 ? 1 : 0, a, (hipStream_t)hip_stream));
+    return SGD_OK;
+}
+
 extern "C" int sgd_op_frozen_run(float* h, const float* const* deltas, int32_t r, int64_t n, void* hip_stream) {
     if (!h || !deltas || r < 1 || r > kMaxRun || n < 4 || n % 4) return fail(SGD_E_ARG, "bad frozen-run arguments");
     FrozenRun f{};

@@ -54,19 +54,31 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
         v[i] = (live && c < nvec) ? ((const float4*)x)[c] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
     if (FOLD && live) {
-        // the frozen run ending at this unit: its cached updates in stack order, written back
+        // the frozen run ending at this unit: its cached updates in stack order, written back.
+        // G updates are loaded together before they are added (still one at a time, in stack
+        // order), so a run costs one memory round trip per group of G, not per update; G keeps
+        // at most 16 float4 of updates in registers.
         const long roff = (long)row * nvec;
-        for (int k = 0; k < a.nfold; ++k) {
-            const float4* dk = (const float4*)a.fold[k] + roff;
+        constexpr int G = VPL >= 16 ? 1 : (16 / VPL < 4 ? 16 / VPL : 4);
+        for (int k0 = 0; k0 < a.nfold; k0 += G) {
+            float4 dv[G][VPL];
 #pragma unroll
-            for (int i = 0; i < VPL; ++i) {
-                const int c = t + i * TPR;
-                if (c < nvec) {
-                    const float4 dv = dk[c];
-                    v[i].x = v[i].x + dv.x;
-                    v[i].y = v[i].y + dv.y;
-                    v[i].z = v[i].z + dv.z;
-                    v[i].w = v[i].w + dv.w;
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int i = 0; i < VPL; ++i) {
+                    const int c = t + i * TPR;
+                    dv[g][i] = (k0 + g < a.nfold && c < nvec) ? ((const float4*)a.fold[k0 + g] + roff)[c]
+                                                              : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                if (k0 + g >= a.nfold) break;
+#pragma unroll
+                for (int i = 0; i < VPL; ++i) {
+                    v[i].x = v[i].x + dv[g][i].x;
+                    v[i].y = v[i].y + dv[g][i].y;
+                    v[i].z = v[i].z + dv[g][i].z;
+                    v[i].w = v[i].w + dv[g][i].w;
                 }
             }
         }
@@ -76,15 +88,18 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
             if (c < nvec) ((float4*)x)[c] = v[i];
         }
     }
+    // every multiply-add below is an explicit fmaf (or an explicit plain product): the compiler
+    // may contract a*b + c differently in different instantiations, and a pre-norm that absorbed
+    // a frozen run must give bitwise the rows of the plain one
 #pragma unroll
     for (int i = 0; i < VPL; ++i)
-        s += (a.kind == 0) ? (v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w)
+        s += (a.kind == 0) ? fmaf(v[i].w, v[i].w, fmaf(v[i].z, v[i].z, fmaf(v[i].y, v[i].y, v[i].x * v[i].x)))
                            : (v[i].x + v[i].y + v[i].z + v[i].w);
     s = row_sum<WPR>(s, red);
     const float invd = 1.0f / (float)a.d;
     float mean = 0.f, rstd;
     if (a.kind == 0) {
-        rstd = 1.0f / sqrtf(s * invd + a.eps);
+        rstd = 1.0f / sqrtf(fmaf(s, invd, a.eps));
     } else {
         mean = s * invd;
         float q = 0.f;
@@ -93,11 +108,11 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
             const int c = t + i * TPR;
             if (c < nvec) {
                 const float dx = v[i].x - mean, dy = v[i].y - mean, dz = v[i].z - mean, dw = v[i].w - mean;
-                q += dx * dx + dy * dy + dz * dz + dw * dw;
+                q += fmaf(dw, dw, fmaf(dz, dz, fmaf(dy, dy, dx * dx)));
             }
         }
         q = row_sum<WPR>(q, red);
-        rstd = 1.0f / sqrtf(q * invd + a.eps);
+        rstd = 1.0f / sqrtf(fmaf(q, invd, a.eps));
     }
     if (!live) return;
     OutT* y = (OutT*)a.y + (long)row * a.d;
@@ -112,11 +127,12 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
             o[0] *= w.x; o[1] *= w.y; o[2] *= w.z; o[3] *= w.w;
         } else if (a.kind == 1) {
             const float4 w = ((const float4*)a.w)[c], b = ((const float4*)a.b)[c];
-            o[0] = o[0] * w.x + b.x; o[1] = o[1] * w.y + b.y; o[2] = o[2] * w.z + b.z; o[3] = o[3] * w.w + b.w;
+            o[0] = fmaf(o[0], w.x, b.x); o[1] = fmaf(o[1], w.y, b.y);
+            o[2] = fmaf(o[2], w.z, b.z); o[3] = fmaf(o[3], w.w, b.w);
         } else {
             const float4 sc = *(const float4*)(a.scale + mrow + c * 4), sh = *(const float4*)(a.shift + mrow + c * 4);
-            o[0] = o[0] * (1.0f + sc.x) + sh.x; o[1] = o[1] * (1.0f + sc.y) + sh.y;
-            o[2] = o[2] * (1.0f + sc.z) + sh.z; o[3] = o[3] * (1.0f + sc.w) + sh.w;
+            o[0] = fmaf(o[0], 1.0f + sc.x, sh.x); o[1] = fmaf(o[1], 1.0f + sc.y, sh.y);
+            o[2] = fmaf(o[2], 1.0f + sc.z, sh.z); o[3] = fmaf(o[3], 1.0f + sc.w, sh.w);
         }
         store4<OutT>(y + c * 4, o[0], o[1], o[2], o[3]);
     }

@@ -235,6 +235,35 @@ def test_norm(P, dtype, kind, d, M):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("kind,d,M,r", [(0, 4096, 1024, 1), (0, 4096, 1024, 3), (0, 4096, 1024, 9), (1, 1280, 4099, 2),
+                                        (1, 1024, 4099, 5), (2, 1152, 4099, 4), (0, 256, 70, 32), (2, 1152, 70, 7)])
+def test_norm_fold_bitwise(P, dtype, kind, d, M, r):
+    """The pre-norm that absorbs a frozen run: the stream and the normalised rows bit for bit
+    those of the frozen-run pass followed by the plain pre-norm, for runs of 1 to 32 updates
+    (loaded in groups, added one at a time in stack order) and every norm kind and row split."""
+    import torch
+    rng = np.random.default_rng(kind * 1000 + d + M + r)
+    ntok = 35 if M == 70 else 4099
+    x = (rng.standard_normal((M, d)) * 3 + 0.5).astype(np.float32)
+    deltas = [dev((rng.standard_normal((M, d)) * 0.7).astype(np.float32)) for _ in range(r)]
+    w = dev((1 + 0.1 * rng.standard_normal(d)).astype(np.float32))
+    b = dev((0.1 * rng.standard_normal(d)).astype(np.float32))
+    md = dev(rng.standard_normal((-(-M // ntok), 6 * d)).astype(np.float32))
+    kw = {"w": w} if kind == 0 else {"w": w, "b": b} if kind == 1 else {"shift": md[:, :d], "scale": md[:, d:2 * d],
+                                                                         "ntok": ntok}
+    eps = 1e-6 if kind == 2 else 1e-5
+    x1, x2 = dev(x), dev(x)
+    y1, y2 = empty((M, d), dtype), empty((M, d), dtype)
+    P.op_frozen_run(x1.view(-1), [t.view(-1) for t in deltas])
+    P.op_norm(kind, x1, y1, eps, **kw)
+    P.op_norm_fold(kind, x2, y2, eps, deltas, **kw)
+    torch.cuda.synchronize()
+    bits = (lambda t: t.view(torch.int16)) if dtype == "bf16" else (lambda t: t.view(torch.int32))
+    assert torch.equal(x1.view(torch.int32), x2.view(torch.int32))
+    assert torch.equal(bits(y1), bits(y2))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("B,d,n_out", [(32, 1152, 6912), (2, 1152, 6912), (5, 256, 200), (40, 128, 96), (3, 64, 32)])
 def test_adaln_mod(P, dtype, B, d, n_out):
     """DiT modulation vectors SiLU(c) W_ada^T + b: fp32 accumulation of the exact products
