@@ -182,3 +182,27 @@ def test_branch_drift_policy(P, name):
     print(name, "branch units, drift teacher-forced errors", ["%.2e" % e for e in errs])
     assert max(errs) <= TOL[cfg.dtype], errs
     dm.close()
+
+
+@pytest.mark.parametrize("granularity", ["block", "branch"])
+@pytest.mark.parametrize("pattern", ["tail_active", "alternating_long"])
+def test_runs_longer_than_one_launch(P, granularity, pattern):
+    """Frozen runs longer than the 32 updates one launch takes (40 blocks, 80 branch units):
+    the launcher splits them, launches the full segments on their own and hands the last one
+    to the next active unit's pre-norm; fp32 teacher-forced against the oracle (1e-4)."""
+    cfg = synth.get_config("tiny_ragged", L=40)
+    w, x = synth.model_weights(cfg), synth.inputs(cfg)
+    dm = P.DeviceModel(cfg, w, x, granularity=granularity)
+    U = dm.n_units
+    if pattern == "tail_active":
+        S = np.ones(U, int)
+        S[-1] = cfg.T
+    else:
+        S = np.array([cfg.T if j in (0, 37, 38, U - 1) else 1 for j in range(U)])
+    mask = osch.active_mask(S, cfg.T)
+    ref = oracle_trajectory(cfg, w, x, mask, granularity=granularity)
+    got = gpu_teacher_forced(dm, cfg, ref.z, x["z"], P.schedule_from_lifetimes(S, cfg.T))
+    errs = [rel_err(g, r) for g, r in zip(got, ref.z)]
+    print(granularity, pattern, "per-step error", ["%.2e" % e for e in errs])
+    assert max(errs) <= TOL["f32"], errs
+    dm.close()
