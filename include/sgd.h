@@ -156,7 +156,8 @@ typedef struct {
 } sgd_sched_params;
 
 /* Output of the schedule calls.  The caller allocates every array on the host; optional
- * arrays may be NULL.  L and T are filled in by the library.
+ * arrays may be NULL.  L and T are filled in by the library; L counts the scheduled units
+ * (the sgd_unit list: blocks or single branches, see sgd_granularity).
  *   lifetimes  [L]      S_l
  *   active     [T*L]    active[(s-1)*L + l] = (s <= S_l)
  *   unit_raw   [L]      raw unit score q~_l of the rule        (optional)
