@@ -154,6 +154,11 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
     __syncthreads();  // padding zeroed
     lstore(0, 0);
     __syncthreads();
+    // Every load issued so far (the query fragments, block 0) has completed on the main path;
+    // saying so for every path keeps the waitcnt insertion from treating the query fragments
+    // as possibly in flight inside the loop, where it would wait on the loop's own key/value
+    // prefetch before each score MFMA and serialise the prefetch.
+    __builtin_amdgcn_s_waitcnt(0);
     for (int kb = 0; kb < nkb; ++kb) {
         const int k0 = kb * BKV;
         const int buf = kb & 1;
@@ -374,6 +379,11 @@ __global__ __launch_bounds__(2 * NQG * 64, 2) void attn_split_bf16_kernel(AttnAr
     if (kh < nkb) lstore(kh * BKV, 0);
     if (kh + 2 < nkb) gload((kh + 2) * BKV);
     __syncthreads();
+    // Wait for every load issued so far (the query fragments, and block 2 + kh, which the first
+    // iteration stores to LDS right away anyway): otherwise the waitcnt insertion treats the
+    // query fragments as possibly in flight inside the loop (on paths that skip a prologue
+    // store) and waits on the loop's own key/value prefetch before each score MFMA.
+    __builtin_amdgcn_s_waitcnt(0);
     for (int it = 0; it < nit; ++it) {
         const int kb = 2 * it + kh;
         const int k0 = kb * BKV;
