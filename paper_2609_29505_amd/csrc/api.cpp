@@ -165,7 +165,9 @@ extern "C" int sgd_model_create(const sgd_model_desc* desc, sgd_model** out) {
     m->w_hid = take((size_t)m->M * d.F * m->es);
     const bool cond = d.arch == SGD_ARCH_DIT || d.arch == SGD_ARCH_SDXL_UNET;
     m->w_siluc = take(cond ? (size_t)d.B * d.d * 4 : 0);
-    m->w_mod = take(cond ? (size_t)d.B * (d.arch == SGD_ARCH_DIT ? 6 : 1) * d.d * 4 : 0);
+    // one modulation slot per block: a step computes every needed block's in one launch
+    m->mod_slot = cond ? align256((size_t)d.B * (d.arch == SGD_ARCH_DIT ? 6 : 1) * d.d * 4) : 0;
+    m->w_mod = take(m->mod_slot * d.L);
     m->w_hb = take(d.arch == SGD_ARCH_UVIT ? 2 * Md * m->es : 0);
     m->w_skip = take(d.arch == SGD_ARCH_UVIT ? (size_t)(d.L / 2) * align256(Md * m->es) : 0);
     m->ckv_unit = align256(2 * cheads * m->es);
@@ -336,7 +338,6 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
     void* ob = S.ws + m->w_ob;
     void* hid = S.ws + m->w_hid;
     float* siluc = (float*)(S.ws + m->w_siluc);
-    float* mod = (float*)(S.ws + m->w_mod);
     auto hb = [&](int i) { return (void*)(S.ws + m->w_hb + i * Md * m->es); };
     auto skipbuf = [&](int i) { return (void*)(S.ws + m->w_skip + (size_t)i * align256(Md * m->es)); };
     const bool uvit = d.arch == SGD_ARCH_UVIT, dit = d.arch == SGD_ARCH_DIT, sdxl = arch_cross(d.arch);
@@ -368,6 +369,31 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
     };
     if (sdxl && plan.ckv && plan.ckv_fill)
         for (int l = 0; l < L; ++l) ctx_kv(l, plan.ckv + (size_t)l * m->ckv_unit);
+
+    // block l's modulation (DiT: AdaLN shift, scale and gate of both branches; UNet: the ResNet
+    // branch's time projection) for every block whose consumer runs this step, in one launch
+    // per kMaxModUnits blocks instead of one per block
+    auto mod_of = [&](int l) { return (float*)(S.ws + m->w_mod + (size_t)l * m->mod_slot); };
+    if (dit || unet) {
+        ModBatch mb;
+        auto flush = [&] {
+            if (!mb.n) return;
+            S.run(SGD_K_COND, [&] {
+                return launch_adaln_mod_batch(dt, siluc, mb, d.B, dd, dit ? 6 * dd : dd, S.st);
+            });
+            mb.n = 0;
+        };
+        for (int l = 0; l < L; ++l) {
+            bool need = false;  // DiT: any unit of the block; UNet: its ResNet branch (the first)
+            for (int k = 0; k < (dit ? m->nb : 1); ++k) need = need || act[l * m->nb + k];
+            if (!need) continue;
+            mb.W[mb.n] = dit ? m->u[l].w_ada : m->u[l].w_temb;
+            mb.bias[mb.n] = (const float*)(dit ? m->u[l].b_ada : m->u[l].b_temb);
+            mb.mod[mb.n] = mod_of(l);
+            if (++mb.n == kMaxModUnits) flush();
+        }
+        flush();
+    }
 
     // a frozen run that ends at an active unit is added by that unit's first norm kernel
     // (same additions, same order) instead of a pass of its own
@@ -418,7 +444,6 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
     auto last_of_block = [&](int u) { return u % nb == nb - 1; };
     // a U-ViT out-block's first unit: its skip linear reads h before anything else
     auto out_start = [&](int u) { return uvit && u / nb > half && u % nb == 0; };
-    int mod_block = -1;  // DiT: the block whose modulation `mod` holds
 
     int u = 0;
     while (u < nu && S.err == hipSuccess) {
@@ -474,24 +499,12 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
         // branch's update and adds the later ones; a branch unit stores its own
         bool first = true;
         auto dmode = [&]() { const int r = dl ? (first || nb > 1 ? 1 : 2) : 0; first = false; return r; };
-        const float* mod_l = nullptr;
-        if (dit) {
-            if (mod_block != l) {
-                S.run(SGD_K_COND, [&] {
-                    return launch_adaln_mod(dt, siluc, w.w_ada, (const float*)w.b_ada, mod, d.B, dd, 6 * dd, S.st);
-                });
-                mod_block = l;
-            }
-            mod_l = mod;
-        }
+        const float* mod_l = dit ? mod_of(l) : nullptr;
         const int br = branch_of(u);
         if (unet && (br < 0 || br == BR_RESNET)) {
-            // ResNet block: the unit's time projection, GroupNorm + SiLU, 3x3 convolution (+ bias
-            // + time projection) into the hidden buffer, GroupNorm + SiLU, 3x3 convolution added
-            // to the stream
-            S.run(SGD_K_COND, [&] {
-                return launch_adaln_mod(dt, siluc, w.w_temb, (const float*)w.b_temb, mod, d.B, dd, dd, S.st);
-            });
+            // ResNet block: GroupNorm + SiLU, 3x3 convolution (+ bias + the block's time
+            // projection, computed with the step's modulations) into the hidden buffer,
+            // GroupNorm + SiLU, 3x3 convolution added to the stream
             GroupNormArgs gn{h, xb, d.B, N, dd, d.groups, 1e-5f, (const float*)w.gn1_w, (const float*)w.gn1_b};
             S.run(SGD_K_GNORM, [&] { return launch_group_norm_silu(0, gn, S.ws + m->w_gn, S.st); });
             GemmArgs g;
@@ -499,7 +512,7 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
             g.conv_side = d.grid; g.conv_c = dd;
             EpiParams e;
             e.kind = EP_ACT; e.bias = (const float*)w.b_conv1; e.out = hid; e.ldo = dd; e.act = ACT_NONE;
-            e.rowbias = mod; e.rowbias_ld = dd; e.ntok = N;
+            e.rowbias = mod_of(l); e.rowbias_ld = dd; e.ntok = N;
             S.run(SGD_K_GEMM_CONV, [&] { return launch_gemm(dt, g, e, S.st); });
             GroupNormArgs gn2{hid, xb, d.B, N, dd, d.groups, 1e-5f, (const float*)w.gn2_w, (const float*)w.gn2_b};
             S.run(SGD_K_GNORM, [&] { return launch_group_norm_silu(1, gn2, S.ws + m->w_gn, S.st); });

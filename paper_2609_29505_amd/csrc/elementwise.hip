@@ -244,8 +244,10 @@ template <> struct Wvec<float> {
 };
 
 template <typename WT>
-__global__ __launch_bounds__(256) void adaln_mod_kernel(const float* x, const WT* W, const float* bias,
-                                                        float* mod, int B, int d, int n_out) {
+__global__ __launch_bounds__(256) void adaln_mod_kernel(const float* x, ModBatch mb, int B, int d, int n_out) {
+    const WT* W = (const WT*)mb.W[blockIdx.z];
+    const float* bias = mb.bias[blockIdx.z];
+    float* mod = mb.mod[blockIdx.z];
     constexpr int FJ = 64, SB = 32, KC = 64, LD = KC + 4;
     constexpr int WV = Wvec<WT>::PER;                     // weights per vector load
     constexpr int WLOADS = FJ * KC / WV / 256;            // weight vectors per thread per chunk
@@ -329,54 +331,77 @@ __global__ __launch_bounds__(256) void adaln_mod_kernel(const float* x, const WT
 // three bf16 parts, x = hi + mid + lo (each part the round-to-nearest-even bf16 of what the
 // previous parts leave: x - hi has at most 16 significant bits and x - hi - mid at most 8, so
 // hi + mid + lo == x exactly), and bf16 x bf16 products are exact in fp32: the MFMAs sum the
-// fp32 products of the FMA kernel above, in another order.  A workgroup owns 32 features x 32 samples
-// (v_mfma_f32_32x32x16_bf16: A = the x parts, one sample per lane row; B = the weight rows,
-// one feature per lane column); its sixteen waves take consecutive 16-deep k steps, every
-// lane loads its operands straight from global memory (16 bytes of weights, 32 bytes of x
-// per step, all steps of a wave issued together), and the partial tiles are summed in LDS
-// in wave order (deterministic).
-constexpr int kModWaves = 16, kModChunk = 5;
-__global__ __launch_bounds__(kModWaves * 64) void adaln_mod_mfma_kernel(const float* x, const bf16* W,
-                                                                        const float* bias, float* mod, int B,
-                                                                        int d, int n_out) {
+// fp32 products of the FMA kernel above, in another order.  A workgroup owns 32 features x 32
+// samples (v_mfma_f32_32x32x16_bf16: A = the x parts, one sample per lane row; B = the weight
+// rows, one feature per lane column) and walks k in chunks of 256: the chunk's 32 weight rows
+// and 32 x rows are read with 16-byte loads in which every wave covers whole 128-byte lines
+// (reading the MFMA layout straight from memory touches 32 lines per load instruction, and the
+// kernel was bound by that request rate), stored to LDS, and wave w takes the chunk's k step w.
+// A thread issues the loads of up to kModG chunks before storing the first (one memory round
+// trip for d <= 1536).  The partial tiles of the sixteen waves are summed in LDS in wave order
+// (deterministic).
+constexpr int kModWaves = 16, kModKC = 16 * kModWaves, kModG = 6;
+constexpr int kModWS = kModKC * 2 + 16, kModXS = kModKC * 4 + 16;  // padded LDS row bytes
+__global__ __launch_bounds__(kModWaves * 64) void adaln_mod_mfma_kernel(const float* x, ModBatch mb, int B, int d,
+                                                                        int n_out) {
+    const bf16* W = (const bf16*)mb.W[blockIdx.z];
+    const float* bias = mb.bias[blockIdx.z];
+    float* mod = mb.mod[blockIdx.z];
+    __shared__ __attribute__((aligned(16))) char sw[32 * kModWS];
+    __shared__ __attribute__((aligned(16))) char sx[32 * kModXS];
     __shared__ float red[kModWaves][32 * 32];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int j0 = blockIdx.x * 32, b0 = blockIdx.y * 32;
-    const int col = lane & 31, kh = (lane >> 5) * 8;
-    const int steps = d / 16;
-    const int s0 = wave * steps / kModWaves, s1 = (wave + 1) * steps / kModWaves;
-    const bool jin = j0 + col < n_out, bin = b0 + col < B;
-    const bf16* wrow = W + (long)(jin ? j0 + col : 0) * d + kh;
-    const float* xrow = x + (long)(bin ? b0 + col : 0) * d + kh;
+    // loads of a chunk: weight row tid / 32, bytes 16 (tid % 32) of its 512; x rows tid / 64
+    // and tid / 64 + 16, bytes 16 (tid % 64) of their 1024
+    const int wr = tid >> 5, wc = (tid & 31) * 16, xr = tid >> 6, xc = (tid & 63) * 16;
+    const bool win = j0 + wr < n_out, xin0 = b0 + xr < B, xin1 = b0 + xr + 16 < B;
+    const char* wsrc = (const char*)(W + (long)(win ? j0 + wr : 0) * d) + wc;
+    const char* xsrc0 = (const char*)(x + (long)(xin0 ? b0 + xr : 0) * d) + xc;
+    const char* xsrc1 = (const char*)(x + (long)(xin1 ? b0 + xr + 16 : 0) * d) + xc;
+    // fragments: lane l reads row l % 32 at k offset 8 (l / 32) of the wave's k step
+    const int col = lane & 31, fk = wave * 16 + (lane >> 5) * 8;
+    const char* fw = sw + col * kModWS + fk * 2;
+    const char* fx = sx + col * kModXS + fk * 4;
+    const int nch = (d + kModKC - 1) / kModKC;
     f32x16 acc;
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-    for (int s = s0; s < s1; s += kModChunk) {
-        u32x4 wv[kModChunk];
-        f32x4 xa[kModChunk], xb[kModChunk];
+    for (int c0 = 0; c0 < nch; c0 += kModG) {
+        u32x4 rw[kModG], rx0[kModG], rx1[kModG];
+        const u32x4 z{0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int c = 0; c < kModChunk; ++c) {
-            const bool ok = s + c < s1;
-            const int k = (s + c) * 16;
-            wv[c] = ok && jin ? *(const u32x4*)(wrow + k) : u32x4{0u, 0u, 0u, 0u};
-            xa[c] = ok && bin ? *(const f32x4*)(xrow + k) : f32x4{0.f, 0.f, 0.f, 0.f};
-            xb[c] = ok && bin ? *(const f32x4*)(xrow + k + 4) : f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int g = 0; g < kModG; ++g) {
+            const int kb = (c0 + g) * kModKC;  // (d is a multiple of 16: a load lies wholly inside or past d)
+            const bool kw = c0 + g < nch && kb + wc / 2 < d, kx = c0 + g < nch && kb + xc / 4 < d;
+            rw[g] = win && kw ? *(const u32x4*)(wsrc + (long)kb * 2) : z;
+            rx0[g] = xin0 && kx ? *(const u32x4*)(xsrc0 + (long)kb * 4) : z;
+            rx1[g] = xin1 && kx ? *(const u32x4*)(xsrc1 + (long)kb * 4) : z;
         }
 #pragma unroll
-        for (int c = 0; c < kModChunk; ++c) {
-            bf16x8 hi, mid, lo;
+        for (int g = 0; g < kModG; ++g) {
+            if (c0 + g >= nch) break;
+            __syncthreads();  // every wave has read the previous chunk's fragments
+            *(u32x4*)(sw + wr * kModWS + wc) = rw[g];
+            *(u32x4*)(sx + xr * kModXS + xc) = rx0[g];
+            *(u32x4*)(sx + (xr + 16) * kModXS + xc) = rx1[g];
+            __syncthreads();
+            if ((c0 + g) * kModKC + wave * 16 < d) {
+                const bf16x8 wf = *(const bf16x8*)fw;
+                const f32x4 xa = *(const f32x4*)fx, xb = *(const f32x4*)(fx + 16);
+                bf16x8 hi, mid, lo;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float v = e < 4 ? xa[c][e] : xb[c][e - 4];
-                hi[e] = f2bf(v);
-                const float r1 = v - bf2f(hi[e]);
-                mid[e] = f2bf(r1);
-                lo[e] = f2bf(r1 - bf2f(mid[e]));
+                for (int e = 0; e < 8; ++e) {
+                    const float v = e < 4 ? xa[e] : xb[e - 4];
+                    hi[e] = f2bf(v);
+                    const float r1 = v - bf2f(hi[e]);
+                    mid[e] = f2bf(r1);
+                    lo[e] = f2bf(r1 - bf2f(mid[e]));
+                }
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lo, wf, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(mid, wf, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(hi, wf, acc, 0, 0, 0);
             }
-            const bf16x8 wf = __builtin_bit_cast(bf16x8, wv[c]);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lo, wf, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(mid, wf, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(hi, wf, acc, 0, 0, 0);
         }
     }
     // lane l holds feature column l % 32 and, for register r, sample row
@@ -391,18 +416,28 @@ __global__ __launch_bounds__(kModWaves * 64) void adaln_mod_mfma_kernel(const fl
     if (b0 + i < B && j0 + j < n_out) mod[(long)(b0 + i) * n_out + j0 + j] = v + (bias ? bias[j0 + j] : 0.f);
 }
 
-hipError_t launch_adaln_mod(int dtype, const float* x, const void* W, const float* bias, float* mod, int B,
-                            int d, int n_out, hipStream_t st) {
+hipError_t launch_adaln_mod_batch(int dtype, const float* x, const ModBatch& mb, int B, int d, int n_out,
+                                  hipStream_t st) {
     if (d % 64) return hipErrorInvalidValue;  // whole 64-deep k chunks (the model requires d % 128 == 0)
+    if (mb.n < 1 || mb.n > kMaxModUnits) return hipErrorInvalidValue;
     if (dtype == 1) {
-        dim3 grid((n_out + 31) / 32, (B + 31) / 32), block(kModWaves * 64);
-        hipLaunchKernelGGL(adaln_mod_mfma_kernel, grid, block, 0, st, x, (const bf16*)W, bias, mod, B, d, n_out);
+        dim3 grid((n_out + 31) / 32, (B + 31) / 32, mb.n), block(kModWaves * 64);
+        hipLaunchKernelGGL(adaln_mod_mfma_kernel, grid, block, 0, st, x, mb, B, d, n_out);
     } else {
-        dim3 grid((n_out + 63) / 64, (B + 31) / 32), block(256);
-        hipLaunchKernelGGL(adaln_mod_kernel<float>, grid, block, 0, st, x, (const float*)W, bias, mod, B, d,
-                           n_out);
+        dim3 grid((n_out + 63) / 64, (B + 31) / 32, mb.n), block(256);
+        hipLaunchKernelGGL(adaln_mod_kernel<float>, grid, block, 0, st, x, mb, B, d, n_out);
     }
     return hipGetLastError();
+}
+
+hipError_t launch_adaln_mod(int dtype, const float* x, const void* W, const float* bias, float* mod, int B,
+                            int d, int n_out, hipStream_t st) {
+    ModBatch mb;
+    mb.n = 1;
+    mb.W[0] = W;
+    mb.bias[0] = bias;
+    mb.mod[0] = mod;
+    return launch_adaln_mod_batch(dtype, x, mb, B, d, n_out, st);
 }
 
 __global__ __launch_bounds__(256) void to_bf16_kernel(const float* x, bf16* y, long n) {

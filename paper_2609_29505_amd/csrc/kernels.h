@@ -114,6 +114,18 @@ hipError_t launch_cond_silu(const float* y, float* x, int B, int d, float t, hip
 // mod[b, j] = sum_k x[b, k] W[j, k] + bias[j]  (DiT AdaLN modulation, W dtype)
 hipError_t launch_adaln_mod(int dtype, const float* x, const void* W, const float* bias, float* mod,
                             int B, int d, int n_out, hipStream_t st);
+// The same product for several units at once (one x, each unit its own W, bias and output):
+// one launch, the unit in the grid's third dimension, each unit's tiles computed exactly as a
+// single-unit launch computes them.
+constexpr int kMaxModUnits = 32;
+struct ModBatch {
+    int n = 0;
+    const void* W[kMaxModUnits] = {};
+    const float* bias[kMaxModUnits] = {};
+    float* mod[kMaxModUnits] = {};
+};
+hipError_t launch_adaln_mod_batch(int dtype, const float* x, const ModBatch& mb, int B, int d, int n_out,
+                                  hipStream_t st);
 // fp32 -> bf16 copy
 hipError_t launch_to_bf16(const float* x, void* y, long n, hipStream_t st);
 

@@ -19,6 +19,7 @@ struct sgd_model {
     int nu = 0;       // scheduled units: L nb
     // workspace layout
     size_t w_h, w_xb, w_q, w_k, w_vt, w_ob, w_hid, w_siluc, w_mod, w_hb, w_skip, w_ckv, w_gn, w_total;
+    size_t mod_slot = 0;  // bytes of one block's modulation in the workspace
     // cache layout
     size_t c_delta, c_ctx, c_total;
     size_t ckv_unit;  // bytes of one unit's context K and V^T

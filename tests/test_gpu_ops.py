@@ -264,10 +264,13 @@ def test_norm_fold_bitwise(P, dtype, kind, d, M, r):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("B,d,n_out", [(32, 1152, 6912), (2, 1152, 6912), (5, 256, 200), (40, 128, 96), (3, 64, 32)])
+@pytest.mark.parametrize("B,d,n_out", [(32, 1152, 6912), (2, 1152, 6912), (5, 256, 200), (40, 128, 96), (3, 64, 32),
+                                         (8, 1280, 1280), (33, 2048, 100), (4, 1600, 70)])
 def test_adaln_mod(P, dtype, B, d, n_out):
     """DiT modulation vectors SiLU(c) W_ada^T + b: fp32 accumulation of the exact products
-    (bf16 weights run on the matrix cores with x split into three bf16 parts)."""
+    (bf16 weights run on the matrix cores with x split into three bf16 parts).  Shapes: DiT,
+    the UNet time projection, ragged features and samples, and k ranges of several load groups
+    of 256-deep chunks with a partial last chunk."""
     rng = np.random.default_rng(B * 7 + d + n_out)
     x = om.silu(rng.standard_normal((B, d))).astype(np.float32)
     W = synth.store(rng.standard_normal((n_out, d)) / np.sqrt(d), dtype)
