@@ -416,11 +416,134 @@ __global__ __launch_bounds__(kModWaves * 64) void adaln_mod_mfma_kernel(const fl
     if (b0 + i < B && j0 + j < n_out) mod[(long)(b0 + i) * n_out + j0 + j] = v + (bias ? bias[j0 + j] : 0.f);
 }
 
+// Wide variant for many output features (the DiT modulation, 6 d outputs per block): a
+// workgroup owns 32 samples x 32 WV features and each of its WV waves owns 32 features over
+// the whole k range, so no partial tiles are exchanged and SiLU(c) is read once per 32 WV
+// features.  k goes in 64-deep chunks through LDS: x split once into its three bf16 parts by
+// the thread that loads it, the weight rows with 16-byte loads covering whole 128-byte lines;
+// every thread keeps the loads of kWideG chunks in flight.  Per output the products go into
+// one accumulator, k step by k step (lo, mid, hi each), whatever WV is: the launcher picks WV
+// for the grid size and the results do not depend on it.
+constexpr int kWideKC = 64, kWideG = 3;
+constexpr int kWideRS = kWideKC * 2 + 16;  // padded LDS row bytes (bf16 weights and x parts)
+template <int WV>
+__global__ __launch_bounds__(WV * 64) void adaln_mod_wide_kernel(const float* x, ModBatch mb, int B, int d,
+                                                                 int n_out) {
+    constexpr int NT = WV * 64, FW = WV * 32, XP = 512 / NT;  // x passes per chunk
+    __shared__ __attribute__((aligned(16))) char sw[FW * kWideRS];
+    __shared__ __attribute__((aligned(16))) char sx[3 * 32 * kWideRS];
+    const bf16* W = (const bf16*)mb.W[blockIdx.z];
+    const float* bias = mb.bias[blockIdx.z];
+    float* mod = mb.mod[blockIdx.z];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int j0 = blockIdx.x * FW, b0 = blockIdx.y * 32;
+    // loads of a chunk: x rows tid / 16 + (NT / 16) p, floats 4 (tid % 16) .. + 3 of their 64;
+    // weight rows tid / 8 + (NT / 8) i, bf16 8 (tid % 8) .. + 7 of their 64
+    const int xr = tid >> 4, xe = (tid & 15) * 4, wr = tid >> 3, we = (tid & 7) * 8;
+    bool xin[XP], win[4];
+    const float* xsrc[XP];
+    const bf16* wsrc[4];
+#pragma unroll
+    for (int p = 0; p < XP; ++p) {
+        const int b = b0 + xr + (NT / 16) * p;
+        xin[p] = b < B;
+        xsrc[p] = x + (long)(xin[p] ? b : 0) * d + xe;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int j = j0 + wr + (NT / 8) * i;
+        win[i] = j < n_out;
+        wsrc[i] = W + (long)(win[i] ? j : 0) * d + we;
+    }
+    // fragments: lane l takes x parts of sample l % 32 and weight row 32 wave + l % 32, at k
+    // offset 8 (l / 32) of each 16-deep step
+    const int col = lane & 31, kh = (lane >> 5) * 8;
+    const char* fw = sw + (wave * 32 + col) * kWideRS + kh * 2;
+    const char* fx = sx + col * kWideRS + kh * 2;
+    const int nch = d / kWideKC;
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+    for (int c0 = 0; c0 < nch; c0 += kWideG) {
+        f32x4 rx[kWideG][XP];
+        u32x4 rw[kWideG][4];
+#pragma unroll
+        for (int g = 0; g < kWideG; ++g) {
+            const bool ok = c0 + g < nch;
+            const int k = (c0 + g) * kWideKC;
+#pragma unroll
+            for (int p = 0; p < XP; ++p)
+                rx[g][p] = ok && xin[p] ? *(const f32x4*)(xsrc[p] + k) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                rw[g][i] = ok && win[i] ? *(const u32x4*)(wsrc[i] + k) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int g = 0; g < kWideG; ++g) {
+            if (c0 + g >= nch) break;
+            __syncthreads();  // every wave has read the previous chunk's fragments
+#pragma unroll
+            for (int p = 0; p < XP; ++p) {
+                bf16x4 hi, mid, lo;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float v = rx[g][p][e];
+                    hi[e] = f2bf(v);
+                    const float r1 = v - bf2f(hi[e]);
+                    mid[e] = f2bf(r1);
+                    lo[e] = f2bf(r1 - bf2f(mid[e]));
+                }
+                char* xd = sx + (xr + (NT / 16) * p) * kWideRS + xe * 2;
+                *(bf16x4*)xd = hi;
+                *(bf16x4*)(xd + 32 * kWideRS) = mid;
+                *(bf16x4*)(xd + 64 * kWideRS) = lo;
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) *(u32x4*)(sw + (wr + (NT / 8) * i) * kWideRS + we * 2) = rw[g][i];
+            __syncthreads();
+#pragma unroll
+            for (int q = 0; q < kWideKC / 16; ++q) {
+                const bf16x8 wf = *(const bf16x8*)(fw + q * 32);
+                const bf16x8 xh = *(const bf16x8*)(fx + q * 32);
+                const bf16x8 xm = *(const bf16x8*)(fx + 32 * kWideRS + q * 32);
+                const bf16x8 xl = *(const bf16x8*)(fx + 64 * kWideRS + q * 32);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xl, wf, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xm, wf, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xh, wf, acc, 0, 0, 0);
+            }
+        }
+    }
+    // lane l holds feature 32 wave + l % 32 and, for register r, sample row
+    // (r / 4) * 8 + (l / 32) * 4 + r % 4 of the tile
+    const int j = j0 + wave * 32 + col;
+    if (j >= n_out) return;
+    const float bj = bias ? bias[j] : 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int i = (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        if (b0 + i < B) mod[(long)(b0 + i) * n_out + j] = acc[r] + bj;
+    }
+}
+
 hipError_t launch_adaln_mod_batch(int dtype, const float* x, const ModBatch& mb, int B, int d, int n_out,
                                   hipStream_t st) {
     if (d % 64) return hipErrorInvalidValue;  // whole 64-deep k chunks (the model requires d % 128 == 0)
     if (mb.n < 1 || mb.n > kMaxModUnits) return hipErrorInvalidValue;
-    if (dtype == 1) {
+    if (dtype == 1 && n_out >= 2048) {
+        // many features (DiT: 6 d per block): the widest workgroups that still give two per CU
+        const long tiles = (long)((B + 31) / 32) * mb.n;
+        const auto groups = [&](int wv) { return (long)((n_out + 32 * wv - 1) / (32 * wv)) * tiles; };
+        if (groups(8) >= 512) {
+            dim3 grid((n_out + 255) / 256, (B + 31) / 32, mb.n);
+            hipLaunchKernelGGL(adaln_mod_wide_kernel<8>, grid, dim3(512), 0, st, x, mb, B, d, n_out);
+        } else if (groups(4) >= 512) {
+            dim3 grid((n_out + 127) / 128, (B + 31) / 32, mb.n);
+            hipLaunchKernelGGL(adaln_mod_wide_kernel<4>, grid, dim3(256), 0, st, x, mb, B, d, n_out);
+        } else {
+            dim3 grid((n_out + 63) / 64, (B + 31) / 32, mb.n);
+            hipLaunchKernelGGL(adaln_mod_wide_kernel<2>, grid, dim3(128), 0, st, x, mb, B, d, n_out);
+        }
+    } else if (dtype == 1) {
         dim3 grid((n_out + 31) / 32, (B + 31) / 32, mb.n), block(kModWaves * 64);
         hipLaunchKernelGGL(adaln_mod_mfma_kernel, grid, block, 0, st, x, mb, B, d, n_out);
     } else {

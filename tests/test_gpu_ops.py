@@ -265,12 +265,14 @@ def test_norm_fold_bitwise(P, dtype, kind, d, M, r):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("B,d,n_out", [(32, 1152, 6912), (2, 1152, 6912), (5, 256, 200), (40, 128, 96), (3, 64, 32),
-                                         (8, 1280, 1280), (33, 2048, 100), (4, 1600, 70)])
+                                         (8, 1280, 1280), (33, 2048, 100), (4, 1600, 70), (40, 320, 2100),
+                                         (3, 64, 2048)])
 def test_adaln_mod(P, dtype, B, d, n_out):
     """DiT modulation vectors SiLU(c) W_ada^T + b: fp32 accumulation of the exact products
     (bf16 weights run on the matrix cores with x split into three bf16 parts).  Shapes: DiT,
-    the UNet time projection, ragged features and samples, and k ranges of several load groups
-    of 256-deep chunks with a partial last chunk."""
+    the UNet time projection, ragged features and samples, k ranges of several load groups with
+    a partial last chunk, and the wide variant (2048 outputs or more) with ragged features,
+    more than 32 samples and one or several load groups."""
     rng = np.random.default_rng(B * 7 + d + n_out)
     x = om.silu(rng.standard_normal((B, d))).astype(np.float32)
     W = synth.store(rng.standard_normal((n_out, d)) / np.sqrt(d), dtype)
@@ -279,6 +281,27 @@ def test_adaln_mod(P, dtype, B, d, n_out):
     P.op_adaln_mod(dev(x), dev(W), mod, bias=dev(b))
     ref = x.astype(np.float64) @ decode(W, dtype).T + b
     assert relmax(host(mod), ref) < 2e-6
+
+
+def test_adaln_mod_wide_widths_bitwise(P):
+    """The wide modulation kernel (2048 outputs or more) takes workgroups of eight, four or two
+    waves as the grid size allows, and computes every output in the same order whatever the
+    width: the rows of a 512-sample problem (eight-wave workgroups) equal those of its 256- and
+    32-sample slices (four- and two-wave workgroups) bit for bit."""
+    rng = np.random.default_rng(5)
+    B, d, n_out = 512, 256, 8192
+    x = om.silu(rng.standard_normal((B, d))).astype(np.float32)
+    W = synth.store(rng.standard_normal((n_out, d)) / np.sqrt(d), "bf16")
+    b = synth.representable(0.02 * rng.standard_normal(n_out), "f32")
+    outs = []
+    for nb in (512, 256, 32):
+        mod = empty((nb, n_out), "f32")
+        P.op_adaln_mod(dev(np.ascontiguousarray(x[:nb])), dev(W), mod, bias=dev(b))
+        outs.append(host(mod))
+    ref = x[:32].astype(np.float64) @ decode(W, "bf16").T + b
+    assert relmax(outs[2], ref) < 2e-6
+    assert np.array_equal(outs[0][:256], outs[1])
+    assert np.array_equal(outs[0][:32], outs[2])
 
 
 def test_frozen_run_bitwise(P):
