@@ -487,7 +487,7 @@ def kernel_table(cfg, n_traj, T, profile) -> dict:
     es = 2 if cfg.dtype == "bf16" else 4
     peak = PEAK_BF16 if cfg.dtype == "bf16" else PEAK_F32
     fl = unit_flops(cfg)
-    classes = ["gemm_qkv", "attn", "gemm_o", "gemm_w1", "gemm_w2", "norm"]
+    classes = ["gemm_qkv", "attn", "gemm_o", "gemm_w1", "gemm_w2", "norm", "norm_parts"]
     if cfg.arch in ("sdxl", "sdxl_unet"):
         classes += ["gemm_x", "attn_x"]
     if cfg.arch == "sdxl_unet":
@@ -509,8 +509,10 @@ def kernel_table(cfg, n_traj, T, profile) -> dict:
             nbytes = M * d * ((4 + 2) + (2 + 2)) / 2
             rec.update({"GB/s": round(nbytes * n / (ms / 1000.0) / 1e9, 1),
                         "frac_hbm": round(nbytes * n / (ms / 1000.0) / PEAK_HBM, 4)})
-        elif c == "norm":
-            nbytes = M * d * (4 + es)  # fp32 stream in, normalised rows out
+        elif c in ("norm", "norm_parts"):
+            # fp32 stream in, normalised rows out; adding a split output GEMM's two partial
+            # products also reads them and writes the stream back
+            nbytes = M * d * (4 + es) if c == "norm" else M * d * (4 * 4 + es)
             rec.update({"GB/s": round(nbytes * n / (ms / 1000.0) / 1e9, 1),
                         "frac_hbm": round(nbytes * n / (ms / 1000.0) / PEAK_HBM, 4)})
         elif c == "gemm_x":

@@ -433,7 +433,8 @@ enum sgd_kernel_class {
     SGD_K_COND = 8, SGD_K_GEMM_SKIP = 9, SGD_K_GEMM_X = 10, SGD_K_ATTN_X = 11,
     SGD_K_DRIFT = 12, SGD_K_GEMM_CONV = 13, SGD_K_GNORM = 14,
     SGD_K_FOLD = 15, /* a pre-norm that also adds the frozen run ending at its unit */
-    SGD_K_COUNT = 16
+    SGD_K_NORM_PARTS = 16, /* a pre-norm that also adds a split MLP output GEMM's partials */
+    SGD_K_COUNT = 17
 };
 
 /* Start timing every launch of kernel class `kclass` (or -1 to stop): the launcher records

@@ -73,6 +73,15 @@ int sgd_op_residual(int32_t dtype, const void* A, int64_t lda, const void* W, co
                     float* delta, int32_t delta_mode, const float* gate, int64_t gate_ld, int32_t ntok,
                     int32_t M, int32_t N, int32_t K, int32_t tile, void* hip_stream);
 
+/* A residual projection in K ranges (the MLP output GEMM of a long-K unit, whose partial
+ * products the next pre-norm adds to the stream; Sec. 3.1's update h + F(h) taken in parts):
+ * parts + s * part_stride receives the fp32 [M x N] product of A's and W's columns
+ * [s K / ksplit, (s + 1) K / ksplit), plus the bias in range 0, for s < ksplit.  bf16 only;
+ * K a multiple of 64 ksplit, 2 <= ksplit <= 8, part_stride >= M N (a multiple of 4); 256 x 128
+ * block tiles. */
+int sgd_op_linear_split(int32_t dtype, const void* A, const void* W, const float* bias, float* parts,
+                        int64_t part_stride, int32_t M, int32_t N, int32_t K, int32_t ksplit, void* hip_stream);
+
 /* h <- h + delta[0] + ... + delta[r-1] elementwise over n fp32 values (n % 4 == 0), in
  * that order (the frozen-unit update of Sec. 3.1 for a run of r frozen units). */
 int sgd_op_frozen_run(float* h, const float* const* deltas, int32_t r, int64_t n, void* hip_stream);

@@ -10,6 +10,7 @@ from .binding import (  # noqa: F401
     SGD_ARCH, SGD_BF16, SGD_F32, SGD_K, SGD_ROLE, SgdError, lib, lib_path,
     schedule_build, matrix_stats, schedule_from_scores, schedule_from_lifetimes, schedule_from_stats,
     SGD_RULE, SGD_UNIT, Schedule, DeviceModel, Cache, Graph, s_min_default, budget_layer_steps,
-    op_linear, op_attention, op_norm, op_norm_fold, op_frozen_run, op_heads, op_residual, op_adaln_mod,
+    op_linear, op_linear_split, op_attention, op_norm, op_norm_fold, op_frozen_run, op_heads, op_residual,
+    op_adaln_mod,
     op_group_norm_silu, op_conv3x3,
 )

@@ -21,7 +21,7 @@ SGD_RULE = {"scr_frob": 0, "random": 1, "depth": 2, "frob": 3, "spectral": 4, "s
             "frob_srank": 6, "raw_scr": 7}
 SGD_ROLE = {"q": 0, "k": 1, "v": 2, "o": 3, "xq": 4, "xk": 5, "xv": 6, "xo": 7, "w1": 8, "w2": 9, "conv": 10}
 SGD_K = {"norm": 0, "gemm_qkv": 1, "attn": 2, "gemm_o": 3, "gemm_w1": 4, "gemm_w2": 5, "frozen": 6,
-         "state": 7, "cond": 8, "gemm_skip": 9, "gemm_x": 10, "attn_x": 11, "drift": 12, "gemm_conv": 13, "gnorm": 14, "fold": 15}
+         "state": 7, "cond": 8, "gemm_skip": 9, "gemm_x": 10, "attn_x": 11, "drift": 12, "gemm_conv": 13, "gnorm": 14, "fold": 15, "norm_parts": 16}
 ERRORS = {-1: "SGD_E_ARG", -2: "SGD_E_SHAPE", -3: "SGD_E_DTYPE", -4: "SGD_E_BUDGET", -5: "SGD_E_STEP",
           -6: "SGD_E_CACHE", -7: "SGD_E_HIP", -8: "SGD_E_NUMERIC"}
 
@@ -94,7 +94,7 @@ EXPORTS = ["sgd_last_error", "sgd_version", "sgd_s_min_default", "sgd_budget_lay
            "sgd_cache_bytes", "sgd_cache_bind", "sgd_cache_reset", "sgd_cache_destroy", "sgd_denoise_step",
            "sgd_denoise_step_noalloc", "sgd_graph_capture", "sgd_graph_launch", "sgd_graph_destroy",
            "sgd_denoise_step_masked", "sgd_drift_bytes", "sgd_drift_step", "sgd_replay_bytes", "sgd_replay_search",
-           "sgd_profile_begin", "sgd_profile_end", "sgd_op_linear", "sgd_op_attention", "sgd_op_norm", "sgd_op_norm_fold",
+           "sgd_profile_begin", "sgd_profile_end", "sgd_op_linear", "sgd_op_linear_split", "sgd_op_attention", "sgd_op_norm", "sgd_op_norm_fold",
            "sgd_op_frozen_run", "sgd_op_heads", "sgd_op_residual", "sgd_op_adaln_mod", "sgd_op_group_norm_silu",
            "sgd_op_group_norm_scratch_bytes", "sgd_op_conv3x3"]
 
@@ -143,6 +143,7 @@ def lib() -> C.CDLL:
             "sgd_profile_begin": [vp, i32, i32],
             "sgd_profile_end": [vp, C.POINTER(C.c_double), C.POINTER(i64)],
             "sgd_op_linear": [i32, vp, i64, vp, i64, vp, vp, i64, i32, i32, i32, i32, i32, i32, vp],
+            "sgd_op_linear_split": [i32, vp, vp, vp, vp, i64, i32, i32, i32, i32, vp],
             "sgd_op_attention": [i32, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp],
             "sgd_op_norm": [i32, i32, vp, vp, i32, i32, C.c_float, vp, vp, vp, vp, i64, i32, vp],
             "sgd_op_norm_fold": [i32, i32, vp, vp, i32, i32, C.c_float, vp, vp, vp, vp, i64, i32,
@@ -360,6 +361,15 @@ def op_linear(A, W, out, bias=None, act=0, gated=False, tile=0, stream=None) -> 
     N = out.shape[1]
     _check(lib().sgd_op_linear(_dtype_code(A), _p(A), A.stride(0), _p(W), W.stride(0), _p(bias), _p(out),
                                out.stride(0), M, N, K, act, int(gated), tile, C.c_void_p(_stream_ptr(stream))))
+
+
+def op_linear_split(A, W, parts, bias=None, stream=None) -> None:
+    """parts[s] = A[:, K_s] W[:, K_s]^T (+ bias for s = 0) over ksplit = parts.shape[0] K ranges;
+    A [M, K], W [N, K] bf16, parts [ksplit, M, N] fp32, contiguous device tensors."""
+    M, K = A.shape
+    ks, _, N = parts.shape
+    _check(lib().sgd_op_linear_split(_dtype_code(A), _p(A), _p(W), _p(bias), _p(parts), parts.stride(0), M, N, K,
+                                     ks, C.c_void_p(_stream_ptr(stream))))
 
 
 def op_attention(q, k, vt, o, B, H, dh, nq, nk, stream=None) -> None:

@@ -174,6 +174,13 @@ extern "C" int sgd_model_create(const sgd_model_desc* desc, sgd_model** out) {
     m->w_ckv = take(arch_cross(d.arch) ? m->ckv_unit : 0);
     m->w_gn = take(d.arch == SGD_ARCH_SDXL_UNET ? group_norm_scratch_bytes(d.B, d.N, d.groups) : 0);
     m->w_total = o;
+    if (m->dt == 1) {
+        GemmArgs g;
+        g.M = (int)m->M; g.N = d.d; g.K = d.F; g.lda0 = d.F; g.ldb = d.F;
+        const int ks = gemm_bf16_ksplit(g);
+        m->part_bytes = align256(Md * 4);
+        if (ks > 1 && m->w_q + ks * m->part_bytes <= m->w_hid) m->w2_ksplit = ks;
+    }
     o = 0;
     m->c_delta = take((size_t)m->nu * align256(Md * 4));
     m->c_ctx = take(arch_cross(d.arch) ? (size_t)d.L * m->ckv_unit : 0);
@@ -307,6 +314,13 @@ int check_step_shapes(const sgd_model* m) {
     e.rope = 0; e.kind = EP_RESID; g.N = d.d; ok = ok && gemm_shape_ok(m->dt, g, e);
     e.kind = gated ? EP_GATED : EP_ACT; g.N = gated ? 2 * d.F : d.F; ok = ok && gemm_shape_ok(m->dt, g, e);
     e.kind = EP_RESID; g.N = d.d; g.K = d.F; ok = ok && gemm_shape_ok(m->dt, g, e);
+    if (m->w2_ksplit > 1) {
+        GemmArgs gs = g;
+        gs.ksplit = m->w2_ksplit;
+        EpiParams es = e;
+        es.kind = EP_PARTIAL; es.part_stride = (long)(m->part_bytes / 4);
+        ok = ok && gemm_shape_ok(m->dt, gs, es);
+    }
     if (d.arch == SGD_ARCH_SDXL_UNET) {
         g.K = 9 * d.d; g.lda0 = d.d; g.ldb = 9 * d.d; g.conv_side = d.grid; g.conv_c = d.d;
         ok = ok && gemm_shape_ok(m->dt, g, e);
@@ -398,13 +412,16 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
     // a frozen run that ends at an active unit is added by that unit's first norm kernel
     // (same additions, same order) instead of a pass of its own
     std::vector<const float*> fold;
+    bool fold_parts = false;  // fold holds a split MLP output GEMM's partial products
     auto norm = [&](const float* w, const float* b, const float* shift, const float* scale) {
         NormArgs a{h, xb, (int)M, dd, norm_kind, norm_eps, w, b, shift, scale, 6L * dd, N};
         a.nfold = (int)fold.size();
         for (int i = 0; i < a.nfold; ++i) a.fold[i] = fold[i];
-        const int kclass = fold.empty() ? SGD_K_NORM : SGD_K_FOLD;
+        const int kclass = fold.empty() ? SGD_K_NORM : fold_parts ? SGD_K_NORM_PARTS : SGD_K_FOLD;
+        const bool parts = fold_parts;
         fold.clear();
-        S.run(kclass, [&] { return launch_norm(dt, a, S.st); });
+        fold_parts = false;
+        S.run(kclass, [&] { return launch_norm(dt, a, S.st, parts); });
     };
     auto resid = [&](int kclass, const void* A, long lda, int K, const void* W, const void* bias, const float* gate,
                      float* dlt, int dmode, void* hcopy) {
@@ -557,7 +574,27 @@ int run_step(sgd_model* m, void* state, int step, const StepPlan& plan, const sg
             e.F = F;
             S.run(SGD_K_GEMM_W1, [&] { return launch_gemm(dt, g, e, S.st); });
             // the MLP is a block's last branch: the block's output copy goes with it
-            resid(SGD_K_GEMM_W2, hid, F, F, w.w2, w.b2, mod_l ? mod_l + 5 * dd : nullptr, dl, dmode(), out_copy(l));
+            const float* gate2 = mod_l ? mod_l + 5 * dd : nullptr;
+            const int dm2 = dmode();
+            void* copy2 = out_copy(l);
+            // K ranges of the split product go into fp32 partials that the next unit's pre-norm
+            // adds to h in range order: only when that unit computes and reads h first through
+            // its pre-norm, and this step has no gate, cached-update store, copy or drift record
+            const bool next_norm = u + 1 < nu && act[u + 1] && !out_start(u + 1) &&
+                                   !(unet && (nb == 1 || branch_of(u + 1) == BR_RESNET));
+            if (m->w2_ksplit > 1 && !gate2 && !dm2 && !copy2 && !dr && next_norm) {
+                GemmArgs g2;
+                g2.A0 = hid; g2.lda0 = F; g2.B = w.w2; g2.ldb = F; g2.M = (int)M; g2.N = dd; g2.K = F;
+                g2.ksplit = m->w2_ksplit;
+                EpiParams e2;
+                e2.kind = EP_PARTIAL; e2.bias = (const float*)w.b2; e2.h = (float*)(S.ws + m->w_q); e2.d = dd;
+                e2.part_stride = (long)(m->part_bytes / 4);
+                S.run(SGD_K_GEMM_W2, [&] { return launch_gemm(dt, g2, e2, S.st); });
+                for (int s2 = 0; s2 < m->w2_ksplit; ++s2) fold.push_back((const float*)(S.ws + m->w_q + s2 * m->part_bytes));
+                fold_parts = true;
+            } else {
+                resid(SGD_K_GEMM_W2, hid, F, F, w.w2, w.b2, gate2, dl, dm2, copy2);
+            }
         }
         ++u;
     }
@@ -801,6 +838,21 @@ extern "C" int sgd_op_linear(int32_t dtype, const void* A, int64_t lda, const vo
     const int dt = dtype == SGD_BF16 ? 1 : 0;
     if (!gemm_shape_ok(dt, g, e, tile)) return fail(SGD_E_SHAPE, "GEMM shape not supported");
     SGD_HIP_TRY(launch_gemm(dt, g, e, (hipStream_t)hip_stream, tile));
+    return SGD_OK;
+}
+
+extern "C" int sgd_op_linear_split(int32_t dtype, const void* A, const void* W, const float* bias, float* parts,
+                                   int64_t part_stride, int32_t M, int32_t N, int32_t K, int32_t ksplit,
+                                   void* hip_stream) {
+    if (!A || !W || !parts) return fail(SGD_E_ARG, "NULL argument");
+    if (dtype != SGD_BF16) return fail(SGD_E_DTYPE, "split products are bf16 only");
+    if (ksplit < 2 || ksplit > 8) return fail(SGD_E_ARG, "2 <= ksplit <= 8");
+    GemmArgs g;
+    g.A0 = A; g.lda0 = K; g.B = W; g.ldb = K; g.M = M; g.N = N; g.K = K; g.ksplit = ksplit;
+    EpiParams e;
+    e.kind = EP_PARTIAL; e.bias = bias; e.h = parts; e.d = N; e.part_stride = part_stride;
+    if (!gemm_shape_ok(1, g, e)) return fail(SGD_E_SHAPE, "GEMM shape not supported");
+    SGD_HIP_TRY(launch_gemm(1, g, e, (hipStream_t)hip_stream));
     return SGD_OK;
 }
 

@@ -197,6 +197,7 @@ __global__ __launch_bounds__(kF32Waves * 64) void gemm_f32_kernel(GemmArgs g, Ep
 bool gemm_shape_ok(int dtype, const GemmArgs& g, const EpiParams& e, int tile) {
     if (g.M <= 0 || g.N <= 0 || g.K <= 0) return false;
     if (dtype == 1) return gemm_bf16_shape_ok(g, e, tile);
+    if (g.ksplit != 1 || e.kind == EP_PARTIAL) return false;  // split products: bf16 only
     if (g.K % 16 || g.N % 64) return false;
     if (g.A1 && (g.K0 % 16)) return false;
     if (e.kind == EP_HEADS && (e.rope || e.d % 64)) return false;
@@ -205,6 +206,7 @@ bool gemm_shape_ok(int dtype, const GemmArgs& g, const EpiParams& e, int tile) {
 
 hipError_t launch_gemm(int dtype, const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile) {
     if (dtype == 1) return launch_gemm_bf16(g, e, st, tile);
+    if (g.ksplit != 1 || e.kind == EP_PARTIAL) return hipErrorInvalidValue;
     const int nt_m = (g.M + 31) / 32, nt_n = g.N / 32;
     hipLaunchKernelGGL(gemm_f32_kernel, dim3(nt_m * nt_n), dim3(kF32Waves * 64), 0, st, g, e);
     return hipGetLastError();

@@ -116,7 +116,7 @@ __device__ __forceinline__ void with_act(int act, Fn&& f) {
 // row of their own, so the q/k/v, activation and gated epilogues issue no global loads.
 template <class C>
 __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds, const GemmArgs& g,
-                                         const EpiParams& ep, int m0, int tn, int wm, int wn0) {
+                                         const EpiParams& ep, int m0, int tn, int wm, int wn0, int split) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int lrow = lane & 31, lhalf = lane >> 5;
     // Thread t handles rows r0(t) + u * RPT of its columns.  When the items of a row do not
@@ -138,7 +138,7 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
     __syncthreads();  // every wave is done with the stage buffers
     for (int c = tid; c < C::BN; c += C::NT) {
         float b = 0.f;
-        if (ep.bias) {
+        if (ep.bias && split == 0) {
             if (gated) b = ep.bias[c < C::BN / 2 ? tn * (C::BN / 2) + c : ep.F + tn * (C::BN / 2) + c - C::BN / 2];
             else if (n0 + c < g.N) b = ep.bias[rope ? rope_row(n0 + c, ep.dh, vstart) : n0 + c];
         }
@@ -276,12 +276,14 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
                     store_bf16x4((bf16*)ep.out + (long)row * ep.ldo + n, o);
                 }
             });
-        } else if (ep.kind == EP_RESID || ep.kind == EP_SKIP) {
+        } else if (ep.kind == EP_RESID || ep.kind == EP_SKIP || ep.kind == EP_PARTIAL) {
             // EP_RESID: v = (acc + bias) [* gate]; h += v; delta = v | delta += v; hcopy = bf16(h)
             // EP_SKIP:  h = acc + bias [+ cached delta]; hcopy = bf16(h)
+            // EP_PARTIAL: part s = acc (+ bias in range 0), as EP_SKIP into h + s * part_stride
             // The global operands of a group of EB items are loaded before any of its stores.
             const bool resid = ep.kind == EP_RESID;
-            const bool rd_delta = resid ? ep.delta_mode == 2 : ep.delta_mode == 1;
+            const bool rd_delta = resid ? ep.delta_mode == 2 : ep.kind == EP_SKIP && ep.delta_mode == 1;
+            float* const hdst = ep.kind == EP_PARTIAL ? ep.h + (long)split * ep.part_stride : ep.h;
             const f32x4 bb = ld4(sbias + c);
             const int nl = min(n, g.N - 4);  // load column (N % 4 == 0)
 #pragma unroll 1
@@ -320,9 +322,9 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
 #pragma unroll
                         for (int q = 0; q < 4; ++q) {
                             hn[q] = v[q] + bb[q];
-                            if (ep.delta_mode == 1) hn[q] = hn[q] + dv[w][q];
+                            if (rd_delta) hn[q] = hn[q] + dv[w][q];
                         }
-                        *(f32x4*)(ep.h + idx) = f32x4{hn[0], hn[1], hn[2], hn[3]};
+                        *(f32x4*)(hdst + idx) = f32x4{hn[0], hn[1], hn[2], hn[3]};
                     }
                     if (ep.hcopy) store_bf16x4((bf16*)ep.hcopy + idx, hn);
                 }
@@ -400,8 +402,11 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
     const bool gated = ep.kind == EP_GATED;
     const int nt_m = (g.M - g.m_begin + C::BM - 1) / C::BM;
     const int nt_n = (g.N + C::BN - 1) / C::BN;
+    // split K: workgroup b takes K range b / T of tile b % T (T tiles); a range's workgroups
+    // keep the tile order of an unsplit launch
+    const int split = (int)blockIdx.x / (nt_m * nt_n);
     int tm, tn;
-    tile_at(tile_position(blockIdx.x, nt_m * nt_n), nt_m, nt_n, g.band, tm, tn);
+    tile_at(tile_position((int)blockIdx.x - split * nt_m * nt_n, nt_m * nt_n), nt_m, nt_n, g.band, tm, tn);
     const int m0 = g.m_begin + tm * C::BM;
     const int F = g.N / 2;
 
@@ -449,7 +454,8 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
     // buffer (sizes stay below OOB), so the descriptor's range check fails.  The main loop
     // therefore runs whole trips without a branch, the padding tiles add zero products, and
     // the compiler sees the same outstanding loads on every trip.
-    const int KT = g.K / C::BK;
+    const int KT = g.K / g.ksplit / C::BK;
+    const int kbase = split * (g.K / g.ksplit);  // first column of the workgroup's K range
     constexpr unsigned OOB = 0xFFFFFF00u;
     u32x4 vreg[C::RD][PARTS];
     auto gload = [&](int kt, int s, int p) {
@@ -469,9 +475,9 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
         } else if (p < AP) {
             const bool second = g.A1 && k0 >= g.K0;
             vreg[s][p] = __builtin_amdgcn_raw_buffer_load_b128(second ? ra1 : ra0, in ? goff[p] : OOB,
-                                                               in ? (second ? (k0 - g.K0) * 2 : k0 * 2) : 0, 0);
+                                                               in ? (second ? (k0 - g.K0) * 2 : (kbase + k0) * 2) : 0, 0);
         } else {
-            vreg[s][p] = __builtin_amdgcn_raw_buffer_load_b128(rb, in ? goff[p] : OOB, in ? k0 * 2 : 0, 0);
+            vreg[s][p] = __builtin_amdgcn_raw_buffer_load_b128(rb, in ? goff[p] : OOB, in ? (kbase + k0) * 2 : 0, 0);
         }
     };
     // stage and part are compile-time constants at every call
@@ -577,7 +583,7 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
     static_assert(C::KSTEPS % 2 == 0, "fragment ring");
     constexpr int TRIP = C::RD % 2 ? 2 * C::RD : C::RD;  // whole register rings and LDS stage pairs
     for (int kt = 0; kt < KT; kt += TRIP) static_for<TRIP>([&](auto jc) { iter(kt + decltype(jc)::value, jc); });
-    epilogue<C>(acc, lds, g, ep, m0, tn, wm, wn0);
+    epilogue<C>(acc, lds, g, ep, m0, tn, wm, wn0, split);
 }
 
 // --------------------------------------------------------------------------- dispatch
@@ -653,9 +659,25 @@ GemmPlan gemm_bf16_plan(const GemmArgs& g, const EpiParams& e) {
 
 int gemm_bf16_auto_tile(const GemmArgs& g, const EpiParams& e) { return gemm_bf16_plan(g, e).tile; }
 
+// Two K ranges where one round of 128 x 128 tiles is the best unsplit plan of a long-K product
+// and 256 x 128 tiles over half of K still fill at most one round: the larger tiles move ~1.5x
+// fewer operand bytes per FLOP through the load path that bounds the small ones (LLaDA's MLP
+// output GEMM, 1024 x 4096 x 12288: 128 tiles x 2 ranges).  The caller adds the two fp32
+// partial products (EP_PARTIAL) to the stream itself.
+int gemm_bf16_ksplit(const GemmArgs& g) {
+    EpiParams e;
+    e.kind = EP_RESID;
+    e.d = g.N;
+    const GemmPlan p = gemm_bf16_plan(g, e);
+    if (p.tile != 4 || p.tail_tile || g.A1 || g.conv_side > 0 || g.K < 8192 || g.K % 128) return 1;
+    const long tiles = (long)((g.M + 255) / 256) * ((g.N + 127) / 128);
+    return 2 * tiles <= 256 ? 2 : 1;
+}
+
 static bool aligned(const void* p, unsigned a) { return ((uintptr_t)p % a) == 0; }
 
 bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
+    if (tile == 0 && e.kind == EP_PARTIAL) tile = 2;
     if (tile == 0) {
         const GemmPlan p = gemm_bf16_plan(g, e);
         if (p.tail_tile && !gemm_bf16_shape_ok(g, e, p.tail_tile)) return false;
@@ -682,7 +704,11 @@ bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
     if (g.N % 4 || g.lda0 % 8 || (g.A1 && g.lda1 % 8) || g.ldb % 8) return false;  // 16-byte rows
     if (e.kind == EP_GATED && (g.N % s.bn || e.ldo % 4)) return false;
     if (e.kind == EP_ACT && e.ldo % 4) return false;
-    if ((e.kind == EP_RESID || e.kind == EP_SKIP) && (g.N != e.d)) return false;
+    if ((e.kind == EP_RESID || e.kind == EP_SKIP || e.kind == EP_PARTIAL) && (g.N != e.d)) return false;
+    if (g.ksplit < 1 || (g.ksplit > 1) != (e.kind == EP_PARTIAL)) return false;
+    if (e.kind == EP_PARTIAL && (g.A1 || g.conv_side > 0 || g.K % (64 * g.ksplit) || e.gate || e.hcopy ||
+                                 e.delta_mode || (long)e.part_stride < (long)g.M * g.N || e.part_stride % 4))
+        return false;
     if (e.kind == EP_HEADS) {
         if (e.d % 32 || e.dh % 4) return false;  // V^T from whole 32-column MFMA blocks
         if (e.rope && e.dh % 8) return false;  // eight-column pair groups within one head
@@ -698,7 +724,7 @@ static hipError_t run_tile(const GemmArgs& g, const EpiParams& e, hipStream_t st
     const int nt_m = (g.M - g.m_begin + C::BM - 1) / C::BM, nt_n = (g.N + C::BN - 1) / C::BN;
     GemmArgs ga = g;
     ga.band = tile_band(nt_m, nt_n, C::BM, C::BN);
-    hipLaunchKernelGGL((gemm_bf16_kernel<C, CONV>), dim3(nt_m * nt_n), dim3(C::NT), 0, st, ga, e);
+    hipLaunchKernelGGL((gemm_bf16_kernel<C, CONV>), dim3(nt_m * nt_n * g.ksplit), dim3(C::NT), 0, st, ga, e);
     return hipGetLastError();
 }
 
@@ -724,6 +750,7 @@ static hipError_t launch_tile(const GemmArgs& g, const EpiParams& e, hipStream_t
 // rows [0, m_split) with the plan's tile, then the tail rows [m_split, M) with the tail tile;
 // both launches index rows globally (the epilogue's sample / token split needs it)
 hipError_t launch_gemm_bf16(const GemmArgs& g, const EpiParams& e, hipStream_t st, int tile) {
+    if (e.kind == EP_PARTIAL && tile == 0) tile = 2;  // the split product's 256 x 128 tiles
     if (tile != 0) return launch_tile(g, e, st, tile);
     const GemmPlan p = gemm_bf16_plan(g, e);
     if (!p.tail_tile) return launch_tile(g, e, st, p.tile);

@@ -26,9 +26,12 @@ struct GemmArgs {
     // (3 ky + kx) conv_c + c of row (sample, y, x) is input (sample, y + ky - 1, x + kx - 1, c),
     // zero outside the grid.  0: a plain GEMM.
     int conv_side = 0, conv_c = 0;
+    // split K (bf16, EP_PARTIAL): workgroups [s T, (s + 1) T) of the T tiles take columns
+    // [s K / ksplit, (s + 1) K / ksplit) of A and B
+    int ksplit = 1;
 };
 
-enum EpKind { EP_HEADS = 0, EP_ACT = 1, EP_GATED = 2, EP_RESID = 3, EP_SKIP = 4 };
+enum EpKind { EP_HEADS = 0, EP_ACT = 1, EP_GATED = 2, EP_RESID = 3, EP_SKIP = 4, EP_PARTIAL = 5 };
 
 struct EpiParams {
     int kind = EP_ACT;
@@ -45,6 +48,9 @@ struct EpiParams {
     const float* gate = nullptr; long gate_ld = 0; void* hcopy = nullptr;
     // EP_ACT: per-sample additive bias rowbias[sample * rowbias_ld + n] (sample = row / ntok)
     const float* rowbias = nullptr; long rowbias_ld = 0;
+    // EP_PARTIAL: K range s of a split product, fp32, to h + s * part_stride ([M x d]); the bias
+    // goes into range 0 only
+    long part_stride = 0;
 };
 
 // dtype: 0 fp32, 1 bf16.  tile: 0 = pick automatically; 1..kGemmTiles a fixed bf16 block
@@ -58,6 +64,10 @@ int gemm_bf16_auto_tile(const GemmArgs& g, const EpiParams& e);
 // automatic tiling: rows [0, m_split) with `tile`, rows [m_split, M) (if any) with tail_tile
 struct GemmPlan { int tile, m_split, tail_tile; };
 GemmPlan gemm_bf16_plan(const GemmArgs& g, const EpiParams& e);
+// K ranges worth splitting the [M x N] product of `g` into (1: none), when one round of
+// 128 x 128 tiles is the best unsplit plan and the K ranges of larger tiles still fit one
+// round; the split product runs 256 x 128 tiles (EP_PARTIAL)
+int gemm_bf16_ksplit(const GemmArgs& g);
 
 // ---------------------------------------------------------------- attention
 // O[b, i, h*dh + j] = softmax_j'(q_i . k_j' / sqrt(dh)) v_j'  over keys j' < nk.
@@ -81,7 +91,9 @@ struct NormArgs {
     int nfold = 0;
     const float* fold[kMaxRun] = {};
 };
-hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t st);
+// parts: the fold holds the partial products of a split residual GEMM rather than a frozen
+// run's cached updates (the same additions, a kernel of its own name)
+hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t st, bool parts = false);
 // y = SiLU(GroupNorm(x) w + b) in bf16 for x [B, N, C] fp32 (in_bf16 = 0) or bf16; groups of
 // C / groups consecutive channels (a multiple of 4) over all N positions of a sample
 struct GroupNormArgs {

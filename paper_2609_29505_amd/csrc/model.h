@@ -20,6 +20,11 @@ struct sgd_model {
     // workspace layout
     size_t w_h, w_xb, w_q, w_k, w_vt, w_ob, w_hid, w_siluc, w_mod, w_hb, w_skip, w_ckv, w_gn, w_total;
     size_t mod_slot = 0;  // bytes of one block's modulation in the workspace
+    // MLP output GEMM in K ranges (1: unsplit); partial s at workspace offset w_q + s * part_bytes,
+    // in the q / k / V^T / attention-output buffers, which no kernel reads between that GEMM and
+    // the next unit's QKV GEMM
+    int w2_ksplit = 1;
+    size_t part_bytes = 0;
     // cache layout
     size_t c_delta, c_ctx, c_total;
     size_t ckv_unit;  // bytes of one unit's context K and V^T

@@ -386,6 +386,36 @@ def test_residual(P, dtype, tile, M, N, K, gated_rows, mode):
         assert np.array_equal(host(td), d0.astype(np.float64))
 
 
+@pytest.mark.parametrize("M,N,K,ks", [(1024, 4096, 12288, 2), (200, 256, 8192, 2), (300, 520, 1024, 4),
+                                      (64, 128, 512, 8)])
+def test_linear_split(P, M, N, K, ks):
+    """K ranges of a residual projection (the split MLP output GEMM): part s is the exact-product
+    fp32 sum over columns [s K / ks, (s + 1) K / ks), the bias in part 0 only; the LLaDA-8B
+    shape, ragged rows and columns, four and eight ranges."""
+    rng = np.random.default_rng(M + N + K + ks)
+    A = synth.store(rng.standard_normal((M, K)), "bf16")
+    W = synth.store(rng.standard_normal((N, K)) / np.sqrt(K), "bf16")
+    b = synth.representable(0.1 * rng.standard_normal(N), "f32")
+    parts = empty((ks, M, N), "f32")
+    P.op_linear_split(dev(A), dev(W), parts, bias=dev(b))
+    got = host(parts)
+    a64, w64 = decode(A, "bf16"), decode(W, "bf16")
+    kr = K // ks
+    for s in range(ks):
+        ref = a64[:, s * kr:(s + 1) * kr] @ w64[:, s * kr:(s + 1) * kr].T + (b if s == 0 else 0.0)
+        assert relmax(got[s], ref) < 1e-5, s
+
+
+def test_linear_split_refuses_bad_ranges(P):
+    import torch
+    A = torch.zeros((64, 640), dtype=torch.bfloat16, device="cuda")
+    W = torch.zeros((128, 640), dtype=torch.bfloat16, device="cuda")
+    for ks in (1, 3, 9):  # one range, K not a multiple of 64 ks, too many ranges
+        parts = torch.zeros((ks, 64, 128), dtype=torch.float32, device="cuda")
+        with pytest.raises(P.SgdError):
+            P.op_linear_split(A, W, parts)
+
+
 @pytest.mark.parametrize("rope", [False, True])
 @pytest.mark.parametrize("tile", TILES)
 def test_heads_kv_only(P, tile, rope):
