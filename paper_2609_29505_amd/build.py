@@ -33,12 +33,31 @@ FLAGS = [
 ]
 
 
+def _spills(remarks: str) -> list:
+    """Kernels whose resource-usage remarks report spilled registers."""
+    out, name = [], None
+    for line in remarks.splitlines():
+        if "Function Name:" in line:
+            name = line.split("Function Name:", 1)[1].split("[")[0].strip()
+        elif "Spill:" in line:
+            n = line.split("Spill:", 1)[1].split("[")[0].strip()
+            if n.isdigit() and int(n) > 0:
+                out.append(f"{name}: {line.split('remark:', 1)[-1].split('[')[0].strip()}")
+    return out
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, src + ".o")
     cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    if src.endswith(".hip"):
+        cmd.append("-Rpass-analysis=kernel-resource-usage")
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
+    # every kernel keeps its registers: a spill goes through scratch memory in the hot loops
+    spills = _spills(r.stderr)
+    if spills:
+        raise RuntimeError(f"register spills in {src}:\n" + "\n".join(spills))
     return obj
 
 

@@ -392,7 +392,7 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[C::TM][C::TN], char* lds,
 // the period's MFMAs (part p after MFMA slot p * SLOTS / PARTS), so neither the texture
 // unit nor the LDS sees a burst and both SIMD waves keep issuing MFMAs.
 
-template <class C, bool CONV>
+template <class C, bool CONV, bool SPLIT>
 __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, EpiParams ep) {
     static_assert(C::STAGES == 2, "two LDS stages plus the register stage");
     __shared__ __attribute__((aligned(1024))) char lds[C::LDS_BYTES];
@@ -404,7 +404,7 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
     const int nt_n = (g.N + C::BN - 1) / C::BN;
     // split K: workgroup b takes K range b / T of tile b % T (T tiles); a range's workgroups
     // keep the tile order of an unsplit launch
-    const int split = (int)blockIdx.x / (nt_m * nt_n);
+    const int split = SPLIT ? (int)blockIdx.x / (nt_m * nt_n) : 0;
     int tm, tn;
     tile_at(tile_position((int)blockIdx.x - split * nt_m * nt_n, nt_m * nt_n), nt_m, nt_n, g.band, tm, tn);
     const int m0 = g.m_begin + tm * C::BM;
@@ -454,8 +454,8 @@ __global__ __launch_bounds__(C::NT, C::OCC) void gemm_bf16_kernel(GemmArgs g, Ep
     // buffer (sizes stay below OOB), so the descriptor's range check fails.  The main loop
     // therefore runs whole trips without a branch, the padding tiles add zero products, and
     // the compiler sees the same outstanding loads on every trip.
-    const int KT = g.K / g.ksplit / C::BK;
-    const int kbase = split * (g.K / g.ksplit);  // first column of the workgroup's K range
+    const int KT = (SPLIT ? g.K / g.ksplit : g.K) / C::BK;
+    const int kbase = SPLIT ? split * (g.K / g.ksplit) : 0;  // first column of the workgroup's K range
     constexpr unsigned OOB = 0xFFFFFF00u;
     u32x4 vreg[C::RD][PARTS];
     auto gload = [&](int kt, int s, int p) {
@@ -705,7 +705,7 @@ bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
     if (e.kind == EP_GATED && (g.N % s.bn || e.ldo % 4)) return false;
     if (e.kind == EP_ACT && e.ldo % 4) return false;
     if ((e.kind == EP_RESID || e.kind == EP_SKIP || e.kind == EP_PARTIAL) && (g.N != e.d)) return false;
-    if (g.ksplit < 1 || (g.ksplit > 1) != (e.kind == EP_PARTIAL)) return false;
+    if (g.ksplit < 1 || (g.ksplit > 1) != (e.kind == EP_PARTIAL) || (g.ksplit > 1 && tile != 2)) return false;
     if (e.kind == EP_PARTIAL && (g.A1 || g.conv_side > 0 || g.K % (64 * g.ksplit) || e.gate || e.hcopy ||
                                  e.delta_mode || (long)e.part_stride < (long)g.M * g.N || e.part_stride % 4))
         return false;
@@ -719,12 +719,13 @@ bool gemm_bf16_shape_ok(const GemmArgs& g, const EpiParams& e, int tile) {
     return true;
 }
 
-template <class C, bool CONV = false>
+template <class C, bool CONV = false, bool SPLIT = false>
 static hipError_t run_tile(const GemmArgs& g, const EpiParams& e, hipStream_t st) {
     const int nt_m = (g.M - g.m_begin + C::BM - 1) / C::BM, nt_n = (g.N + C::BN - 1) / C::BN;
     GemmArgs ga = g;
     ga.band = tile_band(nt_m, nt_n, C::BM, C::BN);
-    hipLaunchKernelGGL((gemm_bf16_kernel<C, CONV>), dim3(nt_m * nt_n * g.ksplit), dim3(C::NT), 0, st, ga, e);
+    hipLaunchKernelGGL((gemm_bf16_kernel<C, CONV, SPLIT>), dim3(nt_m * nt_n * (SPLIT ? g.ksplit : 1)), dim3(C::NT), 0,
+                       st, ga, e);
     return hipGetLastError();
 }
 
@@ -736,6 +737,10 @@ static hipError_t launch_tile(const GemmArgs& g, const EpiParams& e, hipStream_t
             case 5: return run_tile<T256x192, true>(g, e, st);
             default: return hipErrorInvalidValue;
         }
+    }
+    if (g.ksplit > 1) {  // K ranges (EP_PARTIAL): the 256 x 128 tiles only
+        if (tile != 2) return hipErrorInvalidValue;
+        return run_tile<T256x128, false, true>(g, e, st);
     }
     switch (tile) {
         case 1: return run_tile<T256x256>(g, e, st);

@@ -178,3 +178,19 @@ def test_trace_report_recognises_folding_pre_norms():
     act = np.arange(1, cfg.T + 1)[:, None] <= np.asarray(lifetimes["50"])[None, :]
     n = sum(len(bench.frozen_launches(cfg, act[j % cfg.T])[1]) for j in range(3 * cfg.T))
     assert n > 0 and out[0][1] == n
+
+
+def test_build_rejects_register_spills():
+    """The build reads hipcc's resource-usage remarks and names every kernel that spills."""
+    from paper_2609_29505_amd import build
+    remarks = "\n".join([
+        "a.hip:1:1: remark: Function Name: _ZN3sgd1kEv [-Rpass-analysis=kernel-resource-usage]",
+        "a.hip:1:1: remark:     VGPRs: 256 [-Rpass-analysis=kernel-resource-usage]",
+        "a.hip:1:1: remark:     SGPRs Spill: 0 [-Rpass-analysis=kernel-resource-usage]",
+        "a.hip:1:1: remark:     VGPRs Spill: 5 [-Rpass-analysis=kernel-resource-usage]",
+        "a.hip:9:1: remark: Function Name: _ZN3sgd1jEv [-Rpass-analysis=kernel-resource-usage]",
+        "a.hip:9:1: remark:     SGPRs Spill: 0 [-Rpass-analysis=kernel-resource-usage]",
+        "a.hip:9:1: remark:     VGPRs Spill: 0 [-Rpass-analysis=kernel-resource-usage]",
+    ])
+    assert build._spills(remarks) == ["_ZN3sgd1kEv: VGPRs Spill: 5"]
+    assert build._spills(remarks.replace("Spill: 5", "Spill: 0")) == []
