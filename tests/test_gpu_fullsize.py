@@ -97,6 +97,52 @@ def test_fullsize_step_parity(P, name):
     dm.close()
 
 
+def test_fullsize_late_step_real_schedule(P):
+    """The LLaDA-8B-shaped workload at step 40 of its 35 % schedule (the oracle's lifetimes from
+    the stored full-size scores): four active units, frozen runs of 16, 3, 6 and 1 units folded
+    into the next pre-norm and a run of 2 at the end of the stack on its own.  The GPU runs steps
+    1-39 itself; step 40 from its own state and cached updates against the oracle's step 40 on
+    the same state and the same cached updates (2e-2 on the state and on the network output,
+    recovered from the sampler update on the rows it owns)."""
+    import torch
+    name = "llada"
+    cfg, w, x = load(name)
+    T, L = cfg.T, cfg.L
+    pct, s0 = min(cfg.budgets), 40
+    _, graw = load_fullsize_golden(name)
+    bs = osch.lifetimes_budget(osp.normalise(graw), T, osch.budget_layer_steps(pct, L, T), osch.s_min_default(T))
+    S = np.asarray(bs.lifetimes)
+    mask = osch.active_mask(S, T)
+    assert 2 <= int(mask[s0 - 1].sum()) <= L // 4  # mostly frozen at this step
+    dm = P.DeviceModel(cfg, w, x)
+    sched = P.schedule_from_lifetimes(S, T)
+    assert np.array_equal(sched.lifetimes, S)
+    cache = P.Cache(dm)
+    cache.reset()
+    z = torch.from_numpy(x["z"].copy()).cuda()
+    progress(f"{name}: GPU steps 1-{s0 - 1} of the {pct} % schedule")
+    for s in range(1, s0):
+        dm.step(z, s, sched, cache)
+    torch.cuda.synchronize()
+    zin = z.cpu().numpy().astype(np.float64)
+    slot = (cfg.M * cfg.d * 4 + 255) // 256 * 256
+    deltas = {u: cache.buf[u * slot: u * slot + cfg.M * cfg.d * 4].view(torch.float32).cpu().numpy()
+              .astype(np.float64).reshape(zin.shape) for u in range(L) if not mask[s0 - 1][u]}
+    dm.step(z, s0, sched, cache)
+    g = z.cpu().numpy().astype(np.float64)
+    dm.close()
+    progress(f"{name}: oracle step {s0} ({int(mask[s0 - 1].sum())} of {L} units active)")
+    m = om.Model(cfg, w, x, lazy=True)
+    eps = om.denoise_step(m, zin, s0, mask[s0 - 1], deltas)
+    ref = om.sampler_update(cfg, zin, eps, s0)
+    e = rel_err(g, ref)
+    # the network output itself, recovered from the update z - eps / T on the sampler's rows
+    r0, r1 = cfg.update_rows
+    e_eps = rel_err(T * (zin[:, r0:r1] - g[:, r0:r1]), eps[:, r0:r1])
+    progress(f"{name}: step {s0} error {e:.3e}, network output error {e_eps:.3e}")
+    assert e <= TOL[cfg.dtype] and e_eps <= TOL[cfg.dtype], (e, e_eps)
+
+
 @pytest.mark.parametrize("name", FULL)
 def test_fullsize_schedule(P, name):
     """The GPU's scores and schedules at full size against the oracle's stored statistics
