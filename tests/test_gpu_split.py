@@ -60,3 +60,33 @@ def test_split_output_gemm_all_active_is_unscheduled(P, wide):
     dm.close()
     for za, zb in zip(a, b):
         assert np.array_equal(za, zb)
+
+
+def test_split_output_gemm_graph_replays_equal_eager(P, wide):
+    """The split product and its partial-adding pre-norm captured in a whole-trajectory HIP
+    graph: two replays, with eager work between them, equal the eager trajectory bit for bit."""
+    import torch
+    cfg, w, x = wide
+    dm = P.DeviceModel(cfg, w, x)
+    S = np.array([cfg.T, 2, cfg.T, cfg.T])
+    sched = P.schedule_from_lifetimes(S, cfg.T)
+    eager = gpu_trajectory(dm, cfg, x, sched)[-1]
+    stream = torch.cuda.Stream()
+    z0 = torch.from_numpy(x["z"].copy()).cuda()
+    z = torch.empty_like(z0)
+    cache = P.Cache(dm)
+    with torch.cuda.stream(stream):
+        g = dm.capture(z, sched, cache, stream)
+    other = torch.from_numpy(x["z"].copy()).cuda()
+    for rep in range(2):
+        with torch.cuda.stream(stream):
+            z.copy_(z0)
+            g.launch(stream)
+        stream.synchronize()
+        assert np.array_equal(z.cpu().numpy().astype(np.float64), eager), rep
+        c2 = P.Cache(dm)
+        c2.reset()
+        dm.step(other, 1, sched, c2)
+        torch.cuda.synchronize()
+    g.close()
+    dm.close()
