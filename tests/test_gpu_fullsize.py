@@ -27,10 +27,11 @@ FULL = ["tiny", "dit", "uvit", "sdxl", "llada", "sdxl_unet"]
 
 
 def progress(msg):
-    """Progress lines for long full-size cases (the runner may watch gpurun_out/)."""
-    d = os.path.join(os.environ.get("GRAFT_REPO_ROOT", ""), "gpurun_out")
+    """Progress lines for long full-size cases, also appended to a log file in the directory
+    SGD_PROGRESS_DIR names (for runners that watch files rather than captured output)."""
+    d = os.environ.get("SGD_PROGRESS_DIR", "")
     line = f"[{time.strftime('%H:%M:%S')}] {msg}\n"
-    if os.path.isdir(d):
+    if d and os.path.isdir(d):
         with open(os.path.join(d, "fullsize_progress.log"), "a") as f:
             f.write(line)
     print(line, end="", flush=True)
