@@ -9,8 +9,8 @@ events.  --cold cycles through enough distinct weight matrices (>= 1 GiB in all)
 launch streams its weights from HBM, as the step does (each unit has its own weights); by
 default one weight matrix is reused and stays in the 256 MB Infinity Cache.  --copy-mib appends a device-to-device copy of that many MiB, a plain copy of known
 size that calibrates the FETCH_SIZE / WRITE_SIZE counters of a rocprofv3 --pmc pass run over
-the same command.  Kernels: gemm_qkv, gemm_o, gemm_w1, gemm_w2, attn, frozen (a run of
---frozen-r cached updates).
+the same command.  Kernels: gemm_qkv, gemm_o, gemm_w1, gemm_w2, gemm_w2_split (two K ranges
+of fp32 partials), attn, frozen (a run of --frozen-r cached updates).
 """
 from __future__ import annotations
 
@@ -83,6 +83,12 @@ def main() -> int:
         A, W, h = rnd(M, kd), weights(d, kd, scale=kd ** -0.5), torch.randn(M, d, device=dev)
         fn = lambda: P.op_residual(A, W(), h)  # noqa: E731
         flop = 2.0 * M * d * kd
+    elif k == "gemm_w2_split":
+        # the MLP output GEMM in two K ranges of fp32 partial products (the step's split path)
+        A, W = rnd(M, F), weights(d, F, scale=F ** -0.5)
+        parts = torch.empty(2, M, d, device=dev)
+        fn = lambda: P.op_linear_split(A, W(), parts)  # noqa: E731
+        flop = 2.0 * M * d * F
     elif k == "attn":
         q = rnd(B * H, np_, dh)
         kk = rnd(B * H, np_, dh)
