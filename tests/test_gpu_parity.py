@@ -224,3 +224,25 @@ def test_step_errors(P):
     assert e.value.code == -5
     torch.cuda.synchronize()
     dm.close()
+
+
+@pytest.mark.parametrize("name,over", [("tiny_ragged", dict(L=1, T=1)), ("tiny_ragged", dict(B=1, N=1, L=2, T=4)),
+                                       ("llada_mini", dict(L=1, T=3)), ("dit_mini", dict(B=1, L=1, T=2)),
+                                       ("dit_mini", dict(B=3, N=1, L=2, T=2)), ("sdxl_mini", dict(B=1, L=1, T=2)),
+                                       ("uvit_mini", dict(B=1, L=3, T=2)), ("sdxl_unet_mini", dict(B=1, L=1, T=2))])
+def test_degenerate_sizes(P, name, over):
+    """One unit (U-ViT: its smallest stack, one in-block, the mid block and one out-block), one
+    step, one sample, one token per sample (a single key and a one-row GEMM tile); the only unit,
+    or every odd-numbered one, frozen after step 1: teacher-forced against the oracle at every
+    step, at the per-step bar of the workload's dtype."""
+    cfg = synth.get_config(name, **over)
+    w, x = synth.model_weights(cfg), synth.inputs(cfg)
+    S = np.array([cfg.T if l % 2 == 0 and cfg.L > 1 else (1 if cfg.T > 1 else cfg.T) for l in range(cfg.L)])
+    mask = osch.active_mask(S, cfg.T)
+    ref = oracle_trajectory(cfg, w, x, mask)
+    dm = P.DeviceModel(cfg, w, x)
+    got = gpu_teacher_forced(dm, cfg, ref.z, x["z"], P.schedule_from_lifetimes(S, cfg.T))
+    errs = [rel_err(g, r) for g, r in zip(got, ref.z)]
+    print(name, over, "per-step error", ["%.2e" % e for e in errs])
+    assert max(errs) <= TOL[cfg.dtype], errs
+    dm.close()
