@@ -207,3 +207,36 @@ def test_model_units_by_granularity(arch, nb):
     assert sizes[1] - sizes[0] == (nb - 1) * L * slot
     rc, _ = create(2)
     assert rc == -1 and b"granularity" in lib.sgd_last_error()
+
+
+@pytest.mark.parametrize("field,value,code,words", [
+    ("B", 0, -2, b">= 1"), ("N", 0, -2, b">= 1"), ("L", 0, -2, b">= 1"), ("T", 0, -2, b">= 1"),
+    ("d", 384, -2, b"H * head_dim"), ("head_dim", 96, -2, b"head_dim"), ("F", 100, -2, b"F must"),
+    ("dtype", 7, -3, b"dtype"), ("granularity", -1, -1, b"granularity")])
+def test_model_create_refuses_bad_shapes(field, value, code, words):
+    """Empty and unsupported model shapes are refused on the host with their error code and a
+    message naming the constraint, before any device memory is touched (stand-in pointers)."""
+    import ctypes as C
+    lib = _lib_or_skip()
+    b = P.binding
+    L, B, N, d, H, dh, F = 2, 1, 64, 256, 2, 128, 512
+    fake = 1 << 20
+    cw = (b.sgd_unit_weights * L)()
+    for l in range(L):
+        for name in b._W_FIELDS:
+            setattr(cw[l], name, fake)
+    dsc = b.sgd_model_desc()
+    dsc.arch, dsc.dtype = b.SGD_ARCH["tiny"], b.SGD_BF16
+    dsc.B, dsc.N, dsc.d, dsc.H, dsc.head_dim, dsc.F, dsc.L, dsc.T = B, N, d, H, dh, F, L, 10
+    dsc.update_row_begin, dsc.update_row_end = 0, N
+    dsc.class_emb, dsc.ctx = fake, fake
+    dsc.units = C.cast(cw, C.POINTER(b.sgd_unit_weights))
+    h = C.c_void_p()
+    assert lib.sgd_model_create(C.byref(dsc), C.byref(h)) == 0, lib.sgd_last_error()
+    assert lib.sgd_model_destroy(h) == 0
+    setattr(dsc, field, value)
+    if field == "head_dim":  # keep d = H head_dim a multiple of 128 so the head-dim check is reached
+        dsc.H, dsc.d = 4, 4 * value
+    rc = lib.sgd_model_create(C.byref(dsc), C.byref(h))
+    assert rc == code, (field, rc, lib.sgd_last_error())
+    assert words in lib.sgd_last_error(), lib.sgd_last_error()
