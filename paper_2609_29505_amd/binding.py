@@ -441,12 +441,17 @@ def op_frozen_run(h, deltas, stream=None) -> None:
 # ------------------------------------------------------------------ model
 
 def _to_device(arr: np.ndarray, dtype: str):
-    """numpy storage array -> device tensor (uint16 bit patterns are reinterpreted as bf16)."""
+    """numpy storage array -> device tensor (uint16 bit patterns are reinterpreted as bf16).
+    The host tensor is only read (copied to the device), so read-only arrays are used as they are."""
+    import warnings
+
     import torch
-    if arr.dtype == np.uint16:
-        t = torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16)
-    else:
-        t = torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32))
+    with warnings.catch_warnings():
+        warnings.filterwarnings("ignore", message="The given NumPy array is not writable")
+        if arr.dtype == np.uint16:
+            t = torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16)
+        else:
+            t = torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32))
     return t.to("cuda", non_blocking=False)
 
 
