@@ -205,7 +205,9 @@ def test_attention_rising_scores(P, B, H, nq, nk, dh):
                                       # many rows: one wave per row, ragged last workgroup
                                       (0, 256, 4099), (1, 1280, 4099), (2, 1152, 4099),
                                       # many rows of 128-lane multiples: two waves per row
-                                      (1, 1024, 4099), (0, 512, 4097), (2, 2048, 4099)])
+                                      (1, 1024, 4099), (0, 512, 4097), (2, 2048, 4099),
+                                      # many rows too wide for two rows per thread group
+                                      (0, 8192, 4100)])
 def test_norm(P, dtype, kind, d, M):
     rng = np.random.default_rng(kind * 100 + d + M)
     ntok = 35 if M == 70 else 4099
