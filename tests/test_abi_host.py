@@ -212,7 +212,8 @@ def test_model_units_by_granularity(arch, nb):
 @pytest.mark.parametrize("field,value,code,words", [
     ("B", 0, -2, b">= 1"), ("N", 0, -2, b">= 1"), ("L", 0, -2, b">= 1"), ("T", 0, -2, b">= 1"),
     ("d", 384, -2, b"H * head_dim"), ("head_dim", 96, -2, b"head_dim"), ("F", 100, -2, b"F must"),
-    ("dtype", 7, -3, b"dtype"), ("granularity", -1, -1, b"granularity")])
+    ("dtype", 7, -3, b"dtype"), ("granularity", -1, -1, b"granularity"),
+    ("N", 1 << 23, -2, b"2^31")])  # B N d = 2^31: past the largest stream the kernels index
 def test_model_create_refuses_bad_shapes(field, value, code, words):
     """Empty and unsupported model shapes are refused on the host with their error code and a
     message naming the constraint, before any device memory is touched (stand-in pointers)."""
